@@ -1,0 +1,229 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched cGRU-attention scoring step on one MI355X.
+
+One step = one nmt_score_batch call over the whole batch: the forward step
+(H_i, P_i) <- NMT(H_{i-1}, E_i) of the paper's Section 5.1 for B
+hypothesis rows, returning log p of one requested word per row over the full
+target vocabulary plus the new states.  The default workload is the en->ru
+shape: V = 100,000, E = 500, H = A = 1024, B = 2,000 rows over 20 source
+sentences of length U{10..50} (padded to 50), fp32, seeded synthetic weights.
+
+Prints ONE JSON line.  ``value`` is scored hypothesis-words per second
+(rows / step time) with every input already resident in device memory.
+``roofline`` reports the vocabulary-projection kernel (75% of the step's
+flops) against the fp32 MFMA peak, from its own HIP-event duration measured
+inside the timed region.  ``cpu_baseline`` times the fp64 oracle on a
+bounded row sample on the host cores.
+
+  python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+  python bench.py --copy-probe BYTES   # plain copy kernel for counter calibration
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scored hypothesis-words/sec at V=100k, H=1024, B=2000; MFMA util %"
+UNIT = "scored hypothesis-words/s"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCES = ("paper_1605_04809_amd/csrc/kernels.hip", "paper_1605_04809_amd/csrc/device.hpp",
+                  "paper_1605_04809_amd/csrc/internal.hpp")
+TRAFFIC_FILE = "profiles/vocab_lse_{workload}_traffic.txt"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def step_flops(cfg, src_len, sent_id):
+    """Algorithmic flops of one step (padding and never-stored logits excluded)."""
+    E, H, A, C, V = cfg.E, cfg.H, cfg.A, cfg.C, cfg.V
+    L = src_len[sent_id].astype(np.float64)
+    per_row = (2 * (E + H) * 3 * H          # first GRU
+               + 2 * H * A                  # attention query
+               + 2 * (H + C) * 3 * H        # second GRU
+               + 2 * (H + E + C) * E        # readout
+               + 2 * E * V)                 # vocabulary projection
+    attention = float(np.sum(3 * L * A + 2 * L * C))
+    vocab = 2.0 * E * V * len(sent_id)
+    return per_row * len(sent_id) + attention, vocab
+
+
+def read_traffic(workload: str):
+    """HBM bytes per vocab-kernel launch from the committed counter summary,
+    or None if it is missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, TRAFFIC_FILE.format(workload=workload))
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, min_seconds=10.0, max_seconds=30.0):
+    """The fp64 oracle as it stands, on a bounded sample of rows of the workload."""
+    import oracle
+    m = oracle.Model.from_workload(wl)
+    ctx, pctx, _ = oracle.encode(m, wl.src_ids, wl.src_len)   # source initialisation, not timed
+    B = len(wl.y_prev)
+    threads = oracle.num_threads()
+    done, elapsed, chunk, start_row = 0, 0.0, max(threads, 8), 0
+    while elapsed < min_seconds and done < B:
+        rows = np.arange(start_row, min(start_row + chunk, B))
+        t0 = time.perf_counter()
+        oracle.score_batch(m, ctx, pctx, wl.src_len, wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows],
+                           wl.req[rows], intermediates=False)
+        dt = time.perf_counter() - t0
+        elapsed += dt
+        done += len(rows)
+        start_row += len(rows)
+        rate = len(rows) / dt
+        chunk = int(max(threads, min(B - start_row, rate * min(min_seconds - elapsed, max_seconds - elapsed))))
+        if chunk <= 0:
+            break
+    return {"value": done / elapsed, "unit": UNIT, "cores": threads, "kind": "oracle",
+            "sample": f"first {done} of {B} rows of the same workload, one step each, fp64, "
+                      f"{elapsed:.1f} s wall; source encoding excluded"}
+
+
+def copy_probe(nbytes: int, reps: int = 5):
+    import torch
+    n = nbytes // 4
+    x = torch.ones(n, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n * 4, "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="enru_b2000")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS, make_workload
+
+    cfg = CONFIGS[args.config]
+    if cfg.phrase_max:
+        raise SystemExit("the phrase workload is a parity case, not a bench line")
+    wl = make_workload(cfg)
+    B = cfg.B
+    model = nb.Model.from_workload(wl)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    src = nb.nmt_encode(model, cu(wl.src_ids), wl.src_len)
+    s_prev, y_prev, sent_id, req = cu(wl.s_prev), cu(wl.y_prev), cu(wl.sent_id), cu(wl.req)
+    logp = torch.empty(B, device="cuda")
+    logZ = torch.empty(B, device="cuda")
+    s_new = torch.empty((B, cfg.H), device="cuda")
+    ws = torch.empty(nb.nmt_score_workspace_bytes(model, B), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        nb.nmt_score_batch(model, src, s_prev, y_prev, sent_id, req, logp, s_new, logZ, workspace=ws,
+                           stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if nb.nmt_stream_status(model) != nb.NMT_OK:
+        raise SystemExit("device reported an id error during warm-up")
+
+    nb.nmt_profile_begin(model, args.steps)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    phases = nb.nmt_profile_end(model, stream)
+    assert phases["steps"] == args.steps
+    if not bool(torch.isfinite(logp).all()):
+        raise SystemExit("non-finite log-probabilities")
+
+    ms_step = ms_total / args.steps
+    total_flops, vocab_flops = step_flops(cfg, wl.src_len, wl.sent_id)
+    peak = PEAK_TFLOPS[cfg.wtype]
+    vocab_ms = phases["vocab"] / args.steps
+    achieved = vocab_flops / (vocab_ms * 1e-3) / 1e12
+    traffic = read_traffic(cfg.name)
+    out = {
+        "metric": METRIC,
+        "value": B / (ms_step * 1e-3),
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.wtype,
+        "data": "synthetic: seeded N(0, 0.01) random-init weights of the paper's shape, no trained model",
+        "config": {"workload": cfg.name, "V": cfg.V, "E": cfg.E, "H": cfg.H, "A": cfg.A, "B": B,
+                   "S": cfg.S, "src_len": f"U{{{cfg.len_lo}..{cfg.len_hi}}}", "Tpad": cfg.Tpad,
+                   "weights": cfg.wtype},
+        "roofline": {"bound": "mfma", "kernel": "k_vocab_lse", "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": traffic, "algorithmic_flops_per_launch": vocab_flops,
+                     "avg_launch_ms": vocab_ms},
+        "mfma_util_vocab_pct": 100.0 * achieved / peak,
+        "step_tflops": total_flops / (ms_step * 1e-3) / 1e12,
+        "mfma_util_step_pct": 100.0 * total_flops / (ms_step * 1e-3) / 1e12 / peak,
+        "phase_ms": {k: v / args.steps for k, v in phases.items() if k != "steps"},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    src.close()
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

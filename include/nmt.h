@@ -1,0 +1,185 @@
+/*
+ * nmt.h -- C-ABI of libnmt: batched querying of an attentional
+ * conditional-GRU translation model from phrase-based decoding, on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The paper (Section 5.1, "Scoring hypotheses and their expansions";
+ * Figure 2, procedure ScoreBatch) assumes the model has been initialised
+ * with the source sentence, so that the source context is available at all
+ * times, and then performs one forward step per tree depth:
+ * (H_i, P_i) <- NMT(H_{i-1}, E_i), where the rows of the state matrix
+ * H_{i-1} and of the embedding matrix E_i correspond one to one.  This
+ * library exposes exactly those two operations:
+ *
+ *   nmt_encode       -- source initialisation: bidirectional GRU
+ *                       annotations, attention keys and initial states.
+ *   nmt_score_batch  -- one batched decoder step: new states H_i and the
+ *                       normalised log-probability (natural log, full
+ *                       vocabulary) of one requested next word per row.
+ *                       The probability matrix P_i itself is never
+ *                       materialised; only the requested entries and the
+ *                       per-row log normaliser leave the device.
+ *
+ * Model (the DL4MT / Nematus variant of Bahdanau et al. named in Sections 1
+ * and 3; C = 2H, gate blocks ordered [r | z | n], matrices in x.W
+ * orientation [input dim x output dim], row-major):
+ *   GRU(u, h; W, U, bi, bs):  r = sig(uW_r + bi_r + hU_r + bs_r)
+ *                             z = sig(uW_z + bi_z + hU_z + bs_z)
+ *                             n = tanh(uW_n + bi_n + r * (hU_n + bs_n))
+ *                             h' = z*h + (1-z)*n
+ *   encoder:  annotations ctx_i = [fwd GRU_i ; bwd GRU_i] (zero past the
+ *             length), keys pctx_i = ctx_i att_Wc + att_b,
+ *             s0 = tanh(mean_{i<L} ctx_i init_W + init_b)
+ *   step:     x = emb_tgt[y_prev] (zero for y_prev = -1)
+ *             s1 = GRU(x, s_prev; g1_W, g1_U, bi = g1_b, bs = 0)
+ *             alpha = softmax_{i<L}( att_v . tanh(pctx_i + s1 att_Wq) )
+ *             c = sum_i alpha_i ctx_i
+ *             s_new = GRU(c, s1; g2_Wc, g2_U, bi = 0, bs = g2_b)
+ *             t = tanh(s_new ro_Ws + x ro_Wy + c ro_Wc + ro_b)
+ *             logZ = log sum_v exp(t out_W[:,v] + out_b[v])
+ *             logp = t out_W[:,req] + out_b[req] - logZ
+ *
+ * Conventions for every call:
+ *   - "d_" pointers are device memory owned by the caller (for example
+ *     torch tensors passed by data_ptr()); "h_" pointers are host memory.
+ *     fp32 device arrays must be 16-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls that
+ *     take a stream enqueue work on it and return without waiting; host
+ *     arguments are validated synchronously before anything is enqueued.
+ *   - A non-OK status leaves nothing enqueued; nmt_last_error() returns a
+ *     message for the calling thread.
+ */
+#ifndef NMT_H
+#define NMT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nmt_model nmt_model;   /* device copy of all weights (library-owned) */
+typedef struct nmt_source nmt_source; /* ctx, pctx and lengths of S sentences (library-owned) */
+
+typedef enum {
+  NMT_OK = 0,
+  NMT_EINVAL = -1,     /* bad argument: null pointer, bad size, misaligned buffer */
+  NMT_ENOMEM = -2,     /* device allocation failed */
+  NMT_EDEVICE = -3,    /* HIP runtime error */
+  NMT_ERANGE = -4,     /* an id was out of range (host-checked or reported by the device) */
+  NMT_EWORKSPACE = -5  /* workspace smaller than nmt_score_workspace_bytes() */
+} nmt_status;
+
+typedef enum { NMT_F32 = 0, NMT_BF16 = 1 } nmt_dtype;
+
+/* Model dimensions.  V_src / V: source / target vocabulary; E: embedding
+ * width; H: hidden width (annotations are 2H wide); A: attention width.
+ * E, H and A must be positive multiples of 4.  wtype selects the storage of
+ * weights and embeddings on the device; activations, states and all
+ * accumulation stay fp32. */
+typedef struct {
+  int32_t V_src, V, E, H, A;
+  int32_t wtype; /* nmt_dtype */
+} nmt_dims;
+
+/* Host fp32 parameters (shapes with C = 2H):
+ *   emb_src [V_src x E]; enc_f_W, enc_b_W [E x 3H]; enc_f_b, enc_b_b [3H];
+ *   enc_f_U, enc_b_U [H x 3H]; att_Wc [C x A]; att_b [A]; init_W [C x H];
+ *   init_b [H]; emb_tgt [V x E]; g1_W [E x 3H]; g1_b [3H]; g1_U [H x 3H];
+ *   att_Wq [H x A]; att_v [A]; g2_U [H x 3H]; g2_b [3H]; g2_Wc [C x 3H];
+ *   ro_Ws [H x E]; ro_Wy [E x E]; ro_Wc [C x E]; ro_b [E]; out_W [E x V];
+ *   out_b [V].
+ * With wtype = NMT_BF16 the values are rounded to bf16 (nearest, ties to
+ * even) when copied; pass bf16-representable values to store them exactly. */
+typedef struct {
+  const float *emb_src, *enc_f_W, *enc_f_b, *enc_f_U, *enc_b_W, *enc_b_b, *enc_b_U;
+  const float *att_Wc, *att_b, *init_W, *init_b;
+  const float *emb_tgt, *g1_W, *g1_b, *g1_U, *att_Wq, *att_v;
+  const float *g2_U, *g2_b, *g2_Wc, *ro_Ws, *ro_Wy, *ro_Wc, *ro_b, *out_W, *out_b;
+} nmt_weights;
+
+/* Copy the parameters to the current HIP device, re-laid-out for the
+ * kernels.  The caller keeps ownership of the host arrays and may free them
+ * on return.  Synchronous.  Errors: NMT_EINVAL (bad dims or null weight),
+ * NMT_ENOMEM, NMT_EDEVICE. */
+nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out);
+
+/* Free the model (waits for the device first).  NULL is a no-op. */
+void nmt_model_destroy(nmt_model* m);
+
+/* Source initialisation (Section 5.1: the model is initialised with the
+ * source sentence before any hypothesis is scored).  d_src_ids [S x Tpad]
+ * int32 in [0, V_src) for positions below each length (padding positions
+ * are ignored); h_len [S] host int32 in [1, Tpad].  Computes the
+ * annotations, the attention keys and, if d_s0_out is not NULL, the initial
+ * decoder states d_s0_out [S x H].  The returned source owns its device
+ * buffers; it may be used by nmt_score_batch on any stream once the work
+ * enqueued here has completed in stream order.  Out-of-range source ids set
+ * the model's device error flag (see nmt_stream_status) and read as id 0.
+ * Errors: NMT_EINVAL, NMT_ENOMEM, NMT_EDEVICE. */
+nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_src_ids,
+                      const int32_t* h_len, float* d_s0_out, void* stream, nmt_source** out);
+
+/* A source built from given annotations d_ctx [S x Tpad x 2H] (fp32; values
+ * past each length are ignored) instead of the encoder: only the attention
+ * keys are computed.  For testing the decoder step in isolation. */
+nmt_status nmt_source_from_annotations(nmt_model* m, int32_t S, int32_t Tpad, const float* d_ctx,
+                                       const int32_t* h_len, void* stream, nmt_source** out);
+
+/* Device views of a source: d_ctx [S x Tpad x 2H], d_pctx [S x Tpad x A]
+ * (both zero past each length once the building work has completed).
+ * Pointers stay valid until nmt_source_destroy.  Any output may be NULL. */
+nmt_status nmt_source_info(const nmt_source* src, int32_t* S, int32_t* Tpad, const float** d_ctx,
+                           const float** d_pctx);
+
+/* Free a source (waits for the device first).  NULL is a no-op. */
+void nmt_source_destroy(nmt_source* src);
+
+/* Bytes of device workspace nmt_score_batch needs for B rows. */
+size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B);
+
+/* One batched decoder step: the forward step (H_i, P_i) <- NMT(H_{i-1}, E_i)
+ * of Section 5.1 / Figure 2, for B rows.
+ *   d_s_prev [B x H]  states H_{i-1} (fp32)
+ *   d_y_prev [B]      previous target word of each row, -1 = sentence start
+ *                     (the embedding lookups forming E_i)
+ *   d_sent_id [B]     source sentence of each row, in [0, S)
+ *   d_req [B]         requested next word of each row, in [0, V)
+ *   d_logp [B]        out: log p(req | row), natural log, full vocabulary
+ *   d_s_new [B x H]   out: new states H_i (may alias d_s_prev)
+ *   d_logZ [B]        out, nullable: per-row log normaliser
+ *   d_workspace       device scratch of at least
+ *                     nmt_score_workspace_bytes(m, B) bytes, 256-byte aligned
+ * Rows are independent: row b of every output depends only on row b of the
+ * inputs.  B = 0 is a no-op.  The call allocates nothing.  Device-resident
+ * ids out of range set the model's device error flag and give that row
+ * logp = NaN (see nmt_stream_status).  Calls on different streams must use
+ * different workspaces.  Errors: NMT_EINVAL, NMT_EWORKSPACE, NMT_EDEVICE. */
+nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                           const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
+                           float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace,
+                           size_t ws_bytes, void* stream);
+
+/* nmt_score_batch that also writes the step's intermediates (each nullable):
+ * d_alpha [B x Tpad] attention weights (zero past the length), d_c [B x 2H]
+ * context, d_s1 [B x H] first-GRU state, d_t [B x E] readout. */
+nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
+                                 const float* d_s_prev, const int32_t* d_y_prev,
+                                 const int32_t* d_sent_id, const int32_t* d_req, float* d_logp,
+                                 float* d_s_new, float* d_logZ, void* d_workspace,
+                                 size_t ws_bytes, void* stream, float* d_alpha, float* d_c,
+                                 float* d_s1, float* d_t);
+
+/* Wait for `stream`, then report and clear the model's device error flag:
+ * NMT_ERANGE if any call since the last check met an out-of-range id,
+ * NMT_EDEVICE on a HIP error, else NMT_OK. */
+nmt_status nmt_stream_status(nmt_model* m, void* stream);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char* nmt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NMT_H */

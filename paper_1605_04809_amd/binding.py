@@ -1,0 +1,270 @@
+"""ctypes binding of libnmt (include/nmt.h) with the same call names.
+
+Argument marshalling only: every arithmetic step runs in the HIP kernels of
+libnmt.so.  torch tensors provide device memory (``data_ptr()``) and the
+stream (``torch.cuda.current_stream()``).  There is no CPU fallback: if the
+library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnmt.so")
+
+NMT_OK, NMT_EINVAL, NMT_ENOMEM, NMT_EDEVICE, NMT_ERANGE, NMT_EWORKSPACE = 0, -1, -2, -3, -4, -5
+NMT_F32, NMT_BF16 = 0, 1
+STATUS_NAMES = {0: "NMT_OK", -1: "NMT_EINVAL", -2: "NMT_ENOMEM", -3: "NMT_EDEVICE", -4: "NMT_ERANGE",
+                -5: "NMT_EWORKSPACE"}
+
+WEIGHT_FIELDS = (
+    "emb_src", "enc_f_W", "enc_f_b", "enc_f_U", "enc_b_W", "enc_b_b", "enc_b_U",
+    "att_Wc", "att_b", "init_W", "init_b",
+    "emb_tgt", "g1_W", "g1_b", "g1_U", "att_Wq", "att_v",
+    "g2_U", "g2_b", "g2_Wc", "ro_Ws", "ro_Wy", "ro_Wc", "ro_b", "out_W", "out_b",
+)
+
+# Every function the header declares (checked against include/nmt.h by the tests).
+EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_from_annotations",
+           "nmt_source_info", "nmt_source_destroy", "nmt_score_workspace_bytes", "nmt_score_batch",
+           "nmt_score_batch_debug", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
+           "nmt_profile_end")
+
+PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
+
+_VP = ctypes.c_void_p
+_I32 = ctypes.c_int32
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("V_src", _I32), ("V", _I32), ("E", _I32), ("H", _I32), ("A", _I32), ("wtype", _I32)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.POINTER(ctypes.c_float)) for n in WEIGHT_FIELDS]
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("steps", _I32), ("ms", ctypes.c_double * len(PHASES))]
+
+
+class NmtError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libnmt.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_1605_04809_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    lib.nmt_model_create.argtypes = [P(Dims), P(Weights), P(_VP)]
+    lib.nmt_model_destroy.argtypes = [_VP]
+    lib.nmt_model_destroy.restype = None
+    lib.nmt_encode.argtypes = [_VP, _I32, _I32, _VP, P(_I32), _VP, _VP, P(_VP)]
+    lib.nmt_source_from_annotations.argtypes = [_VP, _I32, _I32, _VP, P(_I32), _VP, P(_VP)]
+    lib.nmt_source_info.argtypes = [_VP, P(_I32), P(_I32), P(_VP), P(_VP)]
+    lib.nmt_source_destroy.argtypes = [_VP]
+    lib.nmt_source_destroy.restype = None
+    lib.nmt_score_workspace_bytes.argtypes = [_VP, _I32]
+    lib.nmt_score_workspace_bytes.restype = ctypes.c_size_t
+    score = [_VP, _VP, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]
+    lib.nmt_score_batch.argtypes = score
+    lib.nmt_score_batch_debug.argtypes = score + [_VP, _VP, _VP, _VP]
+    lib.nmt_stream_status.argtypes = [_VP, _VP]
+    lib.nmt_profile_begin.argtypes = [_VP, _I32]
+    lib.nmt_profile_end.argtypes = [_VP, _VP, P(Timing)]
+    lib.nmt_last_error.argtypes = []
+    lib.nmt_last_error.restype = ctypes.c_char_p
+    for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
+              "nmt_score_batch", "nmt_score_batch_debug", "nmt_stream_status", "nmt_profile_begin",
+              "nmt_profile_end"):
+        getattr(lib, f).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().nmt_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != NMT_OK:
+        raise NmtError(rc, last_error())
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a torch tensor (None stays NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+class Model:
+    """nmt_model_create / nmt_model_destroy around host fp32 parameters."""
+
+    def __init__(self, params: Dict[str, np.ndarray], V_src: int, V: int, E: int, H: int, A: int,
+                 wtype: str = "f32"):
+        lib = load_library()
+        self.V_src, self.V, self.E, self.H, self.A = V_src, V, E, H, A
+        self.C = 2 * H
+        self.wtype = wtype
+        dims = Dims(V_src, V, E, H, A, NMT_BF16 if wtype == "bf16" else NMT_F32)
+        keep = [np.ascontiguousarray(params[n], dtype=np.float32) for n in WEIGHT_FIELDS]
+        w = Weights(*[a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for a in keep])
+        h = _VP()
+        _check(lib.nmt_model_create(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(h)))
+        self.handle = h
+
+    @classmethod
+    def from_workload(cls, wl) -> "Model":
+        c = wl.cfg
+        return cls(wl.params, c.V_src, c.V, c.E, c.H, c.A, c.wtype)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().nmt_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Source:
+    """An nmt_source (annotations, attention keys, lengths of S sentences)."""
+
+    def __init__(self, handle, S: int, Tpad: int, src_len: np.ndarray, model: Model):
+        self.handle, self.S, self.Tpad, self.src_len, self.model = handle, S, Tpad, src_len, model
+
+    def device_views(self):
+        """(ctx_ptr, pctx_ptr) device addresses of the source's buffers."""
+        c, p = _VP(), _VP()
+        _check(load_library().nmt_source_info(self.handle, None, None, ctypes.byref(c), ctypes.byref(p)))
+        return c.value, p.value
+
+    def copy_out(self):
+        """Copies of (ctx [S,Tpad,2H], pctx [S,Tpad,A]) as device tensors (test helper)."""
+        import torch
+        cptr, pptr = self.device_views()
+        m = self.model
+        ctx = torch.empty((self.S, self.Tpad, m.C), dtype=torch.float32, device="cuda")
+        pctx = torch.empty((self.S, self.Tpad, m.A), dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        _hip_memcpy_d2d(ctx.data_ptr(), cptr, ctx.numel() * 4)
+        _hip_memcpy_d2d(pctx.data_ptr(), pptr, pctx.numel() * 4)
+        return ctx, pctx
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().nmt_source_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+_hip = None
+
+
+def _hip_memcpy_d2d(dst: int, src: int, nbytes: int):
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipMemcpy.argtypes = [_VP, _VP, ctypes.c_size_t, ctypes.c_int]
+    rc = _hip.hipMemcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
+    if rc != 0:
+        raise RuntimeError(f"hipMemcpy failed ({rc})")
+
+
+def _len_array(src_len):
+    a = np.ascontiguousarray(src_len, dtype=np.int32)
+    return a, a.ctypes.data_as(ctypes.POINTER(_I32))
+
+
+def nmt_encode(model: Model, src_ids, src_len, s0_out=None, stream=None) -> Source:
+    """Source initialisation from device ids [S, Tpad] int32 and host lengths [S]."""
+    lib = load_library()
+    S, T = int(src_ids.shape[0]), int(src_ids.shape[1])
+    lens, lp = _len_array(src_len)
+    h = _VP()
+    _check(lib.nmt_encode(model.handle, S, T, _ptr(src_ids), lp, _ptr(s0_out), _stream(stream), ctypes.byref(h)))
+    return Source(h, S, T, lens.copy(), model)
+
+
+def nmt_source_from_annotations(model: Model, ctx, src_len, stream=None) -> Source:
+    lib = load_library()
+    S, T = int(ctx.shape[0]), int(ctx.shape[1])
+    lens, lp = _len_array(src_len)
+    h = _VP()
+    _check(lib.nmt_source_from_annotations(model.handle, S, T, _ptr(ctx), lp, _stream(stream), ctypes.byref(h)))
+    return Source(h, S, T, lens.copy(), model)
+
+
+def nmt_score_workspace_bytes(model: Model, B: int) -> int:
+    return int(load_library().nmt_score_workspace_bytes(model.handle, B))
+
+
+def nmt_score_batch(model: Model, src: Source, s_prev, y_prev, sent_id, req, logp, s_new, logZ=None,
+                    workspace=None, stream=None, alpha=None, c=None, s1=None, t=None):
+    """One batched decoder step; outputs are written into the given tensors.
+
+    With any of ``alpha``, ``c``, ``s1``, ``t`` given, nmt_score_batch_debug is
+    called and those intermediates are written too.
+    """
+    import torch
+    lib = load_library()
+    B = int(y_prev.shape[0])
+    if workspace is None:
+        workspace = torch.empty(max(nmt_score_workspace_bytes(model, B), 256), dtype=torch.uint8, device="cuda")
+    args = [model.handle, src.handle, B, _ptr(s_prev), _ptr(y_prev), _ptr(sent_id), _ptr(req), _ptr(logp),
+            _ptr(s_new), _ptr(logZ), _ptr(workspace), workspace.numel(), _stream(stream)]
+    if any(x is not None for x in (alpha, c, s1, t)):
+        _check(lib.nmt_score_batch_debug(*args, _ptr(alpha), _ptr(c), _ptr(s1), _ptr(t)))
+    else:
+        _check(lib.nmt_score_batch(*args))
+
+
+def nmt_stream_status(model: Model, stream=None) -> int:
+    """Status code (NMT_OK / NMT_ERANGE / ...) without raising."""
+    return int(load_library().nmt_stream_status(model.handle, _stream(stream)))
+
+
+def nmt_profile_begin(model: Model, max_steps: int):
+    _check(load_library().nmt_profile_begin(model.handle, max_steps))
+
+
+def nmt_profile_end(model: Model, stream=None) -> dict:
+    """Summed milliseconds per phase over the timed steps, plus ``steps``."""
+    t = Timing()
+    _check(load_library().nmt_profile_end(model.handle, _stream(stream), ctypes.byref(t)))
+    out = {name: float(t.ms[i]) for i, name in enumerate(PHASES)}
+    out["steps"] = int(t.steps)
+    return out

@@ -1,0 +1,612 @@
+// api.hip -- the C-ABI of libnmt (declared in include/nmt.h): model upload
+// and re-layout, source initialisation, and the batched decoder step
+// (Section 5.1 of the paper: NMT(H_{i-1}, E_i) over a precomputed source
+// context).  Every arithmetic step runs in the kernels of kernels.hip; this
+// file validates arguments, packs weights once, and enqueues launches.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/nmt.h"
+#include "../../include/nmt_profile.h"
+#include "internal.hpp"
+
+using namespace nmt;
+
+namespace {
+
+thread_local std::string g_err;
+
+nmt_status fail(nmt_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+nmt_status ok() {
+  g_err.clear();
+  return NMT_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Device allocations owned by a model or a source.
+struct Allocs {
+  std::vector<void*> ptrs;
+  hipError_t alloc(void** p, size_t bytes) {
+    hipError_t e = hipMalloc(p, bytes < 256 ? 256 : bytes);
+    if (e == hipSuccess) ptrs.push_back(*p);
+    return e;
+  }
+  void release() {
+    for (void* p : ptrs) (void)hipFree(p);
+    ptrs.clear();
+  }
+};
+
+struct GruBias {
+  float *brz = nullptr, *bni = nullptr, *bns = nullptr;
+};
+
+}  // namespace
+
+struct nmt_model {
+  nmt_dims dims{};
+  int device = 0;
+  Allocs mem;
+  float *emb_src = nullptr, *emb_tgt = nullptr;
+  Packed enc_in, enc_U[2], att_Wc, init_W, g1, att_Wq, g2, ro, out;
+  float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr,
+        *out_b = nullptr;
+  GruBias enc_bias, g1_bias, g2_bias;
+  int* err = nullptr;  // sticky device error flag
+  int nNt = 0;         // vocabulary column tiles
+  // event timing of the step's phases (nmt_profile.h); not thread-safe
+  std::vector<hipEvent_t> prof_events;  // (NMT_NUM_PHASES + 1) per timed step
+  int prof_max = 0, prof_used = 0;
+  bool prof_on = false;
+};
+
+struct nmt_source {
+  int32_t S = 0, Tpad = 0;
+  Allocs mem;
+  float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
+  int32_t* len = nullptr;
+  std::vector<int32_t> h_len;
+};
+
+namespace {
+
+// Host-side packing of x.W-oriented weights into the [Kpad/4][Npad][4]
+// layout of the GEMM kernels.  Segments are stacked along K, each padded to
+// a multiple of KC; `colmap(np)` gives the source column of packed column np
+// (or -1 for a zero column).
+struct Seg {
+  const float* W;  // [K x ld] row-major
+  int K;
+  int ld;
+};
+
+template <class ColMap>
+std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, ColMap colmap, int64_t* Kpad_out) {
+  int64_t Kpad = 0;
+  for (const Seg& s : segs) Kpad += round_up(s.K, KC);
+  std::vector<float> out((size_t)(Kpad * Npad), 0.f);
+  std::vector<int> cols((size_t)Npad);
+  for (int64_t np = 0; np < Npad; ++np) cols[(size_t)np] = colmap(np);
+  int64_t koff = 0;
+  for (const Seg& s : segs) {
+    for (int k = 0; k < s.K; ++k) {
+      const int64_t kk = koff + k;
+      float* dst = out.data() + (kk / 4) * Npad * 4 + (kk % 4);
+      const float* src = s.W + (int64_t)k * s.ld;
+      for (int64_t np = 0; np < Npad; ++np) {
+        const int c = cols[(size_t)np];
+        if (c >= 0) dst[np * 4] = src[c];
+      }
+    }
+    koff += round_up(s.K, KC);
+  }
+  *Kpad_out = Kpad;
+  return out;
+}
+
+hipError_t upload(Allocs& mem, float** d, const float* h, size_t n) {
+  hipError_t e = mem.alloc((void**)d, n * sizeof(float));
+  if (e != hipSuccess) return e;
+  return hipMemcpy(*d, h, n * sizeof(float), hipMemcpyHostToDevice);
+}
+
+hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int N, int TN) {
+  P->N = N;
+  P->Npad = round_up(N, TN);
+  std::vector<float> h = pack_host(segs, P->Npad, [N](int64_t np) { return np < N ? (int)np : -1; }, &P->Kpad);
+  return upload(mem, &P->d, h.data(), h.size());
+}
+
+// GRU packing: column tile u holds [r | z | n] of hidden units u*HB .. u*HB+HB-1.
+hipError_t pack_gru(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int H) {
+  P->N = 3 * H;
+  P->Npad = (int64_t)ceil_div(H, kGruHB) * 3 * kGruHB;
+  std::vector<float> h = pack_host(
+      segs, P->Npad,
+      [H](int64_t np) {
+        const int ub = (int)(np / (3 * kGruHB)), rem = (int)(np % (3 * kGruHB));
+        const int g = rem / kGruHB, j = ub * kGruHB + rem % kGruHB;
+        return j < H ? g * H + j : -1;
+      },
+      &P->Kpad);
+  return upload(mem, &P->d, h.data(), h.size());
+}
+
+// r/z biases summed over both sides; candidate bias split by side.
+hipError_t upload_gru_bias(Allocs& mem, GruBias* b, const float* b_in, const float* b_st, int H) {
+  std::vector<float> rz(2 * H, 0.f), ni(H, 0.f), ns(H, 0.f);
+  for (int j = 0; j < 2 * H; ++j) rz[j] = (b_in ? b_in[j] : 0.f) + (b_st ? b_st[j] : 0.f);
+  for (int j = 0; j < H; ++j) {
+    ni[j] = b_in ? b_in[2 * H + j] : 0.f;
+    ns[j] = b_st ? b_st[2 * H + j] : 0.f;
+  }
+  hipError_t e = upload(mem, &b->brz, rz.data(), rz.size());
+  if (e == hipSuccess) e = upload(mem, &b->bni, ni.data(), ni.size());
+  if (e == hipSuccess) e = upload(mem, &b->bns, ns.data(), ns.size());
+  return e;
+}
+
+ASeg make_seg(const float* p, int64_t ld, int K, int side, const int32_t* gather = nullptr, int gmax = 0) {
+  ASeg s{};
+  s.p = p;
+  s.gather = gather;
+  s.gmax = gmax;
+  s.ld = ld;
+  s.K = K;
+  s.nchunk = ceil_div(K, KC);
+  s.side = side;
+  return s;
+}
+
+AOperand make_a(int M, std::initializer_list<ASeg> segs) {
+  AOperand a{};
+  a.M = M;
+  a.nseg = 0;
+  for (const ASeg& s : segs) a.seg[a.nseg++] = s;
+  return a;
+}
+
+nmt_status check_device(const nmt_model* m) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(NMT_EDEVICE, "hipGetDevice failed");
+  if (dev != m->device) return fail(NMT_EINVAL, "model lives on device %d but device %d is current", m->device, dev);
+  return NMT_OK;
+}
+
+nmt_status hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorOutOfMemory) return fail(NMT_ENOMEM, "%s: out of device memory", what);
+  return fail(NMT_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Workspace layout of one step (offsets in bytes, 256-aligned).
+struct WsLayout {
+  size_t s1, q, c, t, pm, ps, total;
+};
+
+WsLayout ws_layout(const nmt_model* m, int64_t B) {
+  const nmt_dims& d = m->dims;
+  auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+  WsLayout L{};
+  size_t off = 0;
+  L.s1 = off;
+  off += al((size_t)B * d.H * 4);
+  L.q = off;
+  off += al((size_t)B * d.A * 4);
+  L.c = off;
+  off += al((size_t)B * 2 * d.H * 4);
+  L.t = off;
+  off += al((size_t)B * d.E * 4);
+  L.pm = off;
+  off += al((size_t)B * m->nNt * 4);
+  L.ps = off;
+  off += al((size_t)B * m->nNt * 4);
+  L.total = off;
+  return L;
+}
+
+nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_len, bool with_scratch,
+                      hipStream_t st, nmt_source** out) {
+  const nmt_dims& d = m->dims;
+  if (S < 1) return fail(NMT_EINVAL, "S must be >= 1 (got %d)", S);
+  if (Tpad < 1 || Tpad > kMaxTpad) return fail(NMT_EINVAL, "Tpad must be in [1, %d] (got %d)", kMaxTpad, Tpad);
+  if (!h_len) return fail(NMT_EINVAL, "h_len is NULL");
+  for (int s = 0; s < S; ++s)
+    if (h_len[s] < 1 || h_len[s] > Tpad)
+      return fail(NMT_EINVAL, "h_len[%d] = %d is outside [1, Tpad = %d]", s, h_len[s], Tpad);
+  nmt_source* src = new nmt_source();
+  src->S = S;
+  src->Tpad = Tpad;
+  src->h_len.assign(h_len, h_len + S);
+  const size_t rows = (size_t)S * Tpad;
+  hipError_t e = src->mem.alloc((void**)&src->ctx, rows * 2 * d.H * sizeof(float));
+  if (e == hipSuccess) e = src->mem.alloc((void**)&src->pctx, rows * d.A * sizeof(float));
+  if (e == hipSuccess) e = src->mem.alloc((void**)&src->len, S * sizeof(int32_t));
+  if (e == hipSuccess && with_scratch) e = src->mem.alloc((void**)&src->scratch, rows * 6 * d.H * sizeof(float));
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(src->len, src->h_len.data(), S * sizeof(int32_t), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) {
+    src->mem.release();
+    delete src;
+    return hip_fail(e, "source allocation");
+  }
+  *out = src;
+  return NMT_OK;
+}
+
+// Attention keys pctx = ctx att_Wc + att_b for the unmasked positions.
+hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
+  const nmt_dims& d = m->dims;
+  const int C = 2 * d.H;
+  AOperand A = make_a(src->S * src->Tpad, {make_seg(src->ctx, C, C, 0)});
+  PlainEpi ep{src->pctx, d.A, m->att_b, d.A, 0, src->len, src->Tpad};
+  return launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* nmt_last_error(void) { return g_err.c_str(); }
+
+nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out) {
+  if (!dims || !w || !out) return fail(NMT_EINVAL, "NULL argument");
+  *out = nullptr;
+  const nmt_dims d = *dims;
+  if (d.V_src <= 0 || d.V <= 0 || d.E <= 0 || d.H <= 0 || d.A <= 0)
+    return fail(NMT_EINVAL, "dimensions must be positive");
+  if (d.E % 4 || d.H % 4 || d.A % 4) return fail(NMT_EINVAL, "E, H and A must be multiples of 4");
+  if (d.A > 8 * 256) return fail(NMT_EINVAL, "A must be at most 2048");
+  if (d.wtype != NMT_F32) return fail(NMT_EINVAL, "weight type %d is not supported", d.wtype);
+  const float* const* wp = (const float* const*)w;
+  for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
+    if (!wp[i]) return fail(NMT_EINVAL, "weight #%zu is NULL", i);
+
+  nmt_model* m = new nmt_model();
+  m->dims = d;
+  if (hipGetDevice(&m->device) != hipSuccess) {
+    delete m;
+    return fail(NMT_EDEVICE, "hipGetDevice failed");
+  }
+  const int E = d.E, H = d.H, A = d.A, C = 2 * d.H, V = d.V;
+  hipError_t e = hipSuccess;
+  auto step = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+  };
+  step(upload(m->mem, &m->emb_src, w->emb_src, (size_t)d.V_src * E));
+  step(upload(m->mem, &m->emb_tgt, w->emb_tgt, (size_t)V * E));
+  {  // encoder input projections of both directions side by side: [E x 6H]
+    std::vector<float> Win((size_t)E * 6 * H), bin((size_t)6 * H);
+    for (int k = 0; k < E; ++k)
+      for (int j = 0; j < 3 * H; ++j) {
+        Win[(size_t)k * 6 * H + j] = w->enc_f_W[(size_t)k * 3 * H + j];
+        Win[(size_t)k * 6 * H + 3 * H + j] = w->enc_b_W[(size_t)k * 3 * H + j];
+      }
+    for (int j = 0; j < 3 * H; ++j) {
+      bin[j] = w->enc_f_b[j];
+      bin[3 * H + j] = w->enc_b_b[j];
+    }
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->enc_in, {{Win.data(), E, 6 * H}}, 6 * H, kPlainLargeTN));
+    step(upload(m->mem, &m->enc_in_b, bin.data(), bin.size()));
+  }
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[0], {{w->enc_f_U, H, 3 * H}}, H));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[1], {{w->enc_b_U, H, 3 * H}}, H));
+  if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->enc_bias, nullptr, nullptr, H));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wc, {{w->att_Wc, C, A}}, A, kPlainLargeTN));
+  step(upload(m->mem, &m->att_b, w->att_b, A));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN));
+  step(upload(m->mem, &m->init_b, w->init_b, H));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_W, E, 3 * H}, {w->g1_U, H, 3 * H}}, H));
+  if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g1_bias, w->g1_b, nullptr, H));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wq, {{w->att_Wq, H, A}}, A, kPlainSmallTN));
+  step(upload(m->mem, &m->att_v, w->att_v, A));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H));
+  if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g2_bias, nullptr, w->g2_b, H));
+  if (e == hipSuccess)
+    step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN));
+  step(upload(m->mem, &m->ro_b, w->ro_b, E));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->out, {{w->out_W, E, V}}, V, kVocabTN));
+  step(upload(m->mem, &m->out_b, w->out_b, V));
+  step(m->mem.alloc((void**)&m->err, sizeof(int)));
+  if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
+  if (e == hipSuccess) step(hipDeviceSynchronize());
+  if (e != hipSuccess) {
+    m->mem.release();
+    delete m;
+    return hip_fail(e, "nmt_model_create");
+  }
+  m->nNt = (int)(m->out.Npad / kVocabTN);
+  *out = m;
+  return ok();
+}
+
+static void drop_profile_events(nmt_model* m) {
+  for (hipEvent_t ev : m->prof_events) (void)hipEventDestroy(ev);
+  m->prof_events.clear();
+  m->prof_on = false;
+  m->prof_max = m->prof_used = 0;
+}
+
+void nmt_model_destroy(nmt_model* m) {
+  if (!m) return;
+  (void)hipDeviceSynchronize();
+  drop_profile_events(m);
+  m->mem.release();
+  delete m;
+}
+
+nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_src_ids, const int32_t* h_len,
+                      float* d_s0_out, void* stream, nmt_source** out) {
+  if (!m || !out) return fail(NMT_EINVAL, "NULL model or output");
+  *out = nullptr;
+  if (!d_src_ids) return fail(NMT_EINVAL, "d_src_ids is NULL");
+  if (d_s0_out && !aligned16(d_s0_out)) return fail(NMT_EINVAL, "d_s0_out must be 16-byte aligned");
+  nmt_status rc = check_device(m);
+  if (rc != NMT_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  nmt_source* src = nullptr;
+  rc = new_source(m, S, Tpad, h_len, true, st, &src);
+  if (rc != NMT_OK) return rc;
+  const nmt_dims& d = m->dims;
+  const int E = d.E, H = d.H, C = 2 * H;
+  const int64_t rows = (int64_t)S * Tpad;
+  float* Xp = src->scratch;  // [S*Tpad x 6H] input-side pre-activations of both directions
+  hipError_t e = launch_check_src_ids(S, Tpad, d_src_ids, src->len, d.V_src, m->err, st);
+  if (e == hipSuccess) {
+    AOperand A = make_a((int)rows, {make_seg(m->emb_src, E, E, 0, d_src_ids, d.V_src)});
+    PlainEpi ep{Xp, 6 * H, m->enc_in_b, 6 * H, 0, nullptr, 1};
+    e = launch_gemm_plain(Tile::Large, A, m->enc_in, ep, st);
+  }
+  // The recurrence: step t runs the forward direction at position t and the
+  // backward direction at position Tpad-1-t in one launch.  Positions at or
+  // past a sentence's length are written as zeros, which is also the
+  // backward direction's initial state there.
+  const int64_t ldc = (int64_t)Tpad * C, ldx = (int64_t)Tpad * 6 * H;
+  for (int t = 0; t < Tpad && e == hipSuccess; ++t) {
+    GruProblem p[2];
+    for (int dir = 0; dir < 2; ++dir) {
+      const int pos = dir == 0 ? t : Tpad - 1 - t;
+      const int prev = dir == 0 ? pos - 1 : pos + 1;
+      const bool has_prev = prev >= 0 && prev < Tpad;
+      const float* hprev = has_prev ? src->ctx + (int64_t)prev * C + dir * H : nullptr;
+      GruProblem& g = p[dir];
+      g.A = has_prev ? make_a(S, {make_seg(hprev, ldc, H, 1)}) : make_a(S, {});
+      g.Wp = m->enc_U[dir].d;
+      g.Npad = m->enc_U[dir].Npad;
+      g.ep = GruEpi{hprev, ldc, Xp + (int64_t)pos * 6 * H + dir * 3 * H, ldx, m->enc_bias.brz, m->enc_bias.bni,
+                    m->enc_bias.bns, src->ctx + (int64_t)pos * C + dir * H, ldc, src->len, pos, H};
+    }
+    e = launch_gemm_gru(p, 2, H, st);
+  }
+  if (e == hipSuccess) e = source_keys(m, src, st);
+  if (e == hipSuccess && d_s0_out) {
+    float* mean = Xp;  // the pre-activations are consumed by now (stream order)
+    e = launch_masked_mean(S, Tpad, C, src->ctx, src->len, mean, st);
+    if (e == hipSuccess) {
+      AOperand A = make_a(S, {make_seg(mean, C, C, 0)});
+      PlainEpi ep{d_s0_out, H, m->init_b, H, 1, nullptr, 1};
+      e = launch_gemm_plain(Tile::Small, A, m->init_W, ep, st);
+    }
+  }
+  if (e != hipSuccess) {
+    (void)hipStreamSynchronize(st);
+    nmt_source_destroy(src);
+    return hip_fail(e, "nmt_encode");
+  }
+  *out = src;
+  return ok();
+}
+
+nmt_status nmt_source_from_annotations(nmt_model* m, int32_t S, int32_t Tpad, const float* d_ctx,
+                                       const int32_t* h_len, void* stream, nmt_source** out) {
+  if (!m || !out) return fail(NMT_EINVAL, "NULL model or output");
+  *out = nullptr;
+  if (!d_ctx || !aligned16(d_ctx)) return fail(NMT_EINVAL, "d_ctx must be a 16-byte aligned device pointer");
+  nmt_status rc = check_device(m);
+  if (rc != NMT_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  nmt_source* src = nullptr;
+  rc = new_source(m, S, Tpad, h_len, false, st, &src);
+  if (rc != NMT_OK) return rc;
+  hipError_t e = launch_masked_copy(S, Tpad, 2 * m->dims.H, d_ctx, src->len, src->ctx, st);
+  if (e == hipSuccess) e = source_keys(m, src, st);
+  if (e != hipSuccess) {
+    (void)hipStreamSynchronize(st);
+    nmt_source_destroy(src);
+    return hip_fail(e, "nmt_source_from_annotations");
+  }
+  *out = src;
+  return ok();
+}
+
+nmt_status nmt_source_info(const nmt_source* src, int32_t* S, int32_t* Tpad, const float** d_ctx,
+                           const float** d_pctx) {
+  if (!src) return fail(NMT_EINVAL, "NULL source");
+  if (S) *S = src->S;
+  if (Tpad) *Tpad = src->Tpad;
+  if (d_ctx) *d_ctx = src->ctx;
+  if (d_pctx) *d_pctx = src->pctx;
+  return ok();
+}
+
+void nmt_source_destroy(nmt_source* src) {
+  if (!src) return;
+  (void)hipDeviceSynchronize();
+  src->mem.release();
+  delete src;
+}
+
+size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B) {
+  if (!m || B <= 0) return 0;
+  return ws_layout(m, B).total;
+}
+
+nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                                 const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
+                                 float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes,
+                                 void* stream, float* d_alpha, float* d_c, float* d_s1, float* d_t) {
+  if (!m || !src) return fail(NMT_EINVAL, "NULL model or source");
+  if (B < 0) return fail(NMT_EINVAL, "B must be >= 0 (got %d)", B);
+  if (B == 0) return ok();
+  if (!d_s_prev || !d_y_prev || !d_sent_id || !d_req || !d_logp || !d_s_new)
+    return fail(NMT_EINVAL, "a required device pointer is NULL");
+  if (!aligned16(d_s_prev) || !aligned16(d_s_new))
+    return fail(NMT_EINVAL, "d_s_prev and d_s_new must be 16-byte aligned");
+  if ((d_c && !aligned16(d_c)) || (d_s1 && !aligned16(d_s1)) || (d_t && !aligned16(d_t)))
+    return fail(NMT_EINVAL, "debug outputs must be 16-byte aligned");
+  const WsLayout L = ws_layout(m, B);
+  if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < L.total) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
+  nmt_status rc = check_device(m);
+  if (rc != NMT_OK) return rc;
+
+  hipStream_t st = (hipStream_t)stream;
+  const nmt_dims& d = m->dims;
+  const int E = d.E, H = d.H, Aw = d.A, C = 2 * H, V = d.V;
+  char* ws = (char*)d_workspace;
+  float* s1 = (float*)(ws + L.s1);
+  float* q = (float*)(ws + L.q);
+  float* c = (float*)(ws + L.c);
+  float* t = (float*)(ws + L.t);
+  float* pm = (float*)(ws + L.pm);
+  float* ps = (float*)(ws + L.ps);
+  const ASeg x_seg = make_seg(m->emb_tgt, E, E, 0, d_y_prev, V);  // E_i: embedding rows of the previous words
+  hipEvent_t* ev = nullptr;
+  if (m->prof_on && m->prof_used < m->prof_max) ev = &m->prof_events[(size_t)(m->prof_used++) * (NMT_NUM_PHASES + 1)];
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[i], st);
+  };
+  mark(0);
+
+  // first GRU: s1 = GRU(x, s_prev)
+  GruProblem g1;
+  g1.A = make_a(B, {x_seg, make_seg(d_s_prev, H, H, 1)});
+  g1.Wp = m->g1.d;
+  g1.Npad = m->g1.Npad;
+  g1.ep = GruEpi{d_s_prev, H, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns, s1, H, nullptr, 0, H};
+  if (e == hipSuccess) e = launch_gemm_gru(&g1, 1, H, st);
+  mark(NMT_PHASE_GRU1 + 1);
+  // attention query q = s1 att_Wq
+  if (e == hipSuccess) {
+    PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1};
+    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(s1, H, H, 0)}), m->att_Wq, ep, st);
+  }
+  mark(NMT_PHASE_QUERY + 1);
+  // masked attention and context
+  if (e == hipSuccess)
+    e = launch_attention(B, Aw, C, src->Tpad, q, src->pctx, src->ctx, src->len, d_sent_id, src->S, m->att_v, c,
+                         d_alpha, st);
+  mark(NMT_PHASE_ATTENTION + 1);
+  // second GRU: s_new = GRU(c, s1)
+  if (e == hipSuccess) {
+    GruProblem g2;
+    g2.A = make_a(B, {make_seg(s1, H, H, 1), make_seg(c, C, C, 0)});
+    g2.Wp = m->g2.d;
+    g2.Npad = m->g2.Npad;
+    g2.ep = GruEpi{s1, H, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H, nullptr, 0, H};
+    e = launch_gemm_gru(&g2, 1, H, st);
+  }
+  mark(NMT_PHASE_GRU2 + 1);
+  // readout t = tanh(s_new Ws + x Wy + c Wc + b)
+  if (e == hipSuccess) {
+    PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1};
+    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(d_s_new, H, H, 0), x_seg, make_seg(c, C, C, 0)}), m->ro,
+                          ep, st);
+  }
+  mark(NMT_PHASE_READOUT + 1);
+  // vocabulary projection with per-tile log-sum-exp, then the combine
+  if (e == hipSuccess) e = launch_vocab_lse(make_a(B, {make_seg(t, E, E, 0)}), m->out, m->out_b, V, pm, ps, m->nNt, st);
+  mark(NMT_PHASE_VOCAB + 1);
+  if (e == hipSuccess)
+    e = launch_lse_combine(B, pm, ps, m->nNt, t, E, m->out, m->out_b, V, d_req, d_y_prev, d_sent_id, src->S, d_logp,
+                           d_logZ, m->err, st);
+  mark(NMT_PHASE_COMBINE + 1);
+  if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && d_c) e = hipMemcpyAsync(d_c, c, (size_t)B * C * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && d_t) e = hipMemcpyAsync(d_t, t, (size_t)B * E * 4, hipMemcpyDeviceToDevice, st);
+  if (e != hipSuccess) return hip_fail(e, "nmt_score_batch");
+  return ok();
+}
+
+nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                           const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req, float* d_logp,
+                           float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes, void* stream) {
+  return nmt_score_batch_debug(m, src, B, d_s_prev, d_y_prev, d_sent_id, d_req, d_logp, d_s_new, d_logZ, d_workspace,
+                               ws_bytes, stream, nullptr, nullptr, nullptr, nullptr);
+}
+
+nmt_status nmt_stream_status(nmt_model* m, void* stream) {
+  if (!m) return fail(NMT_EINVAL, "NULL model");
+  nmt_status rc = check_device(m);
+  if (rc != NMT_OK) return rc;
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "nmt_stream_status");
+  int flag = 0;
+  e = hipMemcpy(&flag, m->err, sizeof(int), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && flag) e = hipMemset(m->err, 0, sizeof(int));
+  if (e != hipSuccess) return hip_fail(e, "nmt_stream_status");
+  if (flag) return fail(NMT_ERANGE, "an id was out of range in a call since the last status check");
+  return ok();
+}
+
+}  // extern "C"
+
+extern "C" {
+
+nmt_status nmt_profile_begin(nmt_model* m, int32_t max_steps) {
+  if (!m || max_steps < 1) return fail(NMT_EINVAL, "NULL model or max_steps < 1");
+  nmt_status rc = check_device(m);
+  if (rc != NMT_OK) return rc;
+  (void)hipDeviceSynchronize();
+  drop_profile_events(m);
+  const size_t n = (size_t)max_steps * (NMT_NUM_PHASES + 1);
+  m->prof_events.reserve(n);
+  for (size_t i = 0; i < n; ++i) {
+    hipEvent_t ev;
+    hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) {
+      drop_profile_events(m);
+      return hip_fail(e, "nmt_profile_begin");
+    }
+    m->prof_events.push_back(ev);
+  }
+  m->prof_max = max_steps;
+  m->prof_used = 0;
+  m->prof_on = true;
+  return ok();
+}
+
+nmt_status nmt_profile_end(nmt_model* m, void* stream, nmt_timing* out) {
+  if (!m || !out) return fail(NMT_EINVAL, "NULL model or output");
+  if (!m->prof_on) return fail(NMT_EINVAL, "no profile is running");
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  nmt_timing t{};
+  t.steps = m->prof_used;
+  for (int s = 0; s < m->prof_used && e == hipSuccess; ++s) {
+    hipEvent_t* ev = &m->prof_events[(size_t)s * (NMT_NUM_PHASES + 1)];
+    for (int p = 0; p < NMT_NUM_PHASES && e == hipSuccess; ++p) {
+      float ms = 0.f;
+      e = hipEventElapsedTime(&ms, ev[p], ev[p + 1]);
+      t.ms[p] += ms;
+    }
+  }
+  drop_profile_events(m);
+  if (e != hipSuccess) return hip_fail(e, "nmt_profile_end");
+  *out = t;
+  return ok();
+}
+
+}  // extern "C"

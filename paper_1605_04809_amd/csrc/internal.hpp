@@ -1,0 +1,88 @@
+// internal.hpp -- host-side interface between the C-ABI layer (api.hip) and
+// the kernel launchers (kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device.hpp"
+
+namespace nmt {
+
+constexpr int KC = 32;             // K chunk of every fp32 GEMM tile
+constexpr int kMaxTpad = 1024;     // attention keeps one score per source position in LDS
+
+// Tile shapes (rows x packed columns) of the kernel families.
+constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;
+constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
+constexpr int kGruTM = 128, kGruHB = 64;       // HB hidden units -> 3*HB packed columns
+constexpr int kVocabTM = 128, kVocabTN = 128;
+
+// A weight matrix packed for one kernel family: [Kpad/4][Npad][4] fp32.
+struct Packed {
+  float* d = nullptr;
+  int64_t Kpad = 0;  // sum of the padded K of its segments
+  int64_t Npad = 0;
+  int N = 0;         // valid columns (for GRU: 3H)
+};
+
+enum class Tile { Small, Large };
+
+// Epilogue of the plain GEMM: out = act(acc + bias); rows with
+// (m % mask_T) >= mask_len[m / mask_T] are written as zeros.
+struct PlainEpi {
+  float* out;
+  int64_t ldo;
+  const float* bias;  // [N]
+  int N;
+  int act;            // 0: identity, 1: tanh
+  const int32_t* mask_len;
+  int32_t mask_T;
+};
+
+// Epilogue of the GRU gate GEMM (see device.hpp for the cell).
+struct GruEpi {
+  const float* h;     // previous state rows (nullable: zero state)
+  int64_t ldh;
+  const float* xin;   // nullable: precomputed input-side pre-activations [r|z|n] per row
+  int64_t ldx;
+  const float* brz;   // [2H] summed r,z biases
+  const float* bni;   // [H] input-side candidate bias
+  const float* bns;   // [H] state-side candidate bias (inside the reset gate)
+  float* out;
+  int64_t ldo;
+  const int32_t* mask_len;  // nullable: row m is kept iff mask_pos < mask_len[m]
+  int32_t mask_pos;
+  int32_t H;
+};
+
+struct GruProblem {
+  AOperand A;
+  const float* Wp;
+  int64_t Npad;
+  GruEpi ep;
+};
+
+// Launchers (all asynchronous on `st`).
+hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_t st);
+hipError_t launch_vocab_lse(const AOperand& A, const Packed& W, const float* bias, int V, float* pm,
+                            float* ps, int nNt, hipStream_t st);
+hipError_t launch_lse_combine(int B, const float* pm, const float* ps, int nNt, const float* t, int E,
+                              const Packed& W, const float* bias, int V, const int32_t* req,
+                              const int32_t* y_prev, const int32_t* sent_id, int S, float* logp,
+                              float* logZ, int* err, hipStream_t st);
+hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx,
+                            const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
+                            const float* v, float* c, float* alpha, hipStream_t st);
+hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src,
+                                int* err, hipStream_t st);
+hipError_t launch_masked_copy(int S, int Tpad, int C, const float* src, const int32_t* len, float* dst,
+                              hipStream_t st);
+hipError_t launch_masked_mean(int S, int Tpad, int C, const float* ctx, const int32_t* len, float* mean,
+                              hipStream_t st);
+
+inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+
+}  // namespace nmt

@@ -1,0 +1,500 @@
+// kernels.hip -- the HIP kernels of one batched decoder step and of source
+// initialisation, for gfx950.  Equations are listed in include/nmt.h.
+//
+//   k_gemm_plain   MFMA GEMM with bias (+tanh) epilogue: attention query,
+//                  readout, attention keys, encoder input projections.
+//   k_gemm_gru     MFMA GEMM whose tile holds matching r, z and candidate
+//                  columns of the same hidden units, with the GRU cell fused
+//                  into the epilogue (both decoder GRUs, encoder recurrence).
+//   k_vocab_lse    MFMA vocabulary projection fused with a per-tile
+//                  log-sum-exp; the logits never reach HBM.
+//   k_lse_combine  merges the per-tile partials, scores the requested word
+//                  and checks the row's ids.
+//   k_attention    masked MLP attention and context for one row per block.
+#include "internal.hpp"
+
+namespace nmt {
+
+// ----------------------------------------------------------- plain GEMM
+
+template <int TM, int TN, int WM, int WN>
+__global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOperand A, const float* __restrict__ Wp,
+                                                                           int64_t Npad, PlainEpi ep) {
+  constexpr int NT = (TM / WM) * (TN / WN) * 64;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
+  const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm0 = (wave % (TM / WM)) * WM, wn0 = (wave / (TM / WM)) * WN;
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+
+  gemm_mainloop<TM, TN, KC, NT>(A, Wp, Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) {
+#pragma unroll
+    for (int kg = 0; kg < KC / 8; ++kg) {
+      f32x4 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
+    }
+  });
+
+  const int h = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int n = n0 + wn0 + 32 * j + l32;
+    if (n >= ep.N) continue;
+    const float bn = ep.bias ? ep.bias[n] : 0.f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm0 + 32 * i + acc_row(r, h);
+        if (row >= A.M) continue;
+        float v = acc[i][j][r] + bn;
+        if (ep.act == 1) v = tanhf(v);
+        if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
+        ep.out[(int64_t)row * ep.ldo + n] = v;
+      }
+  }
+}
+
+hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
+  if (A.M <= 0 || ep.N <= 0) return hipSuccess;
+  if (t == Tile::Small) {
+    dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN));
+    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32>), grid, dim3(256), 0, st, A, W.d,
+                       W.Npad, ep);
+  } else {
+    dim3 grid(ceil_div(A.M, kPlainLargeTM), (unsigned)(W.Npad / kPlainLargeTN));
+    hipLaunchKernelGGL((k_gemm_plain<kPlainLargeTM, kPlainLargeTN, 64, 64>), grid, dim3(256), 0, st, A, W.d,
+                       W.Npad, ep);
+  }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- GRU GEMM
+
+struct GruBatch {
+  GruProblem p[2];
+};
+
+template <int TM, int HB, int WM>
+__global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatch batch) {
+  constexpr int TN = 3 * HB;
+  constexpr int NT = (TM / WM) * (HB / 32) * 64;
+  constexpr int FM = WM / 32;
+  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
+  const GruProblem& P = batch.p[blockIdx.z];
+  const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm0 = (wave % (TM / WM)) * WM, wu0 = (wave / (TM / WM)) * 32;
+  f32x16 ar[FM], az[FM], ani[FM], ans[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) ar[i] = az[i] = ani[i] = ans[i] = f32x16{};
+
+  auto chunk = [&](const float* As, const float* Bs, auto state_side) {
+#pragma unroll
+    for (int kg = 0; kg < KC / 8; ++kg) {
+      f32x4 a[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+      const f32x4 br = lds_frag<TN>(Bs, kg, wu0);
+      const f32x4 bz = lds_frag<TN>(Bs, kg, HB + wu0);
+      const f32x4 bn = lds_frag<TN>(Bs, kg, 2 * HB + wu0);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          ar[i] = mfma(a[i][jj], br[jj], ar[i]);
+          az[i] = mfma(a[i][jj], bz[jj], az[i]);
+          if constexpr (decltype(state_side)::value)
+            ans[i] = mfma(a[i][jj], bn[jj], ans[i]);
+          else
+            ani[i] = mfma(a[i][jj], bn[jj], ani[i]);
+        }
+    }
+  };
+  gemm_mainloop<TM, TN, KC, NT>(P.A, P.Wp, P.Npad, m0, n0, lds, [&](const float* As, const float* Bs, int side) {
+    if (side)
+      chunk(As, Bs, std::true_type{});
+    else
+      chunk(As, Bs, std::false_type{});
+  });
+
+  const GruEpi& ep = P.ep;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int H = ep.H;
+  const int j = blockIdx.y * HB + wu0 + l32;
+  if (j >= H) return;
+  const float br = ep.brz[j], bz = ep.brz[H + j], bni = ep.bni[j], bns = ep.bns[j];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm0 + 32 * i + acc_row(r, h);
+      if (row >= P.A.M) continue;
+      float xr = 0.f, xz = 0.f, xn = 0.f;
+      if (ep.xin) {
+        const float* x = ep.xin + (int64_t)row * ep.ldx;
+        xr = x[j];
+        xz = x[H + j];
+        xn = x[2 * H + j];
+      }
+      const float hp = ep.h ? ep.h[(int64_t)row * ep.ldh + j] : 0.f;
+      const float rg = sigmoidf_(ar[i][r] + br + xr);
+      const float zg = sigmoidf_(az[i][r] + bz + xz);
+      const float ng = tanhf(ani[i][r] + bni + xn + rg * (ans[i][r] + bns));
+      float hn = zg * hp + (1.f - zg) * ng;
+      if (ep.mask_len && ep.mask_pos >= ep.mask_len[row]) hn = 0.f;
+      ep.out[(int64_t)row * ep.ldo + j] = hn;
+    }
+}
+
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_t st) {
+  if (nprob < 1 || nprob > 2) return hipErrorInvalidValue;
+  GruBatch b;
+  b.p[0] = probs[0];
+  b.p[1] = nprob > 1 ? probs[1] : probs[0];
+  int M = probs[0].A.M;
+  for (int i = 1; i < nprob; ++i) M = M > probs[i].A.M ? M : probs[i].A.M;
+  if (M <= 0) return hipSuccess;
+  dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
+  hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, 64>), grid, dim3(256), 0, st, b);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------ vocabulary projection
+
+// Tiles are numbered so that the blocks one XCD runs back to back (block ids
+// congruent mod 8) cover all row tiles of one column tile before moving to
+// the next: each weight tile is fetched from HBM once per XCD and then
+// served from that XCD's L2.
+template <int TM, int TN, int WM, int WN>
+__global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_vocab_lse(AOperand A, const float* __restrict__ Wp,
+                                                                          int64_t Npad, const float* __restrict__ bias,
+                                                                          int V, int nMt, int nNt,
+                                                                          float* __restrict__ pm,
+                                                                          float* __restrict__ ps) {
+  constexpr int NT = (TM / WM) * (TN / WN) * 64;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int NWN = TN / WN;
+  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
+  const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
+  const int nt = (slot / nMt) * 8 + xcd, mt = slot % nMt;
+  if (nt >= nNt) return;
+  const int m0 = mt * TM, n0 = nt * TN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm0 = (wave % (TM / WM)) * WM, wni = wave / (TM / WM), wn0 = wni * WN;
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+
+  gemm_mainloop<TM, TN, KC, NT>(A, Wp, Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) {
+#pragma unroll
+    for (int kg = 0; kg < KC / 8; ++kg) {
+      f32x4 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
+    }
+  });
+
+  // Per row of the tile: max and sum of exp over this wave's columns, then
+  // over the waves that share the rows (through LDS; the staging buffers are
+  // free after the main loop's last barrier).
+  const int h = lane >> 5, l32 = lane & 31;
+  float bn[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int n = n0 + wn0 + 32 * j + l32;
+    bn[j] = n < V ? bias[n] : -INFINITY;
+  }
+  float* red = lds;  // [NWN][TM][2]
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) mx = fmaxf(mx, acc[i][j][r] + bn[j]);
+      mx = half_max(mx);
+      float s = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) s += __builtin_amdgcn_exp2f((acc[i][j][r] + bn[j] - mx) * kLog2e);
+      }
+      s = half_sum(s);
+      if (l32 == 0) {
+        const int rl = wm0 + 32 * i + acc_row(r, h);
+        red[(wni * TM + rl) * 2] = mx;
+        red[(wni * TM + rl) * 2 + 1] = s;
+      }
+    }
+  __syncthreads();
+  for (int rl = threadIdx.x; rl < TM; rl += NT) {
+    const int row = m0 + rl;
+    if (row >= A.M) continue;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NWN; ++w) mx = fmaxf(mx, red[(w * TM + rl) * 2]);
+    float s = 0.f;
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < NWN; ++w) {
+        const float mw = red[(w * TM + rl) * 2];
+        if (mw != -INFINITY) s += red[(w * TM + rl) * 2 + 1] * __builtin_amdgcn_exp2f((mw - mx) * kLog2e);
+      }
+    }
+    pm[(int64_t)row * nNt + nt] = mx;
+    ps[(int64_t)row * nNt + nt] = s;
+  }
+}
+
+hipError_t launch_vocab_lse(const AOperand& A, const Packed& W, const float* bias, int V, float* pm, float* ps,
+                            int nNt, hipStream_t st) {
+  if (A.M <= 0) return hipSuccess;
+  const int nMt = ceil_div(A.M, kVocabTM);
+  const int groups = ceil_div(nNt, 8);
+  dim3 grid((unsigned)(groups * 8 * nMt));
+  hipLaunchKernelGGL((k_vocab_lse<kVocabTM, kVocabTN, 64, 64>), grid, dim3(256), 0, st, A, W.d, W.Npad, bias, V,
+                     nMt, nNt, pm, ps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------- partials combine
+
+// One wave per row: merges the per-tile (max, sum) pairs into logZ, scores
+// the requested word with its own dot product t . out_W[:, req] + out_b[req],
+// and checks the row's ids (any out of range: NaN outputs and the flag).
+__global__ __launch_bounds__(256) void k_lse_combine(int B, const float* __restrict__ pm, const float* __restrict__ ps,
+                                                     int nNt, const float* __restrict__ t, int E,
+                                                     const float* __restrict__ Wp, int64_t Npad,
+                                                     const float* __restrict__ bias, int V,
+                                                     const int32_t* __restrict__ req,
+                                                     const int32_t* __restrict__ y_prev,
+                                                     const int32_t* __restrict__ sent_id, int S, float* logp,
+                                                     float* logZ, int* err) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= B) return;
+  const int w = req[row], y = y_prev[row], s = sent_id[row];
+  if (w < 0 || w >= V || y < -1 || y >= V || s < 0 || s >= S) {
+    if (lane == 0) {
+      logp[row] = __builtin_nanf("");
+      if (logZ) logZ[row] = __builtin_nanf("");
+      atomicOr(err, 1);
+    }
+    return;
+  }
+  const float* prm = pm + (int64_t)row * nNt;
+  const float* prs = ps + (int64_t)row * nNt;
+  float mx = -INFINITY;
+  for (int i = lane; i < nNt; i += 64) mx = fmaxf(mx, prm[i]);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int i = lane; i < nNt; i += 64) {
+    const float mi = prm[i];
+    if (mi != -INFINITY) sum += prs[i] * expf(mi - mx);
+  }
+  sum = wave_sum(sum);
+  float dot = 0.f;
+  const float* tr = t + (int64_t)row * E;
+  for (int k4 = lane; k4 < E / 4; k4 += 64) {
+    const f32x4 tv = *(const f32x4*)(tr + 4 * k4);
+    const f32x4 wv = *(const f32x4*)(Wp + ((int64_t)k4 * Npad + w) * 4);
+    dot += tv[0] * wv[0] + tv[1] * wv[1] + tv[2] * wv[2] + tv[3] * wv[3];
+  }
+  dot = wave_sum(dot);
+  if (lane == 0) {
+    const float lz = mx + logf(sum);
+    logp[row] = dot + bias[w] - lz;
+    if (logZ) logZ[row] = lz;
+  }
+}
+
+hipError_t launch_lse_combine(int B, const float* pm, const float* ps, int nNt, const float* t, int E,
+                              const Packed& W, const float* bias, int V, const int32_t* req, const int32_t* y_prev,
+                              const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lse_combine, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, pm, ps, nNt, t, E, W.d, W.Npad, bias,
+                     V, req, y_prev, sent_id, S, logp, logZ, err);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ attention
+
+// One block (4 waves) per row.  Wave w scores source positions w, w+4, ...
+// (each lane covers float4 pieces of the attention width), the block
+// normalises the scores over the row's sentence length, then every thread
+// accumulates float4 pieces of the context over the unmasked positions.
+template <int NQ>
+__global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, const float* __restrict__ q,
+                                                   const float* __restrict__ pctx, const float* __restrict__ ctx,
+                                                   const int32_t* __restrict__ len,
+                                                   const int32_t* __restrict__ sent_id, int S,
+                                                   const float* __restrict__ v, float* __restrict__ c,
+                                                   float* __restrict__ alpha) {
+  __shared__ float e[kMaxTpad];
+  __shared__ float red[8];
+  const int row = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int s = sent_id[row];
+  float* crow = c + (int64_t)row * C;
+  if (s < 0 || s >= S) {  // flagged and NaN-ed by the combine kernel; keep the rest finite
+    for (int k4 = threadIdx.x; k4 < C / 4; k4 += 256) *(f32x4*)(crow + 4 * k4) = zero4();
+    if (alpha)
+      for (int i = threadIdx.x; i < Tpad; i += 256) alpha[(int64_t)row * Tpad + i] = 0.f;
+    return;
+  }
+  const int L = len[s];
+  const int A4 = A / 4;
+  f32x4 qv[NQ], vv[NQ];
+#pragma unroll
+  for (int k = 0; k < NQ; ++k) {
+    const int a4 = lane + 64 * k;
+    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) : zero4();
+    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) : zero4();
+  }
+  const float* P = pctx + (int64_t)s * Tpad * A;
+  for (int i = wave; i < L; i += 4) {
+    float acc = 0.f;
+#pragma unroll
+    for (int k = 0; k < NQ; ++k) {
+      const int a4 = lane + 64 * k;
+      if (a4 < A4) {
+        const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
+        acc += vv[k][0] * tanhf(p[0] + qv[k][0]) + vv[k][1] * tanhf(p[1] + qv[k][1]) +
+               vv[k][2] * tanhf(p[2] + qv[k][2]) + vv[k][3] * tanhf(p[3] + qv[k][3]);
+      }
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) e[i] = acc;
+  }
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int i = threadIdx.x; i < L; i += 256) mx = fmaxf(mx, e[i]);
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float sum = 0.f;
+  for (int i = threadIdx.x; i < L; i += 256) sum += expf(e[i] - mx);
+  sum = wave_sum(sum);
+  if (lane == 0) red[4 + wave] = sum;
+  __syncthreads();
+  const float inv = 1.f / ((red[4] + red[5]) + (red[6] + red[7]));
+  for (int i = threadIdx.x; i < L; i += 256) e[i] = expf(e[i] - mx) * inv;
+  if (alpha)
+    for (int i = threadIdx.x; i < Tpad; i += 256) alpha[(int64_t)row * Tpad + i] = 0.f;
+  __syncthreads();
+  if (alpha)
+    for (int i = threadIdx.x; i < L; i += 256) alpha[(int64_t)row * Tpad + i] = e[i];
+  const float* X = ctx + (int64_t)s * Tpad * C;
+  for (int k4 = threadIdx.x; k4 < C / 4; k4 += 256) {
+    f32x4 acc = zero4();
+    for (int i = 0; i < L; ++i) {
+      const f32x4 x = *(const f32x4*)(X + (int64_t)i * C + 4 * k4);
+      const float a = e[i];
+      acc[0] += a * x[0];
+      acc[1] += a * x[1];
+      acc[2] += a * x[2];
+      acc[3] += a * x[3];
+    }
+    *(f32x4*)(crow + 4 * k4) = acc;
+  }
+}
+
+hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+                            const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
+                            hipStream_t st) {
+  if (B <= 0) return hipSuccess;
+  const int nq = ceil_div(A, 256);
+  if (nq <= 1)
+    hipLaunchKernelGGL(k_attention<1>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
+                       alpha);
+  else if (nq <= 2)
+    hipLaunchKernelGGL(k_attention<2>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
+                       alpha);
+  else if (nq <= 4)
+    hipLaunchKernelGGL(k_attention<4>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
+                       alpha);
+  else if (nq <= 8)
+    hipLaunchKernelGGL(k_attention<8>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
+                       alpha);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ source helpers
+
+__global__ void k_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src, int* err) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)S * Tpad) return;
+  const int s = (int)(i / Tpad), p = (int)(i % Tpad);
+  if (p < len[s] && (ids[i] < 0 || ids[i] >= V_src)) atomicOr(err, 1);
+}
+
+hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src, int* err,
+                                hipStream_t st) {
+  const int64_t n = (int64_t)S * Tpad;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_check_src_ids, dim3(ceil_div(n, 256)), dim3(256), 0, st, S, Tpad, ids, len, V_src, err);
+  return hipGetLastError();
+}
+
+__global__ void k_masked_copy(int S, int Tpad, int C, const float* src, const int32_t* len, float* dst) {
+  const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int C4 = C / 4;
+  if (i4 >= (int64_t)S * Tpad * C4) return;
+  const int64_t pos = i4 / C4;
+  const int s = (int)(pos / Tpad), p = (int)(pos % Tpad);
+  ((f32x4*)dst)[i4] = p < len[s] ? ((const f32x4*)src)[i4] : zero4();
+}
+
+hipError_t launch_masked_copy(int S, int Tpad, int C, const float* src, const int32_t* len, float* dst,
+                              hipStream_t st) {
+  const int64_t n = (int64_t)S * Tpad * (C / 4);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_masked_copy, dim3(ceil_div(n, 256)), dim3(256), 0, st, S, Tpad, C, src, len, dst);
+  return hipGetLastError();
+}
+
+// mean over the unmasked positions of each sentence: one block per sentence.
+__global__ void k_masked_mean(int Tpad, int C, const float* ctx, const int32_t* len, float* mean) {
+  const int s = blockIdx.x, L = len[s];
+  const float* X = ctx + (int64_t)s * Tpad * C;
+  for (int k = threadIdx.x; k < C; k += blockDim.x) {
+    float acc = 0.f;
+    for (int i = 0; i < L; ++i) acc += X[(int64_t)i * C + k];
+    mean[(int64_t)s * C + k] = acc / (float)L;
+  }
+}
+
+hipError_t launch_masked_mean(int S, int Tpad, int C, const float* ctx, const int32_t* len, float* mean,
+                              hipStream_t st) {
+  if (S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_masked_mean, dim3(S), dim3(256), 0, st, Tpad, C, ctx, len, mean);
+  return hipGetLastError();
+}
+
+}  // namespace nmt
