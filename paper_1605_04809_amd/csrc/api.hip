@@ -66,7 +66,6 @@ struct nmt_model {
         *out_b = nullptr;
   GruBias enc_bias, g1_bias, g2_bias;
   int* err = nullptr;  // sticky device error flag
-  int nNt = 0;         // vocabulary column tiles
   // event timing of the step's phases (nmt_profile.h); not thread-safe
   std::vector<hipEvent_t> prof_events;  // (NMT_NUM_PHASES + 1) per timed step
   int prof_max = 0, prof_used = 0;
@@ -193,7 +192,8 @@ nmt_status hip_fail(hipError_t e, const char* what) {
 
 // Workspace layout of one step (offsets in bytes, 256-aligned).
 struct WsLayout {
-  size_t s1, q, c, t, pm, ps, total;
+  size_t s1, q, c, t, part, total;
+  int nS;  // vocabulary slices
 };
 
 WsLayout ws_layout(const nmt_model* m, int64_t B) {
@@ -209,10 +209,9 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * 2 * d.H * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.pm = off;
-  off += al((size_t)B * m->nNt * 4);
-  L.ps = off;
-  off += al((size_t)B * m->nNt * 4);
+  L.nS = vocab_slices((int)B, m->out.Npad);
+  L.part = off;
+  off += al((size_t)B * L.nS * sizeof(float2));
   L.total = off;
   return L;
 }
@@ -269,6 +268,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
     return fail(NMT_EINVAL, "dimensions must be positive");
   if (d.E % 4 || d.H % 4 || d.A % 4) return fail(NMT_EINVAL, "E, H and A must be multiples of 4");
   if (d.A > 8 * 256) return fail(NMT_EINVAL, "A must be at most 2048");
+  if (round_up(d.E, KC) > kVocabMaxKpad) return fail(NMT_EINVAL, "E must be at most %d", kVocabMaxKpad);
   if (d.wtype != NMT_F32) return fail(NMT_EINVAL, "weight type %d is not supported", d.wtype);
   const float* const* wp = (const float* const*)w;
   for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
@@ -327,7 +327,6 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
     delete m;
     return hip_fail(e, "nmt_model_create");
   }
-  m->nNt = (int)(m->out.Npad / kVocabTN);
   *out = m;
   return ok();
 }
@@ -480,8 +479,7 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   float* q = (float*)(ws + L.q);
   float* c = (float*)(ws + L.c);
   float* t = (float*)(ws + L.t);
-  float* pm = (float*)(ws + L.pm);
-  float* ps = (float*)(ws + L.ps);
+  float2* part = (float2*)(ws + L.part);
   const ASeg x_seg = make_seg(m->emb_tgt, E, E, 0, d_y_prev, V);  // E_i: embedding rows of the previous words
   hipEvent_t* ev = nullptr;
   if (m->prof_on && m->prof_used < m->prof_max) ev = &m->prof_events[(size_t)(m->prof_used++) * (NMT_NUM_PHASES + 1)];
@@ -528,10 +526,10 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   }
   mark(NMT_PHASE_READOUT + 1);
   // vocabulary projection with per-tile log-sum-exp, then the combine
-  if (e == hipSuccess) e = launch_vocab_lse(make_a(B, {make_seg(t, E, E, 0)}), m->out, m->out_b, V, pm, ps, m->nNt, st);
+  if (e == hipSuccess) e = launch_vocab_lse(t, B, E, m->out, m->out_b, V, part, L.nS, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
-    e = launch_lse_combine(B, pm, ps, m->nNt, t, E, m->out, m->out_b, V, d_req, d_y_prev, d_sent_id, src->S, d_logp,
+    e = launch_lse_combine(B, part, L.nS, t, E, m->out, m->out_b, V, d_req, d_y_prev, d_sent_id, src->S, d_logp,
                            d_logZ, m->err, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);

@@ -16,7 +16,8 @@ constexpr int kMaxTpad = 1024;     // attention keeps one score per source posit
 constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;
 constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
 constexpr int kGruTM = 128, kGruHB = 64;       // HB hidden units -> 3*HB packed columns
-constexpr int kVocabTM = 128, kVocabTN = 128;
+constexpr int kVocabTN = 32;                    // packing granularity of the output weights
+constexpr int kVocabMaxKpad = 576;              // padded E the vocabulary kernel keeps in LDS
 
 // A weight matrix packed for one kernel family: [Kpad/4][Npad][4] fp32.
 struct Packed {
@@ -66,12 +67,14 @@ struct GruProblem {
 // Launchers (all asynchronous on `st`).
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_t st);
-hipError_t launch_vocab_lse(const AOperand& A, const Packed& W, const float* bias, int V, float* pm,
-                            float* ps, int nNt, hipStream_t st);
-hipError_t launch_lse_combine(int B, const float* pm, const float* ps, int nNt, const float* t, int E,
-                              const Packed& W, const float* bias, int V, const int32_t* req,
-                              const int32_t* y_prev, const int32_t* sent_id, int S, float* logp,
-                              float* logZ, int* err, hipStream_t st);
+// Number of vocabulary slices (partials per row) for M rows.
+int vocab_slices(int M, int64_t Npad);
+hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
+                            int nS, hipStream_t st);
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
+                              const float* bias, int V, const int32_t* req, const int32_t* y_prev,
+                              const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
+                              hipStream_t st);
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx,
                             const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, hipStream_t st);

@@ -176,118 +176,179 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_
 
 // ------------------------------------------------ vocabulary projection
 
-// Tiles are numbered so that the blocks one XCD runs back to back (block ids
-// congruent mod 8) cover all row tiles of one column tile before moving to
-// the next: each weight tile is fetched from HBM once per XCD and then
-// served from that XCD's L2.
-template <int TM, int TN, int WM, int WN>
-__global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_vocab_lse(AOperand A, const float* __restrict__ Wp,
-                                                                          int64_t Npad, const float* __restrict__ bias,
-                                                                          int V, int nMt, int nNt,
-                                                                          float* __restrict__ pm,
-                                                                          float* __restrict__ ps) {
-  constexpr int NT = (TM / WM) * (TN / WN) * 64;
-  constexpr int FM = WM / 32, FN = WN / 32;
-  constexpr int NWN = TN / WN;
-  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
+// Streaming vocabulary projection with an online log-sum-exp.
+//
+// A block owns VTM = 64 rows and one slice of the vocabulary.  Its rows of
+// the readout t stay in LDS for the whole kernel ([Kpad/4][64][4] floats,
+// 128 KB at E = 500); the packed output weights stream straight from HBM/L2
+// into registers, four k groups ahead, so the main loop has no barrier.
+// Wave w of the 8 takes the slice's 32-column blocks w, w+8, ...; each lane
+// keeps a running (max, sum of exp) for each of its 32 row slots, and the
+// 32 lanes and 8 waves are merged once at the end.  One (max, sum) pair per
+// row and slice goes to HBM as float2 [slice][row]; the logits never do.
+//
+// Slices are spread over XCDs: blocks with ids congruent mod 8 run on one
+// XCD, and that XCD takes slices xcd, xcd+8, ... for every row tile, so the
+// row tiles of a slice read the same weights from that XCD's L2 and the
+// weights cross HBM once.
+constexpr int VTM = 64;           // rows per block
+constexpr int VNW = 8;            // waves per block
+constexpr int VKMAX = 576;        // max padded E held in LDS (64 x 576 x 4 B = 144 KB)
+constexpr int VPF = 4;            // k groups of weight fragments in flight per wave
+
+__global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E, int Kpad,
+                                                        const float* __restrict__ Wp, int64_t Npad,
+                                                        const float* __restrict__ bias, int V, int nM, int nS,
+                                                        float2* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) float As[VTM * VKMAX];
+  __shared__ float red[VNW][VTM][2];
   const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
-  const int nt = (slot / nMt) * 8 + xcd, mt = slot % nMt;
-  if (nt >= nNt) return;
-  const int m0 = mt * TM, n0 = nt * TN;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm0 = (wave % (TM / WM)) * WM, wni = wave / (TM / WM), wn0 = wni * WN;
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+  const int slice = (slot / nM) * 8 + xcd, mt = slot % nM;
+  if (slice >= nS) return;
+  const int m0 = mt * VTM;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
 
-  gemm_mainloop<TM, TN, KC, NT>(A, Wp, Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) {
-#pragma unroll
-    for (int kg = 0; kg < KC / 8; ++kg) {
-      f32x4 a[FM], b[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
-    }
-  });
-
-  // Per row of the tile: max and sum of exp over this wave's columns, then
-  // over the waves that share the rows (through LDS; the staging buffers are
-  // free after the main loop's last barrier).
-  const int h = lane >> 5, l32 = lane & 31;
-  float bn[FN];
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = n0 + wn0 + 32 * j + l32;
-    bn[j] = n < V ? bias[n] : -INFINITY;
+  // stationary A tile: As[kq][m][4] = t[m0 + m][4kq .. 4kq+3]
+  const int KQ = Kpad / 4;
+  for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
+    const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
+    f32x4 v = zero4();
+    if (row < M && 4 * kq < E) v = *(const f32x4*)(t + (int64_t)row * E + 4 * kq);
+    *(f32x4*)(As + (kq * VTM + m) * 4) = v;
   }
-  float* red = lds;  // [NWN][TM][2]
+  __syncthreads();
+
+  // this slice's 32-column blocks, balanced over the slices
+  const int NB = (int)(Npad / 32);
+  const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
+  const int NKG = Kpad / 8;  // k groups per column block (a multiple of VPF)
+  const int nblk = cb_end - cb_begin > wave ? (cb_end - cb_begin - wave + VNW - 1) / VNW : 0;
+
+  float run_m[2][16], run_s[2][16];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      float mx = -INFINITY;
+      run_m[i][r] = -INFINITY;
+      run_s[i][r] = 0.f;
+    }
+
+  // Weight fragments are read in (column block, k group) order through a
+  // cursor; fragment p of the ring always holds step q with q % VPF == p.
+  const int total = nblk * NKG;
+  const int64_t kstep = 2 * Npad * 4;  // floats between k groups
+  int pcb = cb_begin + wave, pkg = 0, issued = 0;
+  const float* pptr = Wp + ((int64_t)h * Npad + (int64_t)pcb * 32 + l32) * 4;
+  auto load_next = [&]() {
+    const f32x4 v = *(const f32x4*)pptr;
+    ++issued;
+    if (++pkg == NKG) {
+      pkg = 0;
+      pcb += VNW;
+      pptr = Wp + ((int64_t)h * Npad + (int64_t)pcb * 32 + l32) * 4;
+    } else {
+      pptr += kstep;
+    }
+    return v;
+  };
+  f32x4 ring[VPF];
 #pragma unroll
-      for (int j = 0; j < FN; ++j) mx = fmaxf(mx, acc[i][j][r] + bn[j]);
-      mx = half_max(mx);
-      float s = 0.f;
-      if (mx != -INFINITY) {
+  for (int p = 0; p < VPF; ++p) ring[p] = issued < total ? load_next() : zero4();
+
+  for (int q0 = 0; q0 < total; q0 += NKG) {
+    f32x16 acc0 = f32x16{}, acc1 = f32x16{};
+    for (int kg0 = 0; kg0 < NKG; kg0 += VPF) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j) s += __builtin_amdgcn_exp2f((acc[i][j][r] + bn[j] - mx) * kLog2e);
+      for (int p = 0; p < VPF; ++p) {
+        const int kg = kg0 + p;
+        const f32x4 b = ring[p];
+        if (issued < total) ring[p] = load_next();
+        const f32x4 a0 = *(const f32x4*)(As + ((2 * kg + h) * VTM + l32) * 4);
+        const f32x4 a1 = *(const f32x4*)(As + ((2 * kg + h) * VTM + 32 + l32) * 4);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          acc0 = mfma(a0[jj], b[jj], acc0);
+          acc1 = mfma(a1[jj], b[jj], acc1);
+        }
       }
-      s = half_sum(s);
+    }
+    // fold this 32-column block into the running (max, sum) of each row slot
+    const int n = (cb_begin + wave + VNW * (int)(q0 / NKG)) * 32 + l32;
+    if (n < V) {
+      const float bn = bias[n];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float z0 = acc0[r] + bn, z1 = acc1[r] + bn;
+        const float m0n = fmaxf(run_m[0][r], z0), m1n = fmaxf(run_m[1][r], z1);
+        run_s[0][r] = run_s[0][r] * __builtin_amdgcn_exp2f((run_m[0][r] - m0n) * kLog2e) +
+                      __builtin_amdgcn_exp2f((z0 - m0n) * kLog2e);
+        run_s[1][r] = run_s[1][r] * __builtin_amdgcn_exp2f((run_m[1][r] - m1n) * kLog2e) +
+                      __builtin_amdgcn_exp2f((z1 - m1n) * kLog2e);
+        run_m[0][r] = m0n;
+        run_m[1][r] = m1n;
+      }
+    }
+  }
+
+  // merge the 32 lanes of each half-wave (they hold different columns of the same rows)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float mx = half_max(run_m[i][r]);
+      const float s = mx == -INFINITY ? 0.f : run_s[i][r] * __builtin_amdgcn_exp2f((run_m[i][r] - mx) * kLog2e);
+      const float st = half_sum(s);
       if (l32 == 0) {
-        const int rl = wm0 + 32 * i + acc_row(r, h);
-        red[(wni * TM + rl) * 2] = mx;
-        red[(wni * TM + rl) * 2 + 1] = s;
+        const int rl = 32 * i + acc_row(r, h);
+        red[wave][rl][0] = mx;
+        red[wave][rl][1] = st;
       }
     }
   __syncthreads();
-  for (int rl = threadIdx.x; rl < TM; rl += NT) {
-    const int row = m0 + rl;
-    if (row >= A.M) continue;
+  // merge the waves and write this slice's partial for each row
+  if (threadIdx.x < VTM) {
+    const int rl = threadIdx.x, row = m0 + rl;
     float mx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < NWN; ++w) mx = fmaxf(mx, red[(w * TM + rl) * 2]);
+    for (int w = 0; w < VNW; ++w) mx = fmaxf(mx, red[w][rl][0]);
     float s = 0.f;
     if (mx != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < NWN; ++w) {
-        const float mw = red[(w * TM + rl) * 2];
-        if (mw != -INFINITY) s += red[(w * TM + rl) * 2 + 1] * __builtin_amdgcn_exp2f((mw - mx) * kLog2e);
+      for (int w = 0; w < VNW; ++w) {
+        const float mw = red[w][rl][0];
+        if (mw != -INFINITY) s += red[w][rl][1] * __builtin_amdgcn_exp2f((mw - mx) * kLog2e);
       }
     }
-    pm[(int64_t)row * nNt + nt] = mx;
-    ps[(int64_t)row * nNt + nt] = s;
+    if (row < M) part[(int64_t)slice * M + row] = float2{mx, s};
   }
 }
 
-hipError_t launch_vocab_lse(const AOperand& A, const Packed& W, const float* bias, int V, float* pm, float* ps,
-                            int nNt, hipStream_t st) {
-  if (A.M <= 0) return hipSuccess;
-  const int nMt = ceil_div(A.M, kVocabTM);
-  const int groups = ceil_div(nNt, 8);
-  dim3 grid((unsigned)(groups * 8 * nMt));
-  hipLaunchKernelGGL((k_vocab_lse<kVocabTM, kVocabTN, 64, 64>), grid, dim3(256), 0, st, A, W.d, W.Npad, bias, V,
-                     nMt, nNt, pm, ps);
+int vocab_slices(int M, int64_t Npad) {
+  const int nM = ceil_div(M, VTM);
+  int nS = 8 * ceil_div(ceil_div(256, nM), 8);  // fill the 256 CUs (one block per CU)
+  const int NB = (int)(Npad / 32);
+  while (nS > 8 && nS > NB) nS -= 8;
+  return nS;
+}
+
+hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
+                            int nS, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (W.Kpad > VKMAX || W.Kpad % (8 * VPF)) return hipErrorInvalidValue;
+  const int nM = ceil_div(M, VTM);
+  dim3 grid((unsigned)(nS / 8 * 8 * nM));
+  hipLaunchKernelGGL(k_vocab_lse, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, W.d, W.Npad, bias, V, nM, nS,
+                     part);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------- partials combine
 
-// One wave per row: merges the per-tile (max, sum) pairs into logZ, scores
+// One wave per row: merges the per-slice (max, sum) pairs into logZ, scores
 // the requested word with its own dot product t . out_W[:, req] + out_b[req],
 // and checks the row's ids (any out of range: NaN outputs and the flag).
-__global__ __launch_bounds__(256) void k_lse_combine(int B, const float* __restrict__ pm, const float* __restrict__ ps,
-                                                     int nNt, const float* __restrict__ t, int E,
+__global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __restrict__ part, int nS,
+                                                     const float* __restrict__ t, int E,
                                                      const float* __restrict__ Wp, int64_t Npad,
                                                      const float* __restrict__ bias, int V,
                                                      const int32_t* __restrict__ req,
@@ -305,15 +366,13 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float* __restr
     }
     return;
   }
-  const float* prm = pm + (int64_t)row * nNt;
-  const float* prs = ps + (int64_t)row * nNt;
   float mx = -INFINITY;
-  for (int i = lane; i < nNt; i += 64) mx = fmaxf(mx, prm[i]);
+  for (int i = lane; i < nS; i += 64) mx = fmaxf(mx, part[(int64_t)i * B + row].x);
   mx = wave_max(mx);
   float sum = 0.f;
-  for (int i = lane; i < nNt; i += 64) {
-    const float mi = prm[i];
-    if (mi != -INFINITY) sum += prs[i] * expf(mi - mx);
+  for (int i = lane; i < nS; i += 64) {
+    const float2 p = part[(int64_t)i * B + row];
+    if (p.x != -INFINITY) sum += p.y * expf(p.x - mx);
   }
   sum = wave_sum(sum);
   float dot = 0.f;
@@ -331,12 +390,12 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float* __restr
   }
 }
 
-hipError_t launch_lse_combine(int B, const float* pm, const float* ps, int nNt, const float* t, int E,
-                              const Packed& W, const float* bias, int V, const int32_t* req, const int32_t* y_prev,
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
+                              const float* bias, int V, const int32_t* req, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
   if (B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lse_combine, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, pm, ps, nNt, t, E, W.d, W.Npad, bias,
-                     V, req, y_prev, sent_id, S, logp, logZ, err);
+  hipLaunchKernelGGL(k_lse_combine, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E, W.d, W.Npad, bias, V,
+                     req, y_prev, sent_id, S, logp, logZ, err);
   return hipGetLastError();
 }
 
