@@ -206,7 +206,9 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   const int slice = (slot / nM) * 8 + xcd, mt = slot % nM;
   if (slice >= nS) return;
   const int m0 = mt * VTM;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
+  // the wave index is uniform across the wave: keep the loop control scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
 
   // stationary A tile: As[kq][m][4] = t[m0 + m][4kq .. 4kq+3]
   const int KQ = Kpad / 4;
@@ -234,26 +236,29 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
     }
 
   // Weight fragments are read in (column block, k group) order through a
-  // cursor; fragment p of the ring always holds step q with q % VPF == p.
+  // scalar cursor; fragment p of the ring always holds step q with
+  // q % VPF == p.  Loads past this wave's last step re-read fragment 0 of
+  // the matrix (always in bounds) so that no load sits behind a branch.
   const int total = nblk * NKG;
-  const int64_t kstep = 2 * Npad * 4;  // floats between k groups
+  const float* wlane = Wp + ((int64_t)h * Npad + l32) * 4;
   int pcb = cb_begin + wave, pkg = 0, issued = 0;
-  const float* pptr = Wp + ((int64_t)h * Npad + (int64_t)pcb * 32 + l32) * 4;
   auto load_next = [&]() {
-    const f32x4 v = *(const f32x4*)pptr;
+    const int64_t off = issued < total ? ((int64_t)(2 * pkg) * Npad + (int64_t)pcb * 32) * 4 : 0;
     ++issued;
     if (++pkg == NKG) {
       pkg = 0;
       pcb += VNW;
-      pptr = Wp + ((int64_t)h * Npad + (int64_t)pcb * 32 + l32) * 4;
-    } else {
-      pptr += kstep;
     }
-    return v;
+    return *(const f32x4*)(wlane + off);
   };
   f32x4 ring[VPF];
 #pragma unroll
-  for (int p = 0; p < VPF; ++p) ring[p] = issued < total ? load_next() : zero4();
+  for (int p = 0; p < VPF; ++p) ring[p] = load_next();
+  // A fragments ping-pong between an even and an odd register set (VPF is
+  // even), so neither ring needs register moves at the loop back-edge.
+  const float* arow = As + (h * VTM + l32) * 4;  // + 2*kg*VTM*4 per k group
+  f32x4 ae0 = *(const f32x4*)arow, ae1 = *(const f32x4*)(arow + 32 * 4), ao0, ao1;
+  static_assert(VPF % 2 == 0, "even/odd fragment sets");
 
   for (int q0 = 0; q0 < total; q0 += NKG) {
     f32x16 acc0 = f32x16{}, acc1 = f32x16{};
@@ -261,15 +266,26 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
 #pragma unroll
       for (int p = 0; p < VPF; ++p) {
         const int kg = kg0 + p;
-        const f32x4 b = ring[p];
-        if (issued < total) ring[p] = load_next();
-        const f32x4 a0 = *(const f32x4*)(As + ((2 * kg + h) * VTM + l32) * 4);
-        const f32x4 a1 = *(const f32x4*)(As + ((2 * kg + h) * VTM + 32 + l32) * 4);
+        const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next column block)
+        const float* an = arow + kn * 2 * VTM * 4;
+        f32x4 a0, a1;
+        if (p % 2 == 0) {
+          ao0 = *(const f32x4*)an;
+          ao1 = *(const f32x4*)(an + 32 * 4);
+          a0 = ae0;
+          a1 = ae1;
+        } else {
+          ae0 = *(const f32x4*)an;
+          ae1 = *(const f32x4*)(an + 32 * 4);
+          a0 = ao0;
+          a1 = ao1;
+        }
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          acc0 = mfma(a0[jj], b[jj], acc0);
-          acc1 = mfma(a1[jj], b[jj], acc1);
+          acc0 = mfma(a0[jj], ring[p][jj], acc0);
+          acc1 = mfma(a1[jj], ring[p][jj], acc1);
         }
+        ring[p] = load_next();  // refill the slot just consumed, VPF steps ahead
       }
     }
     // fold this 32-column block into the running (max, sum) of each row slot
