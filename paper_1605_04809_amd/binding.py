@@ -14,7 +14,8 @@ from typing import Dict, Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libnmt.so")
+# NMT_LIBRARY may point at another build of the same library (tuning sweeps).
+LIB_PATH = os.environ.get("NMT_LIBRARY") or os.path.join(HERE, "libnmt.so")
 
 NMT_OK, NMT_EINVAL, NMT_ENOMEM, NMT_EDEVICE, NMT_ERANGE, NMT_EWORKSPACE = 0, -1, -2, -3, -4, -5
 NMT_F32, NMT_BF16 = 0, 1

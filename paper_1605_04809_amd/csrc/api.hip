@@ -190,10 +190,25 @@ nmt_status hip_fail(hipError_t e, const char* what) {
   return fail(NMT_EDEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
+// K split of a small-tile plain GEMM: enough blocks for about four per CU,
+// at least four K chunks per block.
+#ifndef NMT_SPLITK_BLOCKS
+#define NMT_SPLITK_BLOCKS 1024
+#endif
+int plain_ksplit(int M, int N, int K_total) {
+  const int tiles = ceil_div(M, kPlainSmallTM) * ceil_div(N, kPlainSmallTN);
+  const int nc = ceil_div(K_total, KC);
+  int ks = ceil_div(NMT_SPLITK_BLOCKS, tiles);
+  if (ks > nc / 4) ks = nc / 4;
+  if (ks > 8) ks = 8;
+  return ks < 1 ? 1 : ks;
+}
+
 // Workspace layout of one step (offsets in bytes, 256-aligned).
 struct WsLayout {
-  size_t s1, q, c, t, part, total;
-  int nS;  // vocabulary slices
+  size_t s1, q, c, t, part, kpart, total;
+  int nS;           // vocabulary slices
+  int ks_q, ks_ro;  // K splits of the query and readout GEMMs
 };
 
 WsLayout ws_layout(const nmt_model* m, int64_t B) {
@@ -212,6 +227,14 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   L.nS = vocab_slices((int)B, m->out.Npad);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
+  L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
+
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H);
+  size_t kp = 0;
+  if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
+  if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
+  L.kpart = off;
+  off += al(kp * 4);
   L.total = off;
   return L;
 }
@@ -499,7 +522,7 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   mark(NMT_PHASE_GRU1 + 1);
   // attention query q = s1 att_Wq
   if (e == hipSuccess) {
-    PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1};
+    PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1, L.ks_q, (float*)(ws + L.kpart)};
     e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(s1, H, H, 0)}), m->att_Wq, ep, st);
   }
   mark(NMT_PHASE_QUERY + 1);
@@ -520,7 +543,7 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   mark(NMT_PHASE_GRU2 + 1);
   // readout t = tanh(s_new Ws + x Wy + c Wc + b)
   if (e == hipSuccess) {
-    PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1};
+    PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
     e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(d_s_new, H, H, 0), x_seg, make_seg(c, C, C, 0)}), m->ro,
                           ep, st);
   }

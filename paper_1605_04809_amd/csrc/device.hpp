@@ -51,6 +51,30 @@ struct AOperand {
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Segment i of A, field by field through uniform selects: indexing the
+// by-value kernel argument (or copying whole segments conditionally) with a
+// runtime index makes the compiler spill it to scratch memory.
+template <class T>
+__device__ __forceinline__ T sel3(int i, T a, T b, T c) {
+  return i == 0 ? a : (i == 1 ? b : c);
+}
+__device__ __forceinline__ ASeg seg_at(const AOperand& A, int i) {
+  ASeg s;
+  s.p = sel3(i, A.seg[0].p, A.seg[1].p, A.seg[2].p);
+  s.gather = sel3(i, A.seg[0].gather, A.seg[1].gather, A.seg[2].gather);
+  s.gmax = sel3(i, A.seg[0].gmax, A.seg[1].gmax, A.seg[2].gmax);
+  s.ld = sel3(i, A.seg[0].ld, A.seg[1].ld, A.seg[2].ld);
+  s.K = sel3(i, A.seg[0].K, A.seg[1].K, A.seg[2].K);
+  s.nchunk = sel3(i, A.seg[0].nchunk, A.seg[1].nchunk, A.seg[2].nchunk);
+  s.side = sel3(i, A.seg[0].side, A.seg[1].side, A.seg[2].side);
+  return s;
+}
+
+__device__ __forceinline__ int total_chunks(const AOperand& A) {
+  return (A.nseg > 0 ? A.seg[0].nchunk : 0) + (A.nseg > 1 ? A.seg[1].nchunk : 0) +
+         (A.nseg > 2 ? A.seg[2].nchunk : 0);
+}
+
 __device__ __forceinline__ const float* seg_row(const ASeg& s, int row, int M) {
   if (row >= M) return nullptr;
   if (s.gather) {
@@ -119,46 +143,50 @@ __device__ __forceinline__ f32x4 lds_frag(const float* S, int kg, int r0) {
   return *(const f32x4*)(S + ((2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)) * 4);
 }
 
-// The generic main loop: walks every chunk of every A segment, staging the
-// next chunk while `compute(As, Bs, side)` runs on the current one.
+// The generic main loop: walks chunks [c_begin, c_end) of the A segments
+// (all chunks by default), staging the next chunk while
+// `compute(As, Bs, side)` runs on the current one.  Chunk c covers packed
+// weight rows c*KC .. c*KC+KC-1, whichever segment it falls in.
 template <int TM, int TN, int KC, int NT, class Compute>
 __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const float* __restrict__ Wp, int64_t Npad,
-                                              int m0, int n0, float* lds, Compute&& compute) {
+                                              int m0, int n0, float* lds, Compute&& compute, int c_begin = 0,
+                                              int c_end = 1 << 30) {
   constexpr int ASZ = TM * KC, BSZ = TN * KC;
   float* As[2] = {lds, lds + ASZ + BSZ};
   float* Bs[2] = {lds + ASZ, lds + 2 * ASZ + BSZ};
   Stager<TM, TN, KC, NT> st;
   const int row = m0 + (int)threadIdx.x % TM;
 
-  int nc = 0;
-  for (int s = 0; s < A.nseg; ++s) nc += A.seg[s].nchunk;
-  if (nc == 0) return;
+  const int nc = total_chunks(A);
+  if (c_end > nc) c_end = nc;
+  if (c_begin >= c_end) return;
 
-  int seg = 0, ch = 0;
-  while (A.seg[seg].nchunk == 0) ++seg;
-  const float* arow = seg_row(A.seg[seg], row, A.M);
-  st.load(arow, A.seg[seg].K, 0, Wp, Npad, 0, n0);
+  int seg = 0, ch = c_begin;
+  ASeg sg = seg_at(A, 0);
+  while (ch >= sg.nchunk) {
+    ch -= sg.nchunk;
+    sg = seg_at(A, ++seg);
+  }
+  const float* arow = seg_row(sg, row, A.M);
+  st.load(arow, sg.K, ch * KC, Wp, Npad, (int64_t)c_begin * (KC / 4), n0);
   st.store(As[0], Bs[0]);
   __syncthreads();
 
-  for (int c = 0; c < nc; ++c) {
-    int nseg = seg, nch = ch + 1;
-    const float* narow = arow;
-    const bool more = c + 1 < nc;
+  for (int c = c_begin; c < c_end; ++c) {
+    const bool more = c + 1 < c_end;
+    const int buf = (c - c_begin) & 1;
+    const int side = sg.side;
     if (more) {
-      if (nch == A.seg[nseg].nchunk) {
-        nch = 0;
-        do { ++nseg; } while (A.seg[nseg].nchunk == 0);
-        narow = seg_row(A.seg[nseg], row, A.M);
+      if (++ch == sg.nchunk) {
+        ch = 0;
+        do { sg = seg_at(A, ++seg); } while (sg.nchunk == 0);
+        arow = seg_row(sg, row, A.M);
       }
-      st.load(narow, A.seg[nseg].K, nch * KC, Wp, Npad, (int64_t)(c + 1) * (KC / 4), n0);
+      st.load(arow, sg.K, ch * KC, Wp, Npad, (int64_t)(c + 1) * (KC / 4), n0);
     }
-    compute(As[c & 1], Bs[c & 1], A.seg[seg].side);
-    if (more) st.store(As[(c + 1) & 1], Bs[(c + 1) & 1]);
+    compute(As[buf], Bs[buf], side);
+    if (more) st.store(As[buf ^ 1], Bs[buf ^ 1]);
     __syncthreads();
-    seg = nseg;
-    ch = nch;
-    arow = narow;
   }
 }
 

@@ -15,7 +15,15 @@ constexpr int kMaxTpad = 1024;     // attention keeps one score per source posit
 // Tile shapes (rows x packed columns) of the kernel families.
 constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;
 constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
-constexpr int kGruTM = 128, kGruHB = 64;       // HB hidden units -> 3*HB packed columns
+// GRU tile: TM rows x HB hidden units (3*HB packed columns), waves of WM rows
+// x 32 units.  Overridable at compile time for tuning sweeps.
+#ifndef NMT_GRU_TM
+#define NMT_GRU_TM 128
+#endif
+#ifndef NMT_GRU_WM
+#define NMT_GRU_WM 32
+#endif
+constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabMaxKpad = 576;              // padded E the vocabulary kernel keeps in LDS
 
@@ -30,7 +38,10 @@ struct Packed {
 enum class Tile { Small, Large };
 
 // Epilogue of the plain GEMM: out = act(acc + bias); rows with
-// (m % mask_T) >= mask_len[m / mask_T] are written as zeros.
+// (m % mask_T) >= mask_len[m / mask_T] are written as zeros.  With
+// ksplit > 1 the K chunks are split over ksplit blocks, which write raw sums
+// to part [ksplit][M][N]; a reduce kernel then adds them in a fixed order
+// and applies the epilogue (deterministic, no atomics).
 struct PlainEpi {
   float* out;
   int64_t ldo;
@@ -39,6 +50,8 @@ struct PlainEpi {
   int act;            // 0: identity, 1: tanh
   const int32_t* mask_len;
   int32_t mask_T;
+  int32_t ksplit = 1;
+  float* part = nullptr;
 };
 
 // Epilogue of the GRU gate GEMM (see device.hpp for the cell).

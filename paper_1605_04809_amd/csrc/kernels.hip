@@ -32,24 +32,49 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
 
-  gemm_mainloop<TM, TN, KC, NT>(A, Wp, Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) {
+  int c_begin = 0, c_end = 1 << 30;
+  if (ep.ksplit > 1) {
+    const int nc = total_chunks(A);
+    c_begin = (int)((int64_t)nc * blockIdx.z / ep.ksplit);
+    c_end = (int)((int64_t)nc * (blockIdx.z + 1) / ep.ksplit);
+  }
+  gemm_mainloop<TM, TN, KC, NT>(
+      A, Wp, Npad, m0, n0, lds,
+      [&](const float* As, const float* Bs, int) {
 #pragma unroll
-    for (int kg = 0; kg < KC / 8; ++kg) {
-      f32x4 a[FM], b[FN];
+        for (int kg = 0; kg < KC / 8; ++kg) {
+          f32x4 a[FM], b[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+          for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
+          for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
+          for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
-    }
-  });
+              for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
+        }
+      },
+      c_begin, c_end);
 
   const int h = lane >> 5, l32 = lane & 31;
+  if (ep.ksplit > 1) {  // raw partial sums; k_splitk_reduce applies the epilogue
+    float* part = ep.part + (int64_t)blockIdx.z * A.M * ep.N;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn0 + 32 * j + l32;
+      if (n >= ep.N) continue;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm0 + 32 * i + acc_row(r, h);
+          if (row < A.M) part[(int64_t)row * ep.N + n] = acc[i][j][r];
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
     const int n = n0 + wn0 + 32 * j + l32;
@@ -69,8 +94,30 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
   }
 }
 
+// Sums the split-K partials in split order, then bias, activation and mask.
+__global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restrict__ part, PlainEpi ep) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)M * N) return;
+  const int row = (int)(i / N), n = (int)(i % N);
+  float v = 0.f;
+  for (int z = 0; z < ksplit; ++z) v += part[(int64_t)z * M * N + i];
+  v += ep.bias ? ep.bias[n] : 0.f;
+  if (ep.act == 1) v = tanhf(v);
+  if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
+  ep.out[(int64_t)row * ep.ldo + n] = v;
+}
+
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
   if (A.M <= 0 || ep.N <= 0) return hipSuccess;
+  if (ep.ksplit > 1) {
+    if (t != Tile::Small || !ep.part) return hipErrorInvalidValue;
+    dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN), ep.ksplit);
+    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32>), grid, dim3(256), 0, st, A, W.d,
+                       W.Npad, ep);
+    const int64_t n = (int64_t)A.M * ep.N;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
+    return hipGetLastError();
+  }
   if (t == Tile::Small) {
     dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN));
     hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32>), grid, dim3(256), 0, st, A, W.d,
@@ -125,12 +172,23 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
         }
     }
   };
-  gemm_mainloop<TM, TN, KC, NT>(P.A, P.Wp, P.Npad, m0, n0, lds, [&](const float* As, const float* Bs, int side) {
-    if (side)
-      chunk(As, Bs, std::true_type{});
+  // One main loop per A segment, each with its side fixed at compile time:
+  // a per-chunk branch between the two candidate accumulators would make the
+  // compiler shuttle every accumulator between AGPRs and VGPRs each chunk.
+  int c0 = 0;
+  for (int sg = 0; sg < P.A.nseg; ++sg) {
+    const ASeg seg = seg_at(P.A, sg);
+    const int c1 = c0 + seg.nchunk;
+    if (seg.side)
+      gemm_mainloop<TM, TN, KC, NT>(
+          P.A, P.Wp, P.Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) { chunk(As, Bs, std::true_type{}); },
+          c0, c1);
     else
-      chunk(As, Bs, std::false_type{});
-  });
+      gemm_mainloop<TM, TN, KC, NT>(
+          P.A, P.Wp, P.Npad, m0, n0, lds,
+          [&](const float* As, const float* Bs, int) { chunk(As, Bs, std::false_type{}); }, c0, c1);
+    c0 = c1;
+  }
 
   const GruEpi& ep = P.ep;
   const int h = lane >> 5, l32 = lane & 31;
@@ -170,7 +228,8 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_
   for (int i = 1; i < nprob; ++i) M = M > probs[i].A.M ? M : probs[i].A.M;
   if (M <= 0) return hipSuccess;
   dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
-  hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, 64>), grid, dim3(256), 0, st, b);
+  constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
+  hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM>), grid, dim3(threads), 0, st, b);
   return hipGetLastError();
 }
 
