@@ -5,6 +5,7 @@
 // file validates arguments, packs weights once, and enqueues launches.
 #include <stdarg.h>
 #include <stdio.h>
+#include <string.h>
 
 #include <string>
 #include <vector>
@@ -59,8 +60,11 @@ struct GruBias {
 struct nmt_model {
   nmt_dims dims{};
   int device = 0;
+  bool bf16 = false;  // weights and embeddings stored as bf16
+  int kc = 32;        // K chunk of the GEMM tiles
+  int64_t emb_ld = 0; // row stride of the embedding tables (elements)
   Allocs mem;
-  float *emb_src = nullptr, *emb_tgt = nullptr;
+  void *emb_src = nullptr, *emb_tgt = nullptr;
   Packed enc_in, enc_U[2], att_Wc, init_W, g1, att_Wq, g2, ro, out;
   float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr,
         *out_b = nullptr;
@@ -82,20 +86,28 @@ struct nmt_source {
 
 namespace {
 
-// Host-side packing of x.W-oriented weights into the [Kpad/4][Npad][4]
-// layout of the GEMM kernels.  Segments are stacked along K, each padded to
-// a multiple of KC; `colmap(np)` gives the source column of packed column np
-// (or -1 for a zero column).
+// Host-side packing of x.W-oriented weights into the [Kpad/KV][Npad][KV]
+// layout of the GEMM kernels (KV = 4 fp32 or 8 bf16).  Segments are stacked
+// along K, each padded to a multiple of the chunk `kc`; `colmap(np)` gives
+// the source column of packed column np (or -1 for a zero column).
 struct Seg {
   const float* W;  // [K x ld] row-major
   int K;
   int ld;
 };
 
+uint16_t to_bf16(float x) {  // nearest, ties to even (inputs are finite)
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
 template <class ColMap>
-std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, ColMap colmap, int64_t* Kpad_out) {
+std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, int kc, int KV, ColMap colmap,
+                             int64_t* Kpad_out) {
   int64_t Kpad = 0;
-  for (const Seg& s : segs) Kpad += round_up(s.K, KC);
+  for (const Seg& s : segs) Kpad += round_up(s.K, kc);
   std::vector<float> out((size_t)(Kpad * Npad), 0.f);
   std::vector<int> cols((size_t)Npad);
   for (int64_t np = 0; np < Npad; ++np) cols[(size_t)np] = colmap(np);
@@ -103,14 +115,14 @@ std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, ColMap 
   for (const Seg& s : segs) {
     for (int k = 0; k < s.K; ++k) {
       const int64_t kk = koff + k;
-      float* dst = out.data() + (kk / 4) * Npad * 4 + (kk % 4);
+      float* dst = out.data() + (kk / KV) * Npad * KV + (kk % KV);
       const float* src = s.W + (int64_t)k * s.ld;
       for (int64_t np = 0; np < Npad; ++np) {
         const int c = cols[(size_t)np];
-        if (c >= 0) dst[np * 4] = src[c];
+        if (c >= 0) dst[np * KV] = src[c];
       }
     }
-    koff += round_up(s.K, KC);
+    koff += round_up(s.K, kc);
   }
   *Kpad_out = Kpad;
   return out;
@@ -122,26 +134,47 @@ hipError_t upload(Allocs& mem, float** d, const float* h, size_t n) {
   return hipMemcpy(*d, h, n * sizeof(float), hipMemcpyHostToDevice);
 }
 
-hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int N, int TN) {
+// Upload fp32 values as fp32 or (rounded) bf16.
+hipError_t upload_w(Allocs& mem, void** d, const std::vector<float>& h, bool bf16) {
+  if (!bf16) return upload(mem, (float**)d, h.data(), h.size());
+  std::vector<uint16_t> b(h.size());
+  for (size_t i = 0; i < h.size(); ++i) b[i] = to_bf16(h[i]);
+  hipError_t e = mem.alloc(d, b.size() * 2);
+  if (e != hipSuccess) return e;
+  return hipMemcpy(*d, b.data(), b.size() * 2, hipMemcpyHostToDevice);
+}
+
+// An embedding table [rows x E]: fp32 as is, bf16 with rows padded to `ld`.
+hipError_t upload_table(Allocs& mem, void** d, const float* h, int64_t rows, int E, int64_t ld, bool bf16) {
+  if (!bf16) return upload(mem, (float**)d, h, (size_t)rows * E);
+  std::vector<float> padded((size_t)(rows * ld), 0.f);
+  for (int64_t r = 0; r < rows; ++r) memcpy(&padded[(size_t)(r * ld)], h + r * E, sizeof(float) * E);
+  return upload_w(mem, d, padded, true);
+}
+
+hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int N, int TN, int kc, bool bf16) {
   P->N = N;
+  P->bf16 = bf16;
   P->Npad = round_up(N, TN);
-  std::vector<float> h = pack_host(segs, P->Npad, [N](int64_t np) { return np < N ? (int)np : -1; }, &P->Kpad);
-  return upload(mem, &P->d, h.data(), h.size());
+  std::vector<float> h =
+      pack_host(segs, P->Npad, kc, bf16 ? 8 : 4, [N](int64_t np) { return np < N ? (int)np : -1; }, &P->Kpad);
+  return upload_w(mem, &P->d, h, bf16);
 }
 
 // GRU packing: column tile u holds [r | z | n] of hidden units u*HB .. u*HB+HB-1.
-hipError_t pack_gru(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int H) {
+hipError_t pack_gru(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int H, int kc, bool bf16) {
   P->N = 3 * H;
+  P->bf16 = bf16;
   P->Npad = (int64_t)ceil_div(H, kGruHB) * 3 * kGruHB;
   std::vector<float> h = pack_host(
-      segs, P->Npad,
+      segs, P->Npad, kc, bf16 ? 8 : 4,
       [H](int64_t np) {
         const int ub = (int)(np / (3 * kGruHB)), rem = (int)(np % (3 * kGruHB));
         const int g = rem / kGruHB, j = ub * kGruHB + rem % kGruHB;
         return j < H ? g * H + j : -1;
       },
       &P->Kpad);
-  return upload(mem, &P->d, h.data(), h.size());
+  return upload_w(mem, &P->d, h, bf16);
 }
 
 // r/z biases summed over both sides; candidate bias split by side.
@@ -158,15 +191,28 @@ hipError_t upload_gru_bias(Allocs& mem, GruBias* b, const float* b_in, const flo
   return e;
 }
 
-ASeg make_seg(const float* p, int64_t ld, int K, int side, const int32_t* gather = nullptr, int gmax = 0) {
+// An fp32 activation segment (chunk kc of the model's precision).
+ASeg make_seg(const float* p, int64_t ld, int K, int side, int kc) {
   ASeg s{};
   s.p = p;
-  s.gather = gather;
-  s.gmax = gmax;
   s.ld = ld;
   s.K = K;
-  s.nchunk = ceil_div(K, KC);
+  s.nchunk = ceil_div(K, kc);
   s.side = side;
+  return s;
+}
+
+// Embedding rows gathered by id (fp32, or bf16 rows padded to emb_ld).
+ASeg emb_seg(const nmt_model* m, const void* table, const int32_t* ids, int nrows) {
+  ASeg s{};
+  s.p = table;
+  s.gather = ids;
+  s.gmax = nrows;
+  s.ld = m->emb_ld;
+  s.K = m->bf16 ? (int)m->emb_ld : m->dims.E;
+  s.nchunk = ceil_div(s.K, m->kc);
+  s.side = 0;
+  s.bf16 = m->bf16 ? 1 : 0;
   return s;
 }
 
@@ -195,9 +241,9 @@ nmt_status hip_fail(hipError_t e, const char* what) {
 #ifndef NMT_SPLITK_BLOCKS
 #define NMT_SPLITK_BLOCKS 1024
 #endif
-int plain_ksplit(int M, int N, int K_total) {
+int plain_ksplit(int M, int N, int K_total, int kc) {
   const int tiles = ceil_div(M, kPlainSmallTM) * ceil_div(N, kPlainSmallTN);
-  const int nc = ceil_div(K_total, KC);
+  const int nc = ceil_div(K_total, kc);
   int ks = ceil_div(NMT_SPLITK_BLOCKS, tiles);
   if (ks > nc / 4) ks = nc / 4;
   if (ks > 8) ks = 8;
@@ -229,7 +275,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
@@ -272,7 +318,7 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
 hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
   const nmt_dims& d = m->dims;
   const int C = 2 * d.H;
-  AOperand A = make_a(src->S * src->Tpad, {make_seg(src->ctx, C, C, 0)});
+  AOperand A = make_a(src->S * src->Tpad, {make_seg(src->ctx, C, C, 0, m->kc)});
   PlainEpi ep{src->pctx, d.A, m->att_b, d.A, 0, src->len, src->Tpad};
   return launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
 }
@@ -291,8 +337,10 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
     return fail(NMT_EINVAL, "dimensions must be positive");
   if (d.E % 4 || d.H % 4 || d.A % 4) return fail(NMT_EINVAL, "E, H and A must be multiples of 4");
   if (d.A > 8 * 256) return fail(NMT_EINVAL, "A must be at most 2048");
-  if (round_up(d.E, KC) > kVocabMaxKpad) return fail(NMT_EINVAL, "E must be at most %d", kVocabMaxKpad);
-  if (d.wtype != NMT_F32) return fail(NMT_EINVAL, "weight type %d is not supported", d.wtype);
+  if (d.wtype != NMT_F32 && d.wtype != NMT_BF16) return fail(NMT_EINVAL, "unknown weight type %d", d.wtype);
+  const bool bf16 = d.wtype == NMT_BF16;
+  if (round_up(d.E, chunk_k(bf16)) > vocab_max_kpad(bf16))
+    return fail(NMT_EINVAL, "E must be at most %d for this weight type", vocab_max_kpad(bf16));
   const float* const* wp = (const float* const*)w;
   for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
     if (!wp[i]) return fail(NMT_EINVAL, "weight #%zu is NULL", i);
@@ -308,8 +356,12 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   auto step = [&](hipError_t r) {
     if (e == hipSuccess) e = r;
   };
-  step(upload(m->mem, &m->emb_src, w->emb_src, (size_t)d.V_src * E));
-  step(upload(m->mem, &m->emb_tgt, w->emb_tgt, (size_t)V * E));
+  m->bf16 = bf16;
+  m->kc = chunk_k(bf16);
+  m->emb_ld = bf16 ? round_up(E, PrecBF16::KV) : E;
+  const int kc = m->kc;
+  step(upload_table(m->mem, &m->emb_src, w->emb_src, d.V_src, E, m->emb_ld, bf16));
+  step(upload_table(m->mem, &m->emb_tgt, w->emb_tgt, V, E, m->emb_ld, bf16));
   {  // encoder input projections of both directions side by side: [E x 6H]
     std::vector<float> Win((size_t)E * 6 * H), bin((size_t)6 * H);
     for (int k = 0; k < E; ++k)
@@ -321,26 +373,26 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
       bin[j] = w->enc_f_b[j];
       bin[3 * H + j] = w->enc_b_b[j];
     }
-    if (e == hipSuccess) step(pack_plain(m->mem, &m->enc_in, {{Win.data(), E, 6 * H}}, 6 * H, kPlainLargeTN));
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->enc_in, {{Win.data(), E, 6 * H}}, 6 * H, kPlainLargeTN, kc, bf16));
     step(upload(m->mem, &m->enc_in_b, bin.data(), bin.size()));
   }
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[0], {{w->enc_f_U, H, 3 * H}}, H));
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[1], {{w->enc_b_U, H, 3 * H}}, H));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[0], {{w->enc_f_U, H, 3 * H}}, H, kc, bf16));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->enc_U[1], {{w->enc_b_U, H, 3 * H}}, H, kc, bf16));
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->enc_bias, nullptr, nullptr, H));
-  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wc, {{w->att_Wc, C, A}}, A, kPlainLargeTN));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wc, {{w->att_Wc, C, A}}, A, kPlainLargeTN, kc, bf16));
   step(upload(m->mem, &m->att_b, w->att_b, A));
-  if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->init_b, w->init_b, H));
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_W, E, 3 * H}, {w->g1_U, H, 3 * H}}, H));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_W, E, 3 * H}, {w->g1_U, H, 3 * H}}, H, kc, bf16));
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g1_bias, w->g1_b, nullptr, H));
-  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wq, {{w->att_Wq, H, A}}, A, kPlainSmallTN));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wq, {{w->att_Wq, H, A}}, A, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->att_v, w->att_v, A));
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H));
+  if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H, kc, bf16));
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g2_bias, nullptr, w->g2_b, H));
   if (e == hipSuccess)
-    step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN));
+    step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->ro_b, w->ro_b, E));
-  if (e == hipSuccess) step(pack_plain(m->mem, &m->out, {{w->out_W, E, V}}, V, kVocabTN));
+  if (e == hipSuccess) step(pack_plain(m->mem, &m->out, {{w->out_W, E, V}}, V, kVocabTN, kc, bf16));
   step(upload(m->mem, &m->out_b, w->out_b, V));
   step(m->mem.alloc((void**)&m->err, sizeof(int)));
   if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
@@ -387,7 +439,7 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
   float* Xp = src->scratch;  // [S*Tpad x 6H] input-side pre-activations of both directions
   hipError_t e = launch_check_src_ids(S, Tpad, d_src_ids, src->len, d.V_src, m->err, st);
   if (e == hipSuccess) {
-    AOperand A = make_a((int)rows, {make_seg(m->emb_src, E, E, 0, d_src_ids, d.V_src)});
+    AOperand A = make_a((int)rows, {emb_seg(m, m->emb_src, d_src_ids, d.V_src)});
     PlainEpi ep{Xp, 6 * H, m->enc_in_b, 6 * H, 0, nullptr, 1};
     e = launch_gemm_plain(Tile::Large, A, m->enc_in, ep, st);
   }
@@ -404,20 +456,20 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
       const bool has_prev = prev >= 0 && prev < Tpad;
       const float* hprev = has_prev ? src->ctx + (int64_t)prev * C + dir * H : nullptr;
       GruProblem& g = p[dir];
-      g.A = has_prev ? make_a(S, {make_seg(hprev, ldc, H, 1)}) : make_a(S, {});
+      g.A = has_prev ? make_a(S, {make_seg(hprev, ldc, H, 1, m->kc)}) : make_a(S, {});
       g.Wp = m->enc_U[dir].d;
       g.Npad = m->enc_U[dir].Npad;
       g.ep = GruEpi{hprev, ldc, Xp + (int64_t)pos * 6 * H + dir * 3 * H, ldx, m->enc_bias.brz, m->enc_bias.bni,
                     m->enc_bias.bns, src->ctx + (int64_t)pos * C + dir * H, ldc, src->len, pos, H};
     }
-    e = launch_gemm_gru(p, 2, H, st);
+    e = launch_gemm_gru(p, 2, H, m->bf16, st);
   }
   if (e == hipSuccess) e = source_keys(m, src, st);
   if (e == hipSuccess && d_s0_out) {
     float* mean = Xp;  // the pre-activations are consumed by now (stream order)
     e = launch_masked_mean(S, Tpad, C, src->ctx, src->len, mean, st);
     if (e == hipSuccess) {
-      AOperand A = make_a(S, {make_seg(mean, C, C, 0)});
+      AOperand A = make_a(S, {make_seg(mean, C, C, 0, m->kc)});
       PlainEpi ep{d_s0_out, H, m->init_b, H, 1, nullptr, 1};
       e = launch_gemm_plain(Tile::Small, A, m->init_W, ep, st);
     }
@@ -503,7 +555,7 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   float* c = (float*)(ws + L.c);
   float* t = (float*)(ws + L.t);
   float2* part = (float2*)(ws + L.part);
-  const ASeg x_seg = make_seg(m->emb_tgt, E, E, 0, d_y_prev, V);  // E_i: embedding rows of the previous words
+  const ASeg x_seg = emb_seg(m, m->emb_tgt, d_y_prev, V);  // E_i: embedding rows of the previous words
   hipEvent_t* ev = nullptr;
   if (m->prof_on && m->prof_used < m->prof_max) ev = &m->prof_events[(size_t)(m->prof_used++) * (NMT_NUM_PHASES + 1)];
   hipError_t e = hipSuccess;
@@ -514,16 +566,16 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
 
   // first GRU: s1 = GRU(x, s_prev)
   GruProblem g1;
-  g1.A = make_a(B, {x_seg, make_seg(d_s_prev, H, H, 1)});
+  g1.A = make_a(B, {x_seg, make_seg(d_s_prev, H, H, 1, m->kc)});
   g1.Wp = m->g1.d;
   g1.Npad = m->g1.Npad;
   g1.ep = GruEpi{d_s_prev, H, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns, s1, H, nullptr, 0, H};
-  if (e == hipSuccess) e = launch_gemm_gru(&g1, 1, H, st);
+  if (e == hipSuccess) e = launch_gemm_gru(&g1, 1, H, m->bf16, st);
   mark(NMT_PHASE_GRU1 + 1);
   // attention query q = s1 att_Wq
   if (e == hipSuccess) {
     PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1, L.ks_q, (float*)(ws + L.kpart)};
-    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(s1, H, H, 0)}), m->att_Wq, ep, st);
+    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(s1, H, H, 0, m->kc)}), m->att_Wq, ep, st);
   }
   mark(NMT_PHASE_QUERY + 1);
   // masked attention and context
@@ -534,17 +586,17 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   // second GRU: s_new = GRU(c, s1)
   if (e == hipSuccess) {
     GruProblem g2;
-    g2.A = make_a(B, {make_seg(s1, H, H, 1), make_seg(c, C, C, 0)});
+    g2.A = make_a(B, {make_seg(s1, H, H, 1, m->kc), make_seg(c, C, C, 0, m->kc)});
     g2.Wp = m->g2.d;
     g2.Npad = m->g2.Npad;
     g2.ep = GruEpi{s1, H, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H, nullptr, 0, H};
-    e = launch_gemm_gru(&g2, 1, H, st);
+    e = launch_gemm_gru(&g2, 1, H, m->bf16, st);
   }
   mark(NMT_PHASE_GRU2 + 1);
   // readout t = tanh(s_new Ws + x Wy + c Wc + b)
   if (e == hipSuccess) {
     PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
-    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(d_s_new, H, H, 0), x_seg, make_seg(c, C, C, 0)}), m->ro,
+    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, make_seg(c, C, C, 0, m->kc)}), m->ro,
                           ep, st);
   }
   mark(NMT_PHASE_READOUT + 1);

@@ -1,21 +1,25 @@
 // device.hpp -- shared device-side building blocks of libnmt (gfx950 only).
 //
-// GEMM tiles follow one scheme everywhere.  A workgroup owns a TM x TN
-// output tile and walks K in chunks of KC, double-buffered in LDS.
+// GEMM tiles follow one scheme in both precisions.  The unit of data is a
+// 16-byte vector holding KV consecutive k of one row (A) or one column (B):
+// four fp32 (KV = 4) or eight bf16 (KV = 8).
 //
-//  * A operand (activations): up to three row-major fp32 segments that are
-//    concatenated along K without being materialised (for example
-//    [embedding rows gathered by word id | previous state]).  Each segment
-//    is read in float4 pieces; a segment's K is padded up to KC with zeros.
+//  * A operand (activations): up to three row-major segments concatenated
+//    along K without being materialised (for example [embedding rows
+//    gathered by word id | previous state]).  Segments are fp32, or bf16
+//    for embedding tables stored in bf16 (rows padded to whole vectors).
+//    The bf16 path rounds fp32 activations to bf16 (nearest even) as it
+//    stages them; accumulation is always fp32.
 //  * B operand (weights): packed once at model creation into
-//    [Kpad/4][Npad][4] ("k4-interleaved"), so one float4 holds four
-//    consecutive k of one output column.
-//  * MFMA: v_mfma_f32_32x32x2f32.  Lane l of a wave supplies A[l%32][k] and
-//    B[k][l%32] with k = l/32.  Within a group of 8 k values, lane half h
-//    uses k = 4h + j on the j-th of four MFMAs, so each lane reads exactly
-//    one float4 of A and one of B per four MFMAs (ds_read_b128).  The sum
-//    over k is order-free, so this permutation changes nothing but the
-//    rounding order.
+//    [Kpad/KV][Npad][KV], so one 16-byte load fetches a whole vector.
+//  * A workgroup owns a TM x TN output tile and walks K in chunks of
+//    KC = 8 * KV (8 vectors per row per chunk), double-buffered in LDS laid
+//    out as [8][rows][16 B].
+//  * MFMA: lane l of a wave supplies row (or column) l%32; lane half
+//    h = l/32 supplies vector 2*kg + h of k group kg.  fp32 issues four
+//    v_mfma_f32_32x32x2f32 per vector pair (k = 4h + j on the j-th);
+//    bf16 issues one v_mfma_f32_32x32x16_bf16 (k = 8h + e).  The sum over
+//    k is order-free, so this only fixes the rounding order.
 //  * Accumulator layout (checked on the device): register r of lane l
 //    holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of the 32x32 block.
 #pragma once
@@ -29,18 +33,56 @@ namespace nmt {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// Eight floats rounded to bf16 (nearest even), returned as 16 raw bytes.
+__device__ __forceinline__ f32x4 pack_bf16(const f32x4& x0, const f32x4& x1) {
+  bf16x8 v;
+  v[0] = (__bf16)x0[0];
+  v[1] = (__bf16)x0[1];
+  v[2] = (__bf16)x0[2];
+  v[3] = (__bf16)x0[3];
+  v[4] = (__bf16)x1[0];
+  v[5] = (__bf16)x1[1];
+  v[6] = (__bf16)x1[2];
+  v[7] = (__bf16)x1[3];
+  return __builtin_bit_cast(f32x4, v);
+}
+
+struct PrecF32 {
+  static constexpr bool kBF16 = false;
+  static constexpr int KV = 4;       // k per 16-byte vector
+  static constexpr int KC = 8 * KV;  // k per chunk
+  __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
+  }
+};
+
+struct PrecBF16 {
+  static constexpr bool kBF16 = true;
+  static constexpr int KV = 8;
+  static constexpr int KC = 8 * KV;
+  __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
+                                                  0, 0, 0);
+  }
+};
+
 // One A-operand segment.
 struct ASeg {
-  const float* p;         // row-major fp32 matrix
+  const void* p;          // row-major matrix, fp32 or (bf16 = 1) bf16
   const int32_t* gather;  // nullable: row m reads row gather[m] of p; ids outside [0, gmax) read zeros
   int32_t gmax;           // rows of p addressable through gather
-  int64_t ld;             // row stride in floats (multiple of 4)
-  int32_t K;              // valid columns (multiple of 4)
+  int64_t ld;             // row stride in elements (bf16 rows: a multiple of 8, zero-padded)
+  int32_t K;              // valid columns (fp32: a multiple of 4; bf16: the padded row length)
   int32_t nchunk;         // ceil(K / KC)
   int32_t side;           // 0: input side, 1: state side (routes the GRU candidate gate)
+  int32_t bf16;           // element type of p
 };
 
 struct AOperand {
@@ -48,8 +90,6 @@ struct AOperand {
   int32_t nseg;
   int32_t M;  // valid rows
 };
-
-__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
 // Segment i of A, field by field through uniform selects: indexing the
 // by-value kernel argument (or copying whole segments conditionally) with a
@@ -67,6 +107,7 @@ __device__ __forceinline__ ASeg seg_at(const AOperand& A, int i) {
   s.K = sel3(i, A.seg[0].K, A.seg[1].K, A.seg[2].K);
   s.nchunk = sel3(i, A.seg[0].nchunk, A.seg[1].nchunk, A.seg[2].nchunk);
   s.side = sel3(i, A.seg[0].side, A.seg[1].side, A.seg[2].side);
+  s.bf16 = sel3(i, A.seg[0].bf16, A.seg[1].bf16, A.seg[2].bf16);
   return s;
 }
 
@@ -75,86 +116,95 @@ __device__ __forceinline__ int total_chunks(const AOperand& A) {
          (A.nseg > 2 ? A.seg[2].nchunk : 0);
 }
 
-__device__ __forceinline__ const float* seg_row(const ASeg& s, int row, int M) {
+// Byte address of this thread's row of segment s (nullptr: a zero row).
+__device__ __forceinline__ const char* seg_row(const ASeg& s, int row, int M) {
   if (row >= M) return nullptr;
+  int64_t r = row;
   if (s.gather) {
-    int g = s.gather[row];
+    const int g = s.gather[row];
     if (g < 0 || g >= s.gmax) return nullptr;
-    return s.p + (int64_t)g * s.ld;
+    r = g;
   }
-  return s.p + (int64_t)row * s.ld;
+  return (const char*)s.p + r * s.ld * (s.bf16 ? 2 : 4);
+}
+
+// The 16-byte A vector at column k of a row, in precision P.
+template <class P>
+__device__ __forceinline__ f32x4 load_a_vec(const char* row, int bf16src, int K, int k) {
+  if (!row || k >= K) return zero4();
+  if constexpr (P::kBF16) {
+    if (bf16src) return *(const f32x4*)(row + 2 * (int64_t)k);  // rows padded to whole vectors
+    const float* r = (const float*)row;
+    const f32x4 x0 = *(const f32x4*)(r + k);
+    const f32x4 x1 = k + 4 < K ? *(const f32x4*)(r + k + 4) : zero4();
+    return pack_bf16(x0, x1);
+  } else {
+    return *(const f32x4*)((const float*)row + k);
+  }
 }
 
 // Global -> register -> LDS staging of one K chunk of the A and B tiles.
-// Each thread owns one tile row for A (NT % TM == 0) and strided float4s of B.
-template <int TM, int TN, int KC, int NT>
+// Each thread owns one tile row for A (NT % TM == 0) and strided vectors of B.
+template <int TM, int TN, int NT, class P>
 struct Stager {
-  static constexpr int KQ = KC / 4;
+  static constexpr int KQ = 8;  // vectors per row per chunk
   static constexpr int NA = TM * KQ / NT;
   static constexpr int NB = TN * KQ / NT;
   static_assert(NT % TM == 0, "one A row per thread");
-  static_assert((TM * KQ) % NT == 0 && (TN * KQ) % NT == 0, "whole float4s per thread");
+  static_assert((TM * KQ) % NT == 0 && (TN * KQ) % NT == 0, "whole vectors per thread");
   f32x4 ra[NA];
   f32x4 rb[NB];
 
   // arow: this thread's row of the current segment (nullptr = zeros);
-  // kseg: k offset of the chunk within the segment; kq_glob: chunk start in
-  // packed-weight rows of 4.
-  __device__ __forceinline__ void load(const float* arow, int segK, int kseg, const float* __restrict__ Wp,
-                                       int64_t Npad, int64_t kq_glob, int n0) {
+  // kseg: k offset of the chunk within the segment; vq_glob: chunk start in
+  // packed-weight vector rows.
+  __device__ __forceinline__ void load(const char* arow, int bf16src, int segK, int kseg,
+                                       const f32x4* __restrict__ Wp, int64_t Npad, int64_t vq_glob, int n0) {
     const int tid = threadIdx.x;
     const int kq0 = tid / TM;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      int k = kseg + 4 * (kq0 + i * (NT / TM));
-      ra[i] = (arow && k < segK) ? *(const f32x4*)(arow + k) : zero4();
-    }
+    for (int i = 0; i < NA; ++i) ra[i] = load_a_vec<P>(arow, bf16src, segK, kseg + P::KV * (kq0 + i * (NT / TM)));
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      int idx = tid + i * NT;
-      int n = idx % TN, kq = idx / TN;
-      rb[i] = *(const f32x4*)(Wp + ((kq_glob + kq) * Npad + n0 + n) * 4);
+      const int idx = tid + i * NT;
+      const int n = idx % TN, kq = idx / TN;
+      rb[i] = Wp[(vq_glob + kq) * Npad + n0 + n];
     }
   }
 
-  __device__ __forceinline__ void store(float* As, float* Bs) const {
+  __device__ __forceinline__ void store(f32x4* As, f32x4* Bs) const {
     const int tid = threadIdx.x;
     const int m = tid % TM, kq0 = tid / TM;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) *(f32x4*)(As + ((kq0 + i * (NT / TM)) * TM + m) * 4) = ra[i];
+    for (int i = 0; i < NA; ++i) As[(kq0 + i * (NT / TM)) * TM + m] = ra[i];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      int idx = tid + i * NT;
-      int n = idx % TN, kq = idx / TN;
-      *(f32x4*)(Bs + (kq * TN + n) * 4) = rb[i];
+      const int idx = tid + i * NT;
+      const int n = idx % TN, kq = idx / TN;
+      Bs[kq * TN + n] = rb[i];
     }
   }
 };
 
-__device__ __forceinline__ f32x16 mfma(float a, float b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-}
-
-// Fragment loads from the staged LDS tiles: the float4 for k group kg of the
-// 32-row (or 32-column) block starting at r0.
+// Fragment of k group kg for the 32-row (or 32-column) block at r0.
 template <int TROWS>
-__device__ __forceinline__ f32x4 lds_frag(const float* S, int kg, int r0) {
+__device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
   const int lane = threadIdx.x & 63;
-  return *(const f32x4*)(S + ((2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)) * 4);
+  return S[(2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)];
 }
 
 // The generic main loop: walks chunks [c_begin, c_end) of the A segments
-// (all chunks by default), staging the next chunk while
-// `compute(As, Bs, side)` runs on the current one.  Chunk c covers packed
-// weight rows c*KC .. c*KC+KC-1, whichever segment it falls in.
-template <int TM, int TN, int KC, int NT, class Compute>
-__device__ __forceinline__ void gemm_mainloop(const AOperand& A, const float* __restrict__ Wp, int64_t Npad,
-                                              int m0, int n0, float* lds, Compute&& compute, int c_begin = 0,
+// (all chunks by default), staging the next chunk while `compute(As, Bs)`
+// runs on the current one.  Chunk c covers packed weight vector rows
+// 8c .. 8c+7, whichever segment it falls in.
+template <int TM, int TN, int NT, class P, class Compute>
+__device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __restrict__ Wp, int64_t Npad, int m0,
+                                              int n0, f32x4* lds, Compute&& compute, int c_begin = 0,
                                               int c_end = 1 << 30) {
-  constexpr int ASZ = TM * KC, BSZ = TN * KC;
-  float* As[2] = {lds, lds + ASZ + BSZ};
-  float* Bs[2] = {lds + ASZ, lds + 2 * ASZ + BSZ};
-  Stager<TM, TN, KC, NT> st;
+  constexpr int ASZ = TM * 8, BSZ = TN * 8;  // vectors per stage
+  f32x4* As[2] = {lds, lds + ASZ + BSZ};
+  f32x4* Bs[2] = {lds + ASZ, lds + 2 * ASZ + BSZ};
+  Stager<TM, TN, NT, P> st;
   const int row = m0 + (int)threadIdx.x % TM;
 
   const int nc = total_chunks(A);
@@ -167,24 +217,23 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const float* __
     ch -= sg.nchunk;
     sg = seg_at(A, ++seg);
   }
-  const float* arow = seg_row(sg, row, A.M);
-  st.load(arow, sg.K, ch * KC, Wp, Npad, (int64_t)c_begin * (KC / 4), n0);
+  const char* arow = seg_row(sg, row, A.M);
+  st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)c_begin * 8, n0);
   st.store(As[0], Bs[0]);
   __syncthreads();
 
   for (int c = c_begin; c < c_end; ++c) {
     const bool more = c + 1 < c_end;
     const int buf = (c - c_begin) & 1;
-    const int side = sg.side;
     if (more) {
       if (++ch == sg.nchunk) {
         ch = 0;
         do { sg = seg_at(A, ++seg); } while (sg.nchunk == 0);
         arow = seg_row(sg, row, A.M);
       }
-      st.load(arow, sg.K, ch * KC, Wp, Npad, (int64_t)(c + 1) * (KC / 4), n0);
+      st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)(c + 1) * 8, n0);
     }
-    compute(As[buf], Bs[buf], side);
+    compute(As[buf], Bs[buf]);
     if (more) st.store(As[buf ^ 1], Bs[buf ^ 1]);
     __syncthreads();
   }

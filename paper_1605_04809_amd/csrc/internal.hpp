@@ -9,8 +9,10 @@
 
 namespace nmt {
 
-constexpr int KC = 32;             // K chunk of every fp32 GEMM tile
 constexpr int kMaxTpad = 1024;     // attention keeps one score per source position in LDS
+
+// K chunk of the GEMM tiles: 8 sixteen-byte vectors of 4 fp32 or 8 bf16.
+inline int chunk_k(bool bf16) { return bf16 ? PrecBF16::KC : PrecF32::KC; }
 
 // Tile shapes (rows x packed columns) of the kernel families.
 constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;
@@ -25,11 +27,12 @@ constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
 #endif
 constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
-constexpr int kVocabMaxKpad = 576;              // padded E the vocabulary kernel keeps in LDS
 
-// A weight matrix packed for one kernel family: [Kpad/4][Npad][4] fp32.
+// A weight matrix packed for one kernel family: [Kpad/KV][Npad][KV] of fp32
+// (KV = 4) or bf16 (KV = 8), 16 bytes per (vector row, column).
 struct Packed {
-  float* d = nullptr;
+  void* d = nullptr;
+  bool bf16 = false;
   int64_t Kpad = 0;  // sum of the padded K of its segments
   int64_t Npad = 0;
   int N = 0;         // valid columns (for GRU: 3H)
@@ -72,16 +75,18 @@ struct GruEpi {
 
 struct GruProblem {
   AOperand A;
-  const float* Wp;
+  const void* Wp;
   int64_t Npad;
   GruEpi ep;
 };
 
 // Launchers (all asynchronous on `st`).
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
-hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_t st);
-// Number of vocabulary slices (partials per row) for M rows.
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st);
+// Number of vocabulary slices (partials per row) for M rows, and the
+// largest padded E the vocabulary kernel keeps in LDS.
 int vocab_slices(int M, int64_t Npad);
+int vocab_max_kpad(bool bf16);
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
                             int nS, hipStream_t st);
 hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,

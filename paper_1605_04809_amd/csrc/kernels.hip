@@ -1,14 +1,18 @@
 // kernels.hip -- the HIP kernels of one batched decoder step and of source
 // initialisation, for gfx950.  Equations are listed in include/nmt.h.
+// The GEMM-family kernels are templates over the precision policy
+// (PrecF32: fp32 weights, PrecBF16: bf16 weights with bf16 MFMA inputs;
+// both accumulate in fp32).
 //
-//   k_gemm_plain   MFMA GEMM with bias (+tanh) epilogue: attention query,
-//                  readout, attention keys, encoder input projections.
+//   k_gemm_plain   MFMA GEMM with bias (+tanh) epilogue, optionally split
+//                  over K: attention query, readout, attention keys,
+//                  encoder input projections, initial state.
 //   k_gemm_gru     MFMA GEMM whose tile holds matching r, z and candidate
 //                  columns of the same hidden units, with the GRU cell fused
 //                  into the epilogue (both decoder GRUs, encoder recurrence).
-//   k_vocab_lse    MFMA vocabulary projection fused with a per-tile
-//                  log-sum-exp; the logits never reach HBM.
-//   k_lse_combine  merges the per-tile partials, scores the requested word
+//   k_vocab_lse    MFMA vocabulary projection streaming the output weights,
+//                  fused with an online log-sum-exp; logits never reach HBM.
+//   k_lse_combine  merges the per-slice partials, scores the requested word
 //                  and checks the row's ids.
 //   k_attention    masked MLP attention and context for one row per block.
 #include "internal.hpp"
@@ -17,12 +21,12 @@ namespace nmt {
 
 // ----------------------------------------------------------- plain GEMM
 
-template <int TM, int TN, int WM, int WN>
-__global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOperand A, const float* __restrict__ Wp,
+template <int TM, int TN, int WM, int WN, class P>
+__global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOperand A, const f32x4* __restrict__ Wp,
                                                                            int64_t Npad, PlainEpi ep) {
   constexpr int NT = (TM / WM) * (TN / WN) * 64;
   constexpr int FM = WM / 32, FN = WN / 32;
-  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
+  __shared__ f32x4 lds[2 * (TM + TN) * 8];
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm0 = (wave % (TM / WM)) * WM, wn0 = (wave / (TM / WM)) * WN;
@@ -38,22 +42,20 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
     c_begin = (int)((int64_t)nc * blockIdx.z / ep.ksplit);
     c_end = (int)((int64_t)nc * (blockIdx.z + 1) / ep.ksplit);
   }
-  gemm_mainloop<TM, TN, KC, NT>(
+  gemm_mainloop<TM, TN, NT, P>(
       A, Wp, Npad, m0, n0, lds,
-      [&](const float* As, const float* Bs, int) {
+      [&](const f32x4* As, const f32x4* Bs) {
 #pragma unroll
-        for (int kg = 0; kg < KC / 8; ++kg) {
+        for (int kg = 0; kg < 4; ++kg) {
           f32x4 a[FM], b[FN];
 #pragma unroll
           for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
 #pragma unroll
           for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
+          for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-              for (int j = 0; j < FN; ++j) acc[i][j] = mfma(a[i][jj], b[j][jj], acc[i][j]);
+            for (int j = 0; j < FN; ++j) P::mma(a[i], b[j], acc[i][j]);
         }
       },
       c_begin, c_end);
@@ -107,27 +109,31 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
   ep.out[(int64_t)row * ep.ldo + n] = v;
 }
 
-hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
-  if (A.M <= 0 || ep.N <= 0) return hipSuccess;
+template <class P>
+hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
+  const f32x4* Wp = (const f32x4*)W.d;
   if (ep.ksplit > 1) {
     if (t != Tile::Small || !ep.part) return hipErrorInvalidValue;
     dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN), ep.ksplit);
-    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32>), grid, dim3(256), 0, st, A, W.d,
-                       W.Npad, ep);
+    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
+                       ep);
     const int64_t n = (int64_t)A.M * ep.N;
     hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
-    return hipGetLastError();
-  }
-  if (t == Tile::Small) {
+  } else if (t == Tile::Small) {
     dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN));
-    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32>), grid, dim3(256), 0, st, A, W.d,
-                       W.Npad, ep);
+    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
+                       ep);
   } else {
     dim3 grid(ceil_div(A.M, kPlainLargeTM), (unsigned)(W.Npad / kPlainLargeTN));
-    hipLaunchKernelGGL((k_gemm_plain<kPlainLargeTM, kPlainLargeTN, 64, 64>), grid, dim3(256), 0, st, A, W.d,
-                       W.Npad, ep);
+    hipLaunchKernelGGL((k_gemm_plain<kPlainLargeTM, kPlainLargeTN, 64, 64, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
+                       ep);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
+  if (A.M <= 0 || ep.N <= 0) return hipSuccess;
+  return W.bf16 ? gemm_plain<PrecBF16>(t, A, W, ep, st) : gemm_plain<PrecF32>(t, A, W, ep, st);
 }
 
 // ------------------------------------------------------------- GRU GEMM
@@ -136,13 +142,14 @@ struct GruBatch {
   GruProblem p[2];
 };
 
-template <int TM, int HB, int WM>
+template <int TM, int HB, int WM, class P>
 __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatch batch) {
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
-  __shared__ __attribute__((aligned(16))) float lds[2 * (TM + TN) * KC];
-  const GruProblem& P = batch.p[blockIdx.z];
+  __shared__ f32x4 lds[2 * (TM + TN) * 8];
+  const GruProblem& Pb = batch.p[blockIdx.z];
+  const f32x4* Wp = (const f32x4*)Pb.Wp;
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm0 = (wave % (TM / WM)) * WM, wu0 = (wave / (TM / WM)) * 32;
@@ -150,9 +157,9 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
 #pragma unroll
   for (int i = 0; i < FM; ++i) ar[i] = az[i] = ani[i] = ans[i] = f32x16{};
 
-  auto chunk = [&](const float* As, const float* Bs, auto state_side) {
+  auto chunk = [&](const f32x4* As, const f32x4* Bs, auto state_side) {
 #pragma unroll
-    for (int kg = 0; kg < KC / 8; ++kg) {
+    for (int kg = 0; kg < 4; ++kg) {
       f32x4 a[FM];
 #pragma unroll
       for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
@@ -160,37 +167,35 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
       const f32x4 bz = lds_frag<TN>(Bs, kg, HB + wu0);
       const f32x4 bn = lds_frag<TN>(Bs, kg, 2 * HB + wu0);
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          ar[i] = mfma(a[i][jj], br[jj], ar[i]);
-          az[i] = mfma(a[i][jj], bz[jj], az[i]);
-          if constexpr (decltype(state_side)::value)
-            ans[i] = mfma(a[i][jj], bn[jj], ans[i]);
-          else
-            ani[i] = mfma(a[i][jj], bn[jj], ani[i]);
-        }
+      for (int i = 0; i < FM; ++i) {
+        P::mma(a[i], br, ar[i]);
+        P::mma(a[i], bz, az[i]);
+        if constexpr (decltype(state_side)::value)
+          P::mma(a[i], bn, ans[i]);
+        else
+          P::mma(a[i], bn, ani[i]);
+      }
     }
   };
   // One main loop per A segment, each with its side fixed at compile time:
   // a per-chunk branch between the two candidate accumulators would make the
   // compiler shuttle every accumulator between AGPRs and VGPRs each chunk.
   int c0 = 0;
-  for (int sg = 0; sg < P.A.nseg; ++sg) {
-    const ASeg seg = seg_at(P.A, sg);
+  for (int sg = 0; sg < Pb.A.nseg; ++sg) {
+    const ASeg seg = seg_at(Pb.A, sg);
     const int c1 = c0 + seg.nchunk;
     if (seg.side)
-      gemm_mainloop<TM, TN, KC, NT>(
-          P.A, P.Wp, P.Npad, m0, n0, lds, [&](const float* As, const float* Bs, int) { chunk(As, Bs, std::true_type{}); },
+      gemm_mainloop<TM, TN, NT, P>(
+          Pb.A, Wp, Pb.Npad, m0, n0, lds, [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); },
           c0, c1);
     else
-      gemm_mainloop<TM, TN, KC, NT>(
-          P.A, P.Wp, P.Npad, m0, n0, lds,
-          [&](const float* As, const float* Bs, int) { chunk(As, Bs, std::false_type{}); }, c0, c1);
+      gemm_mainloop<TM, TN, NT, P>(
+          Pb.A, Wp, Pb.Npad, m0, n0, lds, [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); },
+          c0, c1);
     c0 = c1;
   }
 
-  const GruEpi& ep = P.ep;
+  const GruEpi& ep = Pb.ep;
   const int h = lane >> 5, l32 = lane & 31;
   const int H = ep.H;
   const int j = blockIdx.y * HB + wu0 + l32;
@@ -201,7 +206,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + wm0 + 32 * i + acc_row(r, h);
-      if (row >= P.A.M) continue;
+      if (row >= Pb.A.M) continue;
       float xr = 0.f, xz = 0.f, xn = 0.f;
       if (ep.xin) {
         const float* x = ep.xin + (int64_t)row * ep.ldx;
@@ -219,7 +224,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
     }
 }
 
-hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_t st) {
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st) {
   if (nprob < 1 || nprob > 2) return hipErrorInvalidValue;
   GruBatch b;
   b.p[0] = probs[0];
@@ -229,7 +234,10 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_
   if (M <= 0) return hipSuccess;
   dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
   constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
-  hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM>), grid, dim3(threads), 0, st, b);
+  if (bf16)
+    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM, PrecBF16>), grid, dim3(threads), 0, st, b);
+  else
+    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM, PrecF32>), grid, dim3(threads), 0, st, b);
   return hipGetLastError();
 }
 
@@ -238,28 +246,30 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, hipStream_
 // Streaming vocabulary projection with an online log-sum-exp.
 //
 // A block owns VTM = 64 rows and one slice of the vocabulary.  Its rows of
-// the readout t stay in LDS for the whole kernel ([Kpad/4][64][4] floats,
-// 128 KB at E = 500); the packed output weights stream straight from HBM/L2
-// into registers, four k groups ahead, so the main loop has no barrier.
-// Wave w of the 8 takes the slice's 32-column blocks w, w+8, ...; each lane
-// keeps a running (max, sum of exp) for each of its 32 row slots, and the
-// 32 lanes and 8 waves are merged once at the end.  One (max, sum) pair per
-// row and slice goes to HBM as float2 [slice][row]; the logits never do.
+// the readout t stay in LDS for the whole kernel as 16-byte vectors
+// [Kpad/KV][64] (128 KB fp32 / 64 KB bf16 at E = 500); the packed output
+// weights stream straight from HBM/L2 into registers, four k groups ahead,
+// so the main loop has no barrier.  Wave w of the 8 takes the slice's
+// 32-column blocks w, w+8, ...; each lane keeps a running (max, sum of exp)
+// for each of its 32 row slots, and the 32 lanes and 8 waves are merged
+// once at the end.  One (max, sum) pair per row and slice goes to HBM as
+// float2 [slice][row]; the logits never do.
 //
 // Slices are spread over XCDs: blocks with ids congruent mod 8 run on one
 // XCD, and that XCD takes slices xcd, xcd+8, ... for every row tile, so the
 // row tiles of a slice read the same weights from that XCD's L2 and the
 // weights cross HBM once.
-constexpr int VTM = 64;           // rows per block
-constexpr int VNW = 8;            // waves per block
-constexpr int VKMAX = 576;        // max padded E held in LDS (64 x 576 x 4 B = 144 KB)
-constexpr int VPF = 4;            // k groups of weight fragments in flight per wave
+constexpr int VTM = 64;                 // rows per block
+constexpr int VNW = 8;                  // waves per block
+constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
+constexpr int VPF = 4;                  // k groups of weight fragments in flight per wave
 
+template <class P>
 __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E, int Kpad,
-                                                        const float* __restrict__ Wp, int64_t Npad,
+                                                        const f32x4* __restrict__ Wp, int64_t Npad,
                                                         const float* __restrict__ bias, int V, int nM, int nS,
                                                         float2* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) float As[VTM * VKMAX];
+  __shared__ f32x4 As[VQMAX];
   __shared__ float red[VNW][VTM][2];
   const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
   const int slice = (slot / nM) * 8 + xcd, mt = slot % nM;
@@ -269,20 +279,18 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
 
-  // stationary A tile: As[kq][m][4] = t[m0 + m][4kq .. 4kq+3]
-  const int KQ = Kpad / 4;
+  // stationary A tile: As[kq][m] = vector kq of row m0 + m
+  const int KQ = Kpad / P::KV;
   for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
     const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
-    f32x4 v = zero4();
-    if (row < M && 4 * kq < E) v = *(const f32x4*)(t + (int64_t)row * E + 4 * kq);
-    *(f32x4*)(As + (kq * VTM + m) * 4) = v;
+    As[kq * VTM + m] = load_a_vec<P>(row < M ? (const char*)(t + (int64_t)row * E) : nullptr, 0, E, kq * P::KV);
   }
   __syncthreads();
 
   // this slice's 32-column blocks, balanced over the slices
   const int NB = (int)(Npad / 32);
   const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
-  const int NKG = Kpad / 8;  // k groups per column block (a multiple of VPF)
+  const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
   const int nblk = cb_end - cb_begin > wave ? (cb_end - cb_begin - wave + VNW - 1) / VNW : 0;
 
   float run_m[2][16], run_s[2][16];
@@ -299,24 +307,24 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   // q % VPF == p.  Loads past this wave's last step re-read fragment 0 of
   // the matrix (always in bounds) so that no load sits behind a branch.
   const int total = nblk * NKG;
-  const float* wlane = Wp + ((int64_t)h * Npad + l32) * 4;
+  const f32x4* wlane = Wp + (int64_t)h * Npad + l32;
   int pcb = cb_begin + wave, pkg = 0, issued = 0;
   auto load_next = [&]() {
-    const int64_t off = issued < total ? ((int64_t)(2 * pkg) * Npad + (int64_t)pcb * 32) * 4 : 0;
+    const int64_t off = issued < total ? (int64_t)(2 * pkg) * Npad + (int64_t)pcb * 32 : 0;
     ++issued;
     if (++pkg == NKG) {
       pkg = 0;
       pcb += VNW;
     }
-    return *(const f32x4*)(wlane + off);
+    return wlane[off];
   };
   f32x4 ring[VPF];
 #pragma unroll
   for (int p = 0; p < VPF; ++p) ring[p] = load_next();
   // A fragments ping-pong between an even and an odd register set (VPF is
   // even), so neither ring needs register moves at the loop back-edge.
-  const float* arow = As + (h * VTM + l32) * 4;  // + 2*kg*VTM*4 per k group
-  f32x4 ae0 = *(const f32x4*)arow, ae1 = *(const f32x4*)(arow + 32 * 4), ao0, ao1;
+  const f32x4* arow = As + h * VTM + l32;  // + 2*kg*VTM per k group
+  f32x4 ae0 = arow[0], ae1 = arow[32], ao0, ao1;
   static_assert(VPF % 2 == 0, "even/odd fragment sets");
 
   for (int q0 = 0; q0 < total; q0 += NKG) {
@@ -326,29 +334,26 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
       for (int p = 0; p < VPF; ++p) {
         const int kg = kg0 + p;
         const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next column block)
-        const float* an = arow + kn * 2 * VTM * 4;
+        const f32x4* an = arow + kn * 2 * VTM;
         f32x4 a0, a1;
         if (p % 2 == 0) {
-          ao0 = *(const f32x4*)an;
-          ao1 = *(const f32x4*)(an + 32 * 4);
+          ao0 = an[0];
+          ao1 = an[32];
           a0 = ae0;
           a1 = ae1;
         } else {
-          ae0 = *(const f32x4*)an;
-          ae1 = *(const f32x4*)(an + 32 * 4);
+          ae0 = an[0];
+          ae1 = an[32];
           a0 = ao0;
           a1 = ao1;
         }
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          acc0 = mfma(a0[jj], ring[p][jj], acc0);
-          acc1 = mfma(a1[jj], ring[p][jj], acc1);
-        }
+        P::mma(a0, ring[p], acc0);
+        P::mma(a1, ring[p], acc1);
         ring[p] = load_next();  // refill the slot just consumed, VPF steps ahead
       }
     }
     // fold this 32-column block into the running (max, sum) of each row slot
-    const int n = (cb_begin + wave + VNW * (int)(q0 / NKG)) * 32 + l32;
+    const int n = (cb_begin + wave + VNW * (q0 / NKG)) * 32 + l32;
     if (n < V) {
       const float bn = bias[n];
 #pragma unroll
@@ -406,25 +411,48 @@ int vocab_slices(int M, int64_t Npad) {
   return nS;
 }
 
+int vocab_max_kpad(bool bf16) { return VQMAX / VTM * (bf16 ? PrecBF16::KV : PrecF32::KV); }
+
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
                             int nS, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (W.Kpad > VKMAX || W.Kpad % (8 * VPF)) return hipErrorInvalidValue;
+  const int KV = W.bf16 ? PrecBF16::KV : PrecF32::KV;
+  if (W.Kpad > vocab_max_kpad(W.bf16) || W.Kpad % (2 * KV * VPF)) return hipErrorInvalidValue;
   const int nM = ceil_div(M, VTM);
   dim3 grid((unsigned)(nS / 8 * 8 * nM));
-  hipLaunchKernelGGL(k_vocab_lse, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, W.d, W.Npad, bias, V, nM, nS,
-                     part);
+  if (W.bf16)
+    hipLaunchKernelGGL(k_vocab_lse<PrecBF16>, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad,
+                       (const f32x4*)W.d, W.Npad, bias, V, nM, nS, part);
+  else
+    hipLaunchKernelGGL(k_vocab_lse<PrecF32>, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad,
+                       (const f32x4*)W.d, W.Npad, bias, V, nM, nS, part);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------- partials combine
 
+// Dot product of two 16-byte vectors in precision P (fp32 accumulation).
+template <class P>
+__device__ __forceinline__ float dot_vec(const f32x4& a, const f32x4& b) {
+  if constexpr (P::kBF16) {
+    const bf16x8 x = __builtin_bit_cast(bf16x8, a), y = __builtin_bit_cast(bf16x8, b);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += (float)x[e] * (float)y[e];
+    return s;
+  } else {
+    return a[0] * b[0] + a[1] * b[1] + a[2] * b[2] + a[3] * b[3];
+  }
+}
+
 // One wave per row: merges the per-slice (max, sum) pairs into logZ, scores
-// the requested word with its own dot product t . out_W[:, req] + out_b[req],
-// and checks the row's ids (any out of range: NaN outputs and the flag).
+// the requested word with its own dot product t . out_W[:, req] + out_b[req]
+// (t rounded as the vocabulary kernel's MFMA inputs are), and checks the
+// row's ids (any out of range: NaN outputs and the flag).
+template <class P>
 __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __restrict__ part, int nS,
-                                                     const float* __restrict__ t, int E,
-                                                     const float* __restrict__ Wp, int64_t Npad,
+                                                     const float* __restrict__ t, int E, int Kpad,
+                                                     const f32x4* __restrict__ Wp, int64_t Npad,
                                                      const float* __restrict__ bias, int V,
                                                      const int32_t* __restrict__ req,
                                                      const int32_t* __restrict__ y_prev,
@@ -451,12 +479,9 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
   }
   sum = wave_sum(sum);
   float dot = 0.f;
-  const float* tr = t + (int64_t)row * E;
-  for (int k4 = lane; k4 < E / 4; k4 += 64) {
-    const f32x4 tv = *(const f32x4*)(tr + 4 * k4);
-    const f32x4 wv = *(const f32x4*)(Wp + ((int64_t)k4 * Npad + w) * 4);
-    dot += tv[0] * wv[0] + tv[1] * wv[1] + tv[2] * wv[2] + tv[3] * wv[3];
-  }
+  const char* tr = (const char*)(t + (int64_t)row * E);
+  for (int kq = lane; kq < Kpad / P::KV; kq += 64)
+    dot += dot_vec<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), Wp[(int64_t)kq * Npad + w]);
   dot = wave_sum(dot);
   if (lane == 0) {
     const float lz = mx + logf(sum);
@@ -469,8 +494,12 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
                               const float* bias, int V, const int32_t* req, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
   if (B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lse_combine, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E, W.d, W.Npad, bias, V,
-                     req, y_prev, sent_id, S, logp, logZ, err);
+  if (W.bf16)
+    hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
+                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, req, y_prev, sent_id, S, logp, logZ, err);
+  else
+    hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
+                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, req, y_prev, sent_id, S, logp, logZ, err);
   return hipGetLastError();
 }
 

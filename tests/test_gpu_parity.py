@@ -250,3 +250,36 @@ def test_phrase_scoring_stepwise(gpu):
 def cuda_i32(a):
     import torch
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+# ------------------------------------------------------------ bf16 weights
+
+TOL_LOGP_BF16 = 2e-2      # stated bar: bf16 weights, fp32 accumulation
+TOL_INTER_BF16 = 1e-2     # states and intermediates (bf16 rounding of MFMA inputs)
+
+
+@pytest.mark.parametrize("cfg", [CONFIGS["tiny"].replace(wtype="bf16", B=96),
+                                 MIXED.replace(wtype="bf16", sigma_w=0.1, seed=8)],
+                         ids=["tiny_bf16", "ragged_dims_bf16"])
+def test_bf16_every_row(gpu, cfg):
+    """bf16 storage of weights and embeddings; both sides use the same bf16 values."""
+    _torch()
+    wl = make_workload(cfg)
+    wl.y_prev[::5] = -1
+    g, o = gpu.GpuRun(wl), gpu.OracleRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    compare(g.step(*args), o.step(*args), tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16)
+    g.close()
+
+
+def test_bf16_paper_sized_step_sampled_rows(gpu):
+    _torch()
+    wl = make_workload(CONFIGS["bf16_b4096"])
+    g = gpu.GpuRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    out = g.step(*args)
+    assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
+    rows = sample_rows(wl.cfg.B, 40, seed=6)
+    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
+    compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16)
+    g.close()
