@@ -36,16 +36,22 @@ METRIC = "scored hypothesis-words/sec at V=100k, H=1024, B=2000; MFMA util %"
 UNIT = "scored hypothesis-words/s"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = ("paper_1605_04809_amd/csrc/kernels.hip", "paper_1605_04809_amd/csrc/device.hpp",
-                  "paper_1605_04809_amd/csrc/internal.hpp")
+KERNEL_HEADERS = ("paper_1605_04809_amd/csrc/device.hpp", "paper_1605_04809_amd/csrc/internal.hpp")
+KERNEL_FILE = "paper_1605_04809_amd/csrc/kernels.hip"
+VOCAB_SECTION = ("// ------------------------------------------------ vocabulary projection",
+                 "// ---------------------------------------------------- partials combine")
 TRAFFIC_FILE = "profiles/vocab_lse_{workload}_traffic.txt"
 
 
 def kernel_source_hash() -> str:
+    """Hash of the vocabulary kernel's source section and the shared headers."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_HEADERS:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
+    text = open(os.path.join(ROOT, KERNEL_FILE)).read()
+    a, b = text.index(VOCAB_SECTION[0]), text.index(VOCAB_SECTION[1])
+    h.update(text[a:b].encode())
     return h.hexdigest()[:16]
 
 
@@ -128,7 +134,11 @@ def main():
     ap.add_argument("--config", default="enru_b2000")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
+    ap.add_argument("--print-kernel-hash", action="store_true")
     args = ap.parse_args()
+    if args.print_kernel_hash:
+        print(kernel_source_hash())
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
