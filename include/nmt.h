@@ -171,6 +171,86 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
                                  size_t ws_bytes, void* stream, float* d_alpha, float* d_c,
                                  float* d_s1, float* d_t);
 
+/* One level of the ScoreBatch procedure (Section 5.1, Figure 2): a batched
+ * step whose rows take their input states from a device state pool by index
+ * and may request several next words each.
+ *   d_state_pool [pool_rows x H]  states; row b's input state is
+ *                                 d_state_pool[d_state_row[b]] (so H_{i-1}
+ *                                 is gathered on the device, never copied)
+ *   d_state_row [B]               in [0, pool_rows)
+ *   d_y_prev [B], d_sent_id [B]   as for nmt_score_batch
+ *   d_req_off [B+1], d_req [nreq] requested words of row b are
+ *                                 d_req[d_req_off[b] .. d_req_off[b+1])
+ *                                 (CSR; offsets non-decreasing, in [0, nreq])
+ *   d_logp [nreq]                 out: log p of each request under its row
+ *   d_s_new [B x H]               out: new states (must not overlap the pool)
+ *   d_logZ [B]                    out, nullable
+ * Workspace as for nmt_score_batch with the same B.  Rows with an id out of
+ * range or malformed offsets get NaN outputs and set the device error flag.
+ * Errors: NMT_EINVAL, NMT_EWORKSPACE, NMT_EDEVICE. */
+nmt_status nmt_score_forest_step(nmt_model* m, const nmt_source* src, int32_t B, const float* d_state_pool,
+                                 int32_t pool_rows, const int32_t* d_state_row, const int32_t* d_y_prev,
+                                 const int32_t* d_sent_id, const int32_t* d_req_off, const int32_t* d_req,
+                                 int32_t nreq, float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace,
+                                 size_t ws_bytes, void* stream);
+
+/* A forest of per-hypothesis prefix trees (Section 5.1, Figure 1), built on
+ * the host from (hypothesis, target phrase) pairs.  Host-only; owns its
+ * index arrays. */
+typedef struct nmt_forest nmt_forest;
+
+/* Build the forest.  Hypothesis h has last word h_hyp_word[h] (-1 = sentence
+ * start) and source sentence h_hyp_sent[h]; pair p expands hypothesis
+ * h_pair_hyp[p] by the words h_phrase_words[h_phrase_off[p] ..
+ * h_phrase_off[p+1]) (h_phrase_off has n_pairs+1 entries starting at 0).
+ * Phrases of one hypothesis that share a prefix share its tree nodes.
+ * Level d (1-based) holds one step row per tree node of depth d-1 that has
+ * children; the node's children are that row's requests, so the requests of
+ * level d are the tree edges at depth d.  Errors: NMT_EINVAL, NMT_ERANGE
+ * (a pair names a hypothesis outside [0, n_hyp)). */
+nmt_status nmt_forest_build(int32_t n_hyp, const int32_t* h_hyp_word, const int32_t* h_hyp_sent, int32_t n_pairs,
+                            const int32_t* h_pair_hyp, const int32_t* h_phrase_off, const int32_t* h_phrase_words,
+                            nmt_forest** out);
+
+/* Forest shape: depth (= longest phrase = number of steps), total rows and
+ * requests over all levels, and the largest level's row count.  Any output
+ * may be NULL. */
+nmt_status nmt_forest_shape(const nmt_forest* f, int32_t* depth, int32_t* n_rows, int32_t* n_req, int32_t* max_rows);
+
+/* Host copies of level d (1 <= d <= depth): row and request counts, and for
+ * each row its input-state row (level 1: a hypothesis index; deeper levels:
+ * the global row, counted over all levels, of the parent node's row), its
+ * previous word, sentence and request offsets (rows+1), and the requested
+ * words.  Any output may be NULL; arrays must hold the level's sizes. */
+nmt_status nmt_forest_level(const nmt_forest* f, int32_t d, int32_t* rows, int32_t* nreq, int32_t* h_state_row,
+                            int32_t* h_y_prev, int32_t* h_sent_id, int32_t* h_req_off, int32_t* h_req);
+
+/* Host copy of each pair's path: [n_pairs x depth] global request index of
+ * the pair's edge at every depth, -1 past the end of its phrase. */
+nmt_status nmt_forest_pair_paths(const nmt_forest* f, int32_t* h_path);
+
+/* Bytes of device workspace nmt_score_forest needs for forest f. */
+size_t nmt_forest_workspace_bytes(const nmt_model* m, const nmt_forest* f);
+
+/* The whole ScoreBatch procedure (Figure 2) on the device: one
+ * nmt_score_forest_step per tree depth, each level's input states gathered
+ * from the previous level's output rows, then each pair's log-probability
+ * summed along its path.
+ *   d_hyp_states [n_hyp x H]  the state that goes with each hypothesis' last
+ *                             word (the same convention as d_s_prev)
+ *   d_pair_logp [n_pairs]     out: log p(phrase | hypothesis)
+ *   d_req_logp [n_req]        out, nullable: log p of every tree edge
+ *   d_node_states [n_rows x H] out, nullable: the state each row produces
+ *                             (for reuse as hypothesis states later)
+ * Asynchronous on `stream`; f must stay alive until the work completes.
+ * Errors: NMT_EINVAL, NMT_EWORKSPACE, NMT_EDEVICE. */
+nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_forest* f, const float* d_hyp_states,
+                            float* d_pair_logp, float* d_req_logp, float* d_node_states, void* d_workspace,
+                            size_t ws_bytes, void* stream);
+
+/* Free a forest.  NULL is a no-op. */
+void nmt_forest_destroy(nmt_forest* f);
+
 /* Wait for `stream`, then report and clear the model's device error flag:
  * NMT_ERANGE if any call since the last check met an out-of-range id,
  * NMT_EDEVICE on a HIP error, else NMT_OK. */

@@ -33,7 +33,9 @@ WEIGHT_FIELDS = (
 EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_from_annotations",
            "nmt_source_info", "nmt_source_destroy", "nmt_score_workspace_bytes", "nmt_score_batch",
            "nmt_score_batch_debug", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
-           "nmt_profile_end")
+           "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
+           "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
+           "nmt_forest_destroy")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -87,11 +89,24 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_stream_status.argtypes = [_VP, _VP]
     lib.nmt_profile_begin.argtypes = [_VP, _I32]
     lib.nmt_profile_end.argtypes = [_VP, _VP, P(Timing)]
+    lib.nmt_score_forest_step.argtypes = [_VP, _VP, _I32, _VP, _I32, _VP, _VP, _VP, _VP, _VP, _I32, _VP, _VP, _VP,
+                                          _VP, ctypes.c_size_t, _VP]
+    IP = P(_I32)
+    lib.nmt_forest_build.argtypes = [_I32, IP, IP, _I32, IP, IP, IP, P(_VP)]
+    lib.nmt_forest_shape.argtypes = [_VP, IP, IP, IP, IP]
+    lib.nmt_forest_level.argtypes = [_VP, _I32, IP, IP, IP, IP, IP, IP, IP]
+    lib.nmt_forest_pair_paths.argtypes = [_VP, IP]
+    lib.nmt_forest_workspace_bytes.argtypes = [_VP, _VP]
+    lib.nmt_forest_workspace_bytes.restype = ctypes.c_size_t
+    lib.nmt_score_forest.argtypes = [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]
+    lib.nmt_forest_destroy.argtypes = [_VP]
+    lib.nmt_forest_destroy.restype = None
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
               "nmt_score_batch", "nmt_score_batch_debug", "nmt_stream_status", "nmt_profile_begin",
-              "nmt_profile_end"):
+              "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
+              "nmt_forest_level", "nmt_forest_pair_paths", "nmt_score_forest"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -269,3 +284,94 @@ def nmt_profile_end(model: Model, stream=None) -> dict:
     out = {name: float(t.ms[i]) for i, name in enumerate(PHASES)}
     out["steps"] = int(t.steps)
     return out
+
+
+def nmt_score_forest_step(model: Model, src: Source, state_pool, state_row, y_prev, sent_id, req_off, req, logp,
+                          s_new, logZ=None, workspace=None, stream=None):
+    """One ScoreBatch level: gathered input states, CSR requests (see nmt.h)."""
+    import torch
+    lib = load_library()
+    B = int(y_prev.shape[0])
+    if workspace is None:
+        workspace = torch.empty(max(nmt_score_workspace_bytes(model, B), 256), dtype=torch.uint8, device="cuda")
+    _check(lib.nmt_score_forest_step(model.handle, src.handle, B, _ptr(state_pool), int(state_pool.shape[0]),
+                                     _ptr(state_row), _ptr(y_prev), _ptr(sent_id), _ptr(req_off), _ptr(req),
+                                     int(req.shape[0]), _ptr(logp), _ptr(s_new), _ptr(logZ), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)))
+
+
+def _i32p(a):
+    return a.ctypes.data_as(ctypes.POINTER(_I32))
+
+
+class Forest:
+    """nmt_forest_build over (hypothesis, phrase) pairs; host-only."""
+
+    def __init__(self, hyp_word, hyp_sent, pair_hyp, phrases):
+        lib = load_library()
+        self.hyp_word = np.ascontiguousarray(hyp_word, dtype=np.int32)
+        self.hyp_sent = np.ascontiguousarray(hyp_sent, dtype=np.int32)
+        self.pair_hyp = np.ascontiguousarray(pair_hyp, dtype=np.int32)
+        self.phrase_off = np.zeros(len(phrases) + 1, dtype=np.int32)
+        self.phrase_off[1:] = np.cumsum([len(p) for p in phrases])
+        words = [w for p in phrases for w in p]
+        self.phrase_words = np.asarray(words if words else [0], dtype=np.int32)
+        self.n_hyp, self.n_pairs = len(self.hyp_word), len(phrases)
+        h = _VP()
+        _check(lib.nmt_forest_build(self.n_hyp, _i32p(self.hyp_word), _i32p(self.hyp_sent), self.n_pairs,
+                                    _i32p(self.pair_hyp), _i32p(self.phrase_off), _i32p(self.phrase_words),
+                                    ctypes.byref(h)))
+        self.handle = h
+
+    def shape(self) -> dict:
+        v = [_I32() for _ in range(4)]
+        _check(load_library().nmt_forest_shape(self.handle, *[ctypes.byref(x) for x in v]))
+        return dict(zip(("depth", "n_rows", "n_req", "max_rows"), (int(x.value) for x in v)))
+
+    def level(self, d: int) -> dict:
+        lib = load_library()
+        rows, nreq = _I32(), _I32()
+        _check(lib.nmt_forest_level(self.handle, d, ctypes.byref(rows), ctypes.byref(nreq), None, None, None,
+                                    None, None))
+        R, Q = rows.value, nreq.value
+        out = {k: np.zeros(n, np.int32) for k, n in (("state_row", R), ("y_prev", R), ("sent_id", R),
+                                                        ("req_off", R + 1), ("req", Q))}
+        _check(lib.nmt_forest_level(self.handle, d, None, None, *[_i32p(out[k]) for k in
+                                                                   ("state_row", "y_prev", "sent_id", "req_off",
+                                                                    "req")]))
+        return out
+
+    def pair_paths(self) -> np.ndarray:
+        sh = self.shape()
+        out = np.zeros((self.n_pairs, sh["depth"]), np.int32)
+        if out.size:
+            _check(load_library().nmt_forest_pair_paths(self.handle, _i32p(out)))
+        return out
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().nmt_forest_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def nmt_forest_workspace_bytes(model: Model, forest: Forest) -> int:
+    return int(load_library().nmt_forest_workspace_bytes(model.handle, forest.handle))
+
+
+def nmt_score_forest(model: Model, src: Source, forest: Forest, hyp_states, pair_logp, req_logp=None,
+                     node_states=None, workspace=None, stream=None):
+    """ScoreBatch on the device: per-pair log p(phrase | hypothesis)."""
+    import torch
+    lib = load_library()
+    if workspace is None:
+        workspace = torch.empty(max(nmt_forest_workspace_bytes(model, forest), 256), dtype=torch.uint8,
+                                device="cuda")
+    _check(lib.nmt_score_forest(model.handle, src.handle, forest.handle, _ptr(hyp_states), _ptr(pair_logp),
+                                _ptr(req_logp), _ptr(node_states), _ptr(workspace), workspace.numel(),
+                                _stream(stream)))

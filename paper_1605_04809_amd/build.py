@@ -13,7 +13,7 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmt.so")
-SOURCES = ("kernels.hip", "api.hip")
+SOURCES = ("kernels.hip", "api.hip", "forest.hip")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed-FP32 VALU instructions are disabled for all device code.

@@ -459,7 +459,7 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
       g.A = has_prev ? make_a(S, {make_seg(hprev, ldc, H, 1, m->kc)}) : make_a(S, {});
       g.Wp = m->enc_U[dir].d;
       g.Npad = m->enc_U[dir].Npad;
-      g.ep = GruEpi{hprev, ldc, Xp + (int64_t)pos * 6 * H + dir * 3 * H, ldx, m->enc_bias.brz, m->enc_bias.bni,
+      g.ep = GruEpi{hprev, ldc, nullptr, 0, Xp + (int64_t)pos * 6 * H + dir * 3 * H, ldx, m->enc_bias.brz, m->enc_bias.bni,
                     m->enc_bias.bns, src->ctx + (int64_t)pos * C + dir * H, ldc, src->len, pos, H};
     }
     e = launch_gemm_gru(p, 2, H, m->bf16, st);
@@ -527,26 +527,24 @@ size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B) {
   return ws_layout(m, B).total;
 }
 
-nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
-                                 const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
-                                 float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes,
-                                 void* stream, float* d_alpha, float* d_c, float* d_s1, float* d_t) {
-  if (!m || !src) return fail(NMT_EINVAL, "NULL model or source");
-  if (B < 0) return fail(NMT_EINVAL, "B must be >= 0 (got %d)", B);
-  if (B == 0) return ok();
-  if (!d_s_prev || !d_y_prev || !d_sent_id || !d_req || !d_logp || !d_s_new)
-    return fail(NMT_EINVAL, "a required device pointer is NULL");
-  if (!aligned16(d_s_prev) || !aligned16(d_s_new))
-    return fail(NMT_EINVAL, "d_s_prev and d_s_new must be 16-byte aligned");
-  if ((d_c && !aligned16(d_c)) || (d_s1 && !aligned16(d_s1)) || (d_t && !aligned16(d_t)))
-    return fail(NMT_EINVAL, "debug outputs must be 16-byte aligned");
+}  // extern "C"
+
+namespace {
+
+// One batched decoder step (the forward step of Section 5.1) for B rows.
+// Row b's input state is row state_row[b] of the state pool (row b when
+// state_row is NULL), its previous word y_prev[b], and its requested words
+// are given by rq.  Debug outputs are optional.
+nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const float* pool, int32_t pool_rows,
+                      const int32_t* state_row, const int32_t* d_y_prev, const int32_t* d_sent_id, Requests rq,
+                      float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes, hipStream_t st,
+                      float* d_alpha, float* d_c, float* d_s1, float* d_t) {
   const WsLayout L = ws_layout(m, B);
   if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < L.total) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
   nmt_status rc = check_device(m);
   if (rc != NMT_OK) return rc;
 
-  hipStream_t st = (hipStream_t)stream;
   const nmt_dims& d = m->dims;
   const int E = d.E, H = d.H, Aw = d.A, C = 2 * H, V = d.V;
   char* ws = (char*)d_workspace;
@@ -556,6 +554,9 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
   float* t = (float*)(ws + L.t);
   float2* part = (float2*)(ws + L.part);
   const ASeg x_seg = emb_seg(m, m->emb_tgt, d_y_prev, V);  // E_i: embedding rows of the previous words
+  ASeg h_seg = make_seg(pool, H, H, 1, m->kc);             // H_{i-1}: input states, gathered by row
+  h_seg.gather = state_row;
+  h_seg.gmax = pool_rows;
   hipEvent_t* ev = nullptr;
   if (m->prof_on && m->prof_used < m->prof_max) ev = &m->prof_events[(size_t)(m->prof_used++) * (NMT_NUM_PHASES + 1)];
   hipError_t e = hipSuccess;
@@ -566,10 +567,11 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
 
   // first GRU: s1 = GRU(x, s_prev)
   GruProblem g1;
-  g1.A = make_a(B, {x_seg, make_seg(d_s_prev, H, H, 1, m->kc)});
+  g1.A = make_a(B, {x_seg, h_seg});
   g1.Wp = m->g1.d;
   g1.Npad = m->g1.Npad;
-  g1.ep = GruEpi{d_s_prev, H, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns, s1, H, nullptr, 0, H};
+  g1.ep = GruEpi{pool, H, state_row, pool_rows, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns,
+                 s1, H, nullptr, 0, H};
   if (e == hipSuccess) e = launch_gemm_gru(&g1, 1, H, m->bf16, st);
   mark(NMT_PHASE_GRU1 + 1);
   // attention query q = s1 att_Wq
@@ -589,29 +591,53 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
     g2.A = make_a(B, {make_seg(s1, H, H, 1, m->kc), make_seg(c, C, C, 0, m->kc)});
     g2.Wp = m->g2.d;
     g2.Npad = m->g2.Npad;
-    g2.ep = GruEpi{s1, H, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H, nullptr, 0, H};
+    g2.ep = GruEpi{s1, H, nullptr, 0, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H,
+                   nullptr, 0, H};
     e = launch_gemm_gru(&g2, 1, H, m->bf16, st);
   }
   mark(NMT_PHASE_GRU2 + 1);
   // readout t = tanh(s_new Ws + x Wy + c Wc + b)
   if (e == hipSuccess) {
     PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
-    e = launch_gemm_plain(Tile::Small, make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, make_seg(c, C, C, 0, m->kc)}), m->ro,
+    e = launch_gemm_plain(Tile::Small,
+                          make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, make_seg(c, C, C, 0, m->kc)}), m->ro,
                           ep, st);
   }
   mark(NMT_PHASE_READOUT + 1);
-  // vocabulary projection with per-tile log-sum-exp, then the combine
+  // vocabulary projection with an online log-sum-exp per slice, then the combine
   if (e == hipSuccess) e = launch_vocab_lse(t, B, E, m->out, m->out_b, V, part, L.nS, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
-    e = launch_lse_combine(B, part, L.nS, t, E, m->out, m->out_b, V, d_req, d_y_prev, d_sent_id, src->S, d_logp,
-                           d_logZ, m->err, st);
+    e = launch_lse_combine(B, part, L.nS, t, E, m->out, m->out_b, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
+                           m->err, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && d_c) e = hipMemcpyAsync(d_c, c, (size_t)B * C * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && d_t) e = hipMemcpyAsync(d_t, t, (size_t)B * E * 4, hipMemcpyDeviceToDevice, st);
-  if (e != hipSuccess) return hip_fail(e, "nmt_score_batch");
+  if (e != hipSuccess) return hip_fail(e, "score step");
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                                 const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
+                                 float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes,
+                                 void* stream, float* d_alpha, float* d_c, float* d_s1, float* d_t) {
+  if (!m || !src) return fail(NMT_EINVAL, "NULL model or source");
+  if (B < 0) return fail(NMT_EINVAL, "B must be >= 0 (got %d)", B);
+  if (B == 0) return ok();
+  if (!d_s_prev || !d_y_prev || !d_sent_id || !d_req || !d_logp || !d_s_new)
+    return fail(NMT_EINVAL, "a required device pointer is NULL");
+  if (!aligned16(d_s_prev) || !aligned16(d_s_new))
+    return fail(NMT_EINVAL, "d_s_prev and d_s_new must be 16-byte aligned");
+  if ((d_c && !aligned16(d_c)) || (d_s1 && !aligned16(d_s1)) || (d_t && !aligned16(d_t)))
+    return fail(NMT_EINVAL, "debug outputs must be 16-byte aligned");
+  Requests rq{nullptr, d_req, B, nullptr, 0};
+  return score_step(m, src, B, d_s_prev, B, nullptr, d_y_prev, d_sent_id, rq, d_logp, d_s_new, d_logZ, d_workspace,
+                    ws_bytes, (hipStream_t)stream, d_alpha, d_c, d_s1, d_t);
 }
 
 nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
@@ -620,6 +646,45 @@ nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const
   return nmt_score_batch_debug(m, src, B, d_s_prev, d_y_prev, d_sent_id, d_req, d_logp, d_s_new, d_logZ, d_workspace,
                                ws_bytes, stream, nullptr, nullptr, nullptr, nullptr);
 }
+
+nmt_status nmt_score_forest_step(nmt_model* m, const nmt_source* src, int32_t B, const float* d_state_pool,
+                                 int32_t pool_rows, const int32_t* d_state_row, const int32_t* d_y_prev,
+                                 const int32_t* d_sent_id, const int32_t* d_req_off, const int32_t* d_req,
+                                 int32_t nreq, float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace,
+                                 size_t ws_bytes, void* stream) {
+  if (!m || !src) return fail(NMT_EINVAL, "NULL model or source");
+  if (B < 0 || nreq < 0 || pool_rows < 0) return fail(NMT_EINVAL, "negative size");
+  if (B == 0) return ok();
+  if (!d_state_pool || !d_state_row || !d_y_prev || !d_sent_id || !d_req_off || (nreq > 0 && (!d_req || !d_logp)) ||
+      !d_s_new)
+    return fail(NMT_EINVAL, "a required device pointer is NULL");
+  if (!aligned16(d_state_pool) || !aligned16(d_s_new))
+    return fail(NMT_EINVAL, "d_state_pool and d_s_new must be 16-byte aligned");
+  Requests rq{d_req_off, d_req, nreq, d_state_row, pool_rows};
+  return score_step(m, src, B, d_state_pool, pool_rows, d_state_row, d_y_prev, d_sent_id, rq, d_logp, d_s_new, d_logZ,
+                    d_workspace, ws_bytes, (hipStream_t)stream, nullptr, nullptr, nullptr, nullptr);
+}
+
+}  // extern "C"
+
+// Entry points for forest.hip.
+namespace nmt {
+nmt_status forest_fail(nmt_status st, const char* msg) { return fail(st, "%s", msg); }
+}  // namespace nmt
+
+nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t B, const float* pool,
+                                   int32_t pool_rows, const int32_t* state_row, const int32_t* y_prev,
+                                   const int32_t* sent_id, const int32_t* req_off, const int32_t* req, int32_t nreq,
+                                   float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st) {
+  if (B == 0) return ok();
+  Requests rq{req_off, req, nreq, state_row, pool_rows};
+  return score_step(m, src, B, pool, pool_rows, state_row, y_prev, sent_id, rq, logp, s_new, nullptr, ws, ws_bytes, st,
+                    nullptr, nullptr, nullptr, nullptr);
+}
+
+int32_t nmt_internal_hidden(const nmt_model* m) { return m->dims.H; }
+
+extern "C" {
 
 nmt_status nmt_stream_status(nmt_model* m, void* stream) {
   if (!m) return fail(NMT_EINVAL, "NULL model");

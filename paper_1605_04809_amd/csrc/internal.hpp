@@ -61,6 +61,8 @@ struct PlainEpi {
 struct GruEpi {
   const float* h;     // previous state rows (nullable: zero state)
   int64_t ldh;
+  const int32_t* hrow;  // nullable: row m's state is row hrow[m] of h (outside [0, hrows): zero state)
+  int32_t hrows;
   const float* xin;   // nullable: precomputed input-side pre-activations [r|z|n] per row
   int64_t ldx;
   const float* brz;   // [2H] summed r,z biases
@@ -89,8 +91,18 @@ int vocab_slices(int M, int64_t Npad);
 int vocab_max_kpad(bool bf16);
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
                             int nS, hipStream_t st);
+// Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same
+// indices (req_off nullable: one request per row, req[b] -> logp[b]).
+// state_row (nullable) is checked against pool_rows like the other ids.
+struct Requests {
+  const int32_t* req_off;
+  const int32_t* req;
+  int32_t nreq;
+  const int32_t* state_row;
+  int32_t pool_rows;
+};
 hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
-                              const float* bias, int V, const int32_t* req, const int32_t* y_prev,
+                              const float* bias, int V, const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
                               hipStream_t st);
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx,

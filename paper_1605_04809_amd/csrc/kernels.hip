@@ -214,7 +214,11 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
         xz = x[H + j];
         xn = x[2 * H + j];
       }
-      const float hp = ep.h ? ep.h[(int64_t)row * ep.ldh + j] : 0.f;
+      float hp = 0.f;
+      if (ep.h) {
+        const int hr = ep.hrow ? ep.hrow[row] : row;
+        if (!ep.hrow || (hr >= 0 && hr < ep.hrows)) hp = ep.h[(int64_t)hr * ep.ldh + j];
+      }
       const float rg = sigmoidf_(ar[i][r] + br + xr);
       const float zg = sigmoidf_(az[i][r] + bz + xz);
       const float ng = tanhf(ani[i][r] + bni + xn + rg * (ans[i][r] + bns));
@@ -446,24 +450,32 @@ __device__ __forceinline__ float dot_vec(const f32x4& a, const f32x4& b) {
 }
 
 // One wave per row: merges the per-slice (max, sum) pairs into logZ, scores
-// the requested word with its own dot product t . out_W[:, req] + out_b[req]
+// each requested word with its own dot product t . out_W[:, w] + out_b[w]
 // (t rounded as the vocabulary kernel's MFMA inputs are), and checks the
-// row's ids (any out of range: NaN outputs and the flag).
+// row's ids.  A row with any id out of range, or with malformed request
+// offsets, gets NaN outputs and sets the flag.
 template <class P>
 __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __restrict__ part, int nS,
                                                      const float* __restrict__ t, int E, int Kpad,
                                                      const f32x4* __restrict__ Wp, int64_t Npad,
-                                                     const float* __restrict__ bias, int V,
-                                                     const int32_t* __restrict__ req,
+                                                     const float* __restrict__ bias, int V, Requests rq,
                                                      const int32_t* __restrict__ y_prev,
                                                      const int32_t* __restrict__ sent_id, int S, float* logp,
                                                      float* logZ, int* err) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= B) return;
-  const int w = req[row], y = y_prev[row], s = sent_id[row];
-  if (w < 0 || w >= V || y < -1 || y >= V || s < 0 || s >= S) {
+  const int j0 = rq.req_off ? rq.req_off[row] : row, j1 = rq.req_off ? rq.req_off[row + 1] : row + 1;
+  const bool span_ok = 0 <= j0 && j0 <= j1 && j1 <= rq.nreq;
+  bool ok = span_ok;
+  const int y = y_prev[row], s = sent_id[row];
+  ok = ok && y >= -1 && y < V && s >= 0 && s < S;
+  if (rq.state_row) ok = ok && rq.state_row[row] >= 0 && rq.state_row[row] < rq.pool_rows;
+  if (span_ok)
+    for (int j = j0; j < j1; ++j) ok = ok && rq.req[j] >= 0 && rq.req[j] < V;
+  if (!ok) {
     if (lane == 0) {
-      logp[row] = __builtin_nanf("");
+      if (span_ok)
+        for (int j = j0; j < j1; ++j) logp[j] = __builtin_nanf("");
       if (logZ) logZ[row] = __builtin_nanf("");
       atomicOr(err, 1);
     }
@@ -478,28 +490,29 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
     if (p.x != -INFINITY) sum += p.y * expf(p.x - mx);
   }
   sum = wave_sum(sum);
-  float dot = 0.f;
+  const float lz = mx + logf(sum);
   const char* tr = (const char*)(t + (int64_t)row * E);
-  for (int kq = lane; kq < Kpad / P::KV; kq += 64)
-    dot += dot_vec<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), Wp[(int64_t)kq * Npad + w]);
-  dot = wave_sum(dot);
-  if (lane == 0) {
-    const float lz = mx + logf(sum);
-    logp[row] = dot + bias[w] - lz;
-    if (logZ) logZ[row] = lz;
+  for (int j = j0; j < j1; ++j) {
+    const int w = rq.req[j];
+    float dot = 0.f;
+    for (int kq = lane; kq < Kpad / P::KV; kq += 64)
+      dot += dot_vec<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), Wp[(int64_t)kq * Npad + w]);
+    dot = wave_sum(dot);
+    if (lane == 0) logp[j] = dot + bias[w] - lz;
   }
+  if (lane == 0 && logZ) logZ[row] = lz;
 }
 
 hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
-                              const float* bias, int V, const int32_t* req, const int32_t* y_prev,
+                              const float* bias, int V, const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   if (W.bf16)
     hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
-                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, req, y_prev, sent_id, S, logp, logZ, err);
+                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, rq, y_prev, sent_id, S, logp, logZ, err);
   else
     hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
-                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, req, y_prev, sent_id, S, logp, logZ, err);
+                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, rq, y_prev, sent_id, S, logp, logZ, err);
   return hipGetLastError();
 }
 

@@ -194,3 +194,34 @@ def random_annotations(cfg: Config, seed: int, scale: float = 1.0) -> np.ndarray
     """Source annotations [S, Tpad, 2H] drawn N(0, scale) for injected-context tests."""
     rng = np.random.default_rng(seed)
     return (rng.standard_normal((cfg.S, cfg.Tpad, cfg.C), dtype=np.float32) * np.float32(scale))
+
+
+@dataclass
+class ForestWorkload:
+    """(hypothesis, target phrase) pairs whose phrases share prefixes per hypothesis."""
+    hyp_word: np.ndarray     # [n_hyp] int32, -1 = sentence start
+    hyp_sent: np.ndarray     # [n_hyp] int32
+    hyp_state: np.ndarray    # [n_hyp, H] float32
+    pair_hyp: np.ndarray     # [n_pairs] int32
+    phrases: list            # n_pairs lists of word ids
+
+
+def make_forest(cfg: Config, n_hyp: int, seed: int, max_phrases: int = 6, max_len: int = 4,
+                branch: int = 3) -> ForestWorkload:
+    """Synthetic expansions in the shape of a phrase-based stack: each hypothesis
+    gets 1..max_phrases target phrases of 1..max_len words, drawn position by
+    position from `branch` candidate words per position, so phrases of one
+    hypothesis share prefixes as phrase-table options do."""
+    rng = np.random.default_rng(seed)
+    hyp_word = rng.integers(-1, cfg.V, size=n_hyp, dtype=np.int64).astype(np.int32)
+    hyp_sent = rng.integers(0, cfg.S, size=n_hyp, dtype=np.int64).astype(np.int32)
+    hyp_state = np.tanh(rng.standard_normal((n_hyp, cfg.H), dtype=np.float32)).astype(np.float32)
+    pair_hyp, phrases = [], []
+    for h in range(n_hyp):
+        cand = rng.integers(0, cfg.V, size=(max_len, branch), dtype=np.int64)
+        for _ in range(int(rng.integers(1, max_phrases + 1))):
+            n = int(rng.integers(1, max_len + 1))
+            pick = rng.integers(0, branch, size=n)
+            phrases.append([int(cand[i, pick[i]]) for i in range(n)])
+            pair_hyp.append(h)
+    return ForestWorkload(hyp_word, hyp_sent, hyp_state, np.asarray(pair_hyp, np.int32), phrases)

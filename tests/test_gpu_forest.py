@@ -1,0 +1,142 @@
+"""GPU parity of the ScoreBatch procedure (Section 5.1, Figure 2) against the
+oracle's naive scoring, which steps every (hypothesis, phrase) pair through
+its phrase word by word with no sharing at all.  The forest must give every
+pair the same log-probability while running one step per tree depth."""
+import numpy as np
+import pytest
+
+from paper_1605_04809_amd.workloads import CONFIGS, high_signal, make_forest, make_workload, random_annotations
+
+pytestmark = pytest.mark.gpu
+
+TOL_TOKEN = 1e-4   # per scored word, fp32 (a phrase of k words: k * TOL_TOKEN)
+
+
+def _torch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def oracle_pairs(o, fw, pairs):
+    """Naive scoring: each pair stepped through its phrase on its own (fp64 states)."""
+    pairs = np.asarray(pairs)
+    hyp = fw.pair_hyp[pairs]
+    lens = np.array([len(fw.phrases[p]) for p in pairs])
+    state = fw.hyp_state[hyp].astype(np.float64)
+    y = fw.hyp_word[hyp].copy()
+    total = np.zeros(len(pairs))
+    for k in range(int(lens.max()) if len(pairs) else 0):
+        live = np.nonzero(lens > k)[0]
+        w = np.array([fw.phrases[pairs[i]][k] for i in live], np.int32)
+        r = o.step(state[live], y[live], fw.hyp_sent[hyp[live]], w, intermediates=False)
+        total[live] += r["logp"]
+        state[live] = r["s_new"]
+        y[live] = w
+    return total, lens
+
+
+def run_forest(g, fw, with_nodes=False):
+    torch = _torch()
+    from paper_1605_04809_amd import binding as nb
+    f = nb.Forest(fw.hyp_word, fw.hyp_sent, fw.pair_hyp, fw.phrases)
+    sh = f.shape()
+    hs = torch.from_numpy(fw.hyp_state).cuda()
+    pair_logp = torch.empty(len(fw.phrases), device="cuda")
+    req_logp = torch.empty(max(sh["n_req"], 1), device="cuda")
+    nodes = torch.empty((max(sh["n_rows"], 1), fw.hyp_state.shape[1]), device="cuda") if with_nodes else None
+    nb.nmt_score_forest(g.model, g.src, f, hs, pair_logp, req_logp=req_logp, node_states=nodes)
+    torch.cuda.synchronize()
+    assert nb.nmt_stream_status(g.model) == nb.NMT_OK
+    return f, pair_logp.cpu().numpy(), req_logp.cpu().numpy(), nodes
+
+
+@pytest.mark.parametrize("variant", ["tiny", "tiny_high_signal"])
+def test_forest_matches_naive_stepping(variant):
+    _torch()
+    from tests import gpu_cases
+    cfg = CONFIGS["tiny"].replace(S=3, len_lo=2, len_hi=10)
+    ctx = None
+    if variant == "tiny_high_signal":
+        cfg = high_signal(cfg).replace(sigma_w=0.3)
+        ctx = random_annotations(cfg, seed=21)
+    wl = make_workload(cfg)
+    fw = make_forest(cfg, n_hyp=60, seed=5, max_phrases=6, max_len=5, branch=2)
+    g, o = gpu_cases.GpuRun(wl, ctx_f32=ctx), gpu_cases.OracleRun(wl, ctx_f32=ctx)
+    f, got, _, _ = run_forest(g, fw)
+    want, lens = oracle_pairs(o, fw, np.arange(len(fw.phrases)))
+    err = np.abs(got - want)
+    print(f"{variant}: {len(fw.phrases)} pairs, depth {f.shape()['depth']}, "
+          f"{f.shape()['n_req']} edges, max err {err.max():.2e}", flush=True)
+    assert np.all(err <= TOL_TOKEN * lens)
+    f.close()
+    g.close()
+
+
+def test_forest_step_equals_duplicated_rows():
+    """A CSR row with gathered state equals one plain row per request, bit for bit."""
+    torch = _torch()
+    from tests import gpu_cases
+    from paper_1605_04809_amd import binding as nb
+    cfg = high_signal(CONFIGS["tiny"]).replace(S=2, len_lo=3)
+    wl = make_workload(cfg)
+    fw = make_forest(cfg, n_hyp=50, seed=9, max_phrases=5, max_len=3, branch=3)
+    g = gpu_cases.GpuRun(wl)
+    f = nb.Forest(fw.hyp_word, fw.hyp_sent, fw.pair_hyp, fw.phrases)
+    lv = f.level(1)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    R, Q = lv["y_prev"].size, lv["req"].size
+    logp = torch.empty(Q, device="cuda")
+    s_new = torch.empty((R, cfg.H), device="cuda")
+    nb.nmt_score_forest_step(g.model, g.src, cu(fw.hyp_state), cu(lv["state_row"]), cu(lv["y_prev"]),
+                             cu(lv["sent_id"]), cu(lv["req_off"]), cu(lv["req"]), logp, s_new)
+    # the same requests as plain rows, the state and inputs duplicated per request
+    rows = np.repeat(np.arange(R), np.diff(lv["req_off"]))
+    hyp = lv["state_row"][rows]
+    dup = g.step(fw.hyp_state[hyp], lv["y_prev"][rows], lv["sent_id"][rows], lv["req"], debug=False)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(logp.cpu().numpy(), dup["logp"])
+    np.testing.assert_array_equal(s_new.cpu().numpy()[rows], dup["s_new"])
+    f.close()
+    g.close()
+
+
+def test_forest_paper_scale_sampled_pairs():
+    """1000 hypotheses of the en->ru shape with up to 4 phrases of up to 4 words each."""
+    _torch()
+    from tests import gpu_cases
+    wl = make_workload(CONFIGS["enru_b2000"])
+    fw = make_forest(wl.cfg, n_hyp=1000, seed=11, max_phrases=4, max_len=4, branch=3)
+    g = gpu_cases.GpuRun(wl)
+    f, got, _, _ = run_forest(g, fw, with_nodes=True)
+    sh = f.shape()
+    print(f"paper scale: {len(fw.phrases)} pairs, {sh['n_req']} edges, {sh['n_rows']} rows, "
+          f"depth {sh['depth']}, widest level {sh['max_rows']} rows", flush=True)
+    assert np.all(np.isfinite(got)) and np.all(got <= 0)
+    pairs = np.random.default_rng(4).choice(len(fw.phrases), size=24, replace=False)
+    want, lens = oracle_pairs(gpu_cases.OracleRun(wl), fw, pairs)
+    err = np.abs(got[pairs] - want)
+    print(f"max err {err.max():.2e}", flush=True)
+    assert np.all(err <= TOL_TOKEN * lens)
+    f.close()
+    g.close()
+
+
+def test_forest_bad_word_gives_nan_and_status():
+    torch = _torch()
+    from tests import gpu_cases
+    from paper_1605_04809_amd import binding as nb
+    wl = make_workload(CONFIGS["tiny"])
+    fw = make_forest(wl.cfg, n_hyp=5, seed=2, max_phrases=2, max_len=3, branch=2)
+    fw.phrases[0] = list(fw.phrases[0]) + [wl.cfg.V + 5]   # an out-of-range word at the end of pair 0
+    g = gpu_cases.GpuRun(wl)
+    f, got, _, _ = None, None, None, None
+    f = nb.Forest(fw.hyp_word, fw.hyp_sent, fw.pair_hyp, fw.phrases)
+    out = torch.empty(len(fw.phrases), device="cuda")
+    nb.nmt_score_forest(g.model, g.src, f, torch.from_numpy(fw.hyp_state).cuda(), out)
+    torch.cuda.synchronize()
+    assert np.isnan(out.cpu().numpy()[0])
+    assert nb.nmt_stream_status(g.model) == nb.NMT_ERANGE
+    f.close()
+    g.close()
