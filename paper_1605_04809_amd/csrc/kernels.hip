@@ -266,13 +266,23 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
 constexpr int VTM = 64;                 // rows per block
 constexpr int VNW = 8;                  // waves per block
 constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
-constexpr int VPF = 4;                  // k groups of weight fragments in flight per wave
-
+// Per precision (measured on MI355X): VFN 32-column blocks per wave step
+// and up to VPF_MAX k groups of weight fragments in flight.  fp32: one block,
+// 16 deep; bf16: two blocks (each A fragment feeds two MFMAs), 8 deep.
 template <class P>
+struct VocabTune {
+  static constexpr int VFN = P::kBF16 ? 2 : 1;
+  static constexpr int VPF_MAX = P::kBF16 ? 8 : 16;
+};
+
+// VPF (ring depth) must divide the k groups per column block; the launcher
+// picks the deepest that does.
+template <class P, int VPF>
 __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E, int Kpad,
                                                         const f32x4* __restrict__ Wp, int64_t Npad,
                                                         const float* __restrict__ bias, int V, int nM, int nS,
                                                         float2* __restrict__ part) {
+  constexpr int VFN = VocabTune<P>::VFN;
   __shared__ f32x4 As[VQMAX];
   __shared__ float red[VNW][VTM][2];
   const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
@@ -291,11 +301,13 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   }
   __syncthreads();
 
-  // this slice's 32-column blocks, balanced over the slices
+  // This slice's 32-column blocks, balanced over the slices, taken in groups
+  // of VFN consecutive blocks; wave w takes groups w, w+8, ...
   const int NB = (int)(Npad / 32);
   const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
+  const int ngrp = (cb_end - cb_begin + VFN - 1) / VFN;
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
-  const int nblk = cb_end - cb_begin > wave ? (cb_end - cb_begin - wave + VNW - 1) / VNW : 0;
+  const int nmine = ngrp > wave ? (ngrp - wave + VNW - 1) / VNW : 0;
 
   float run_m[2][16], run_s[2][16];
 #pragma unroll
@@ -306,38 +318,45 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
       run_s[i][r] = 0.f;
     }
 
-  // Weight fragments are read in (column block, k group) order through a
-  // scalar cursor; fragment p of the ring always holds step q with
-  // q % VPF == p.  Loads past this wave's last step re-read fragment 0 of
-  // the matrix (always in bounds) so that no load sits behind a branch.
-  const int total = nblk * NKG;
+  // Weight fragments are read in (group, k group) order through a scalar
+  // cursor; ring slot p always holds step q with q % VPF == p.  Loads past
+  // this wave's last step, or of a group's missing last blocks, re-read
+  // fragment 0 of the matrix (always in bounds) so that no load sits behind
+  // a branch.
+  const int total = nmine * NKG;
   const f32x4* wlane = Wp + (int64_t)h * Npad + l32;
-  int pcb = cb_begin + wave, pkg = 0, issued = 0;
-  auto load_next = [&]() {
-    const int64_t off = issued < total ? (int64_t)(2 * pkg) * Npad + (int64_t)pcb * 32 : 0;
+  int pg = wave, pkg = 0, issued = 0;
+  auto load_next = [&](f32x4 (&dst)[VFN]) {
+#pragma unroll
+    for (int f = 0; f < VFN; ++f) {
+      const int cb = cb_begin + pg * VFN + f;
+      const int64_t off = issued < total && cb < cb_end ? (int64_t)(2 * pkg) * Npad + (int64_t)cb * 32 : 0;
+      dst[f] = wlane[off];
+    }
     ++issued;
     if (++pkg == NKG) {
       pkg = 0;
-      pcb += VNW;
+      pg += VNW;
     }
-    return wlane[off];
   };
-  f32x4 ring[VPF];
+  f32x4 ring[VPF][VFN];
 #pragma unroll
-  for (int p = 0; p < VPF; ++p) ring[p] = load_next();
+  for (int p = 0; p < VPF; ++p) load_next(ring[p]);
   // A fragments ping-pong between an even and an odd register set (VPF is
   // even), so neither ring needs register moves at the loop back-edge.
   const f32x4* arow = As + h * VTM + l32;  // + 2*kg*VTM per k group
   f32x4 ae0 = arow[0], ae1 = arow[32], ao0, ao1;
   static_assert(VPF % 2 == 0, "even/odd fragment sets");
 
-  for (int q0 = 0; q0 < total; q0 += NKG) {
-    f32x16 acc0 = f32x16{}, acc1 = f32x16{};
+  for (int gi = 0; gi < nmine; ++gi) {
+    f32x16 acc[2][VFN];
+#pragma unroll
+    for (int f = 0; f < VFN; ++f) acc[0][f] = acc[1][f] = f32x16{};
     for (int kg0 = 0; kg0 < NKG; kg0 += VPF) {
 #pragma unroll
       for (int p = 0; p < VPF; ++p) {
         const int kg = kg0 + p;
-        const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next column block)
+        const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
         const f32x4* an = arow + kn * 2 * VTM;
         f32x4 a0, a1;
         if (p % 2 == 0) {
@@ -351,25 +370,31 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
           a0 = ao0;
           a1 = ao1;
         }
-        P::mma(a0, ring[p], acc0);
-        P::mma(a1, ring[p], acc1);
-        ring[p] = load_next();  // refill the slot just consumed, VPF steps ahead
+#pragma unroll
+        for (int f = 0; f < VFN; ++f) {
+          P::mma(a0, ring[p][f], acc[0][f]);
+          P::mma(a1, ring[p][f], acc[1][f]);
+        }
+        load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
       }
     }
-    // fold this 32-column block into the running (max, sum) of each row slot
-    const int n = (cb_begin + wave + VNW * (q0 / NKG)) * 32 + l32;
-    if (n < V) {
-      const float bn = bias[n];
+    // fold the group's columns into the running (max, sum) of each row slot
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float z0 = acc0[r] + bn, z1 = acc1[r] + bn;
-        const float m0n = fmaxf(run_m[0][r], z0), m1n = fmaxf(run_m[1][r], z1);
-        run_s[0][r] = run_s[0][r] * __builtin_amdgcn_exp2f((run_m[0][r] - m0n) * kLog2e) +
-                      __builtin_amdgcn_exp2f((z0 - m0n) * kLog2e);
-        run_s[1][r] = run_s[1][r] * __builtin_amdgcn_exp2f((run_m[1][r] - m1n) * kLog2e) +
-                      __builtin_amdgcn_exp2f((z1 - m1n) * kLog2e);
-        run_m[0][r] = m0n;
-        run_m[1][r] = m1n;
+    for (int f = 0; f < VFN; ++f) {
+      const int cb = cb_begin + (wave + VNW * gi) * VFN + f;
+      const int n = cb * 32 + l32;
+      if (cb < cb_end && n < V) {
+        const float bn = bias[n];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float z = acc[i][f][r] + bn;
+            const float mn = fmaxf(run_m[i][r], z);
+            run_s[i][r] = run_s[i][r] * __builtin_amdgcn_exp2f((run_m[i][r] - mn) * kLog2e) +
+                          __builtin_amdgcn_exp2f((z - mn) * kLog2e);
+            run_m[i][r] = mn;
+          }
       }
     }
   }
@@ -417,20 +442,34 @@ int vocab_slices(int M, int64_t Npad) {
 
 int vocab_max_kpad(bool bf16) { return VQMAX / VTM * (bf16 ? PrecBF16::KV : PrecF32::KV); }
 
+template <class P>
+hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part, int nS,
+                     hipStream_t st) {
+  const int nkg = (int)(W.Kpad / (2 * P::KV));
+  const int nM = ceil_div(M, VTM);
+  dim3 grid((unsigned)(nS / 8 * 8 * nM));
+  const f32x4* Wp = (const f32x4*)W.d;
+  constexpr int PF = VocabTune<P>::VPF_MAX;
+  if (PF >= 16 && nkg % 16 == 0)
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp,
+                       W.Npad, bias, V, nM, nS, part);
+  else if (PF >= 8 && nkg % 8 == 0)
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp,
+                       W.Npad, bias, V, nM, nS, part);
+  else if (nkg % 4 == 0)
+    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad, bias, V,
+                       nM, nS, part);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
                             int nS, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  const int KV = W.bf16 ? PrecBF16::KV : PrecF32::KV;
-  if (W.Kpad > vocab_max_kpad(W.bf16) || W.Kpad % (2 * KV * VPF)) return hipErrorInvalidValue;
-  const int nM = ceil_div(M, VTM);
-  dim3 grid((unsigned)(nS / 8 * 8 * nM));
-  if (W.bf16)
-    hipLaunchKernelGGL(k_vocab_lse<PrecBF16>, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad,
-                       (const f32x4*)W.d, W.Npad, bias, V, nM, nS, part);
-  else
-    hipLaunchKernelGGL(k_vocab_lse<PrecF32>, grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad,
-                       (const f32x4*)W.d, W.Npad, bias, V, nM, nS, part);
-  return hipGetLastError();
+  if (W.Kpad > vocab_max_kpad(W.bf16)) return hipErrorInvalidValue;
+  return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, bias, V, part, nS, st)
+                : vocab_lse<PrecF32>(t, M, E, W, bias, V, part, nS, st);
 }
 
 // ---------------------------------------------------- partials combine
