@@ -17,6 +17,7 @@ bounded row sample on the host cores.
 
   python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
   python bench.py --copy-probe BYTES   # plain copy kernel for counter calibration
+  python bench.py --forest             # ScoreBatch over a prefix-tree forest (separate line)
 """
 from __future__ import annotations
 
@@ -126,6 +127,111 @@ def copy_probe(nbytes: int, reps: int = 5):
     print(json.dumps({"copy_probe_bytes": n * 4, "reps": reps}), flush=True)
 
 
+def forest_bench(args):
+    """ScoreBatch (Section 5.1, Figure 2) on a synthetic stack of the en->ru shape.
+
+    Three ways to score the same (hypothesis, phrase) pairs:
+      forest     one row per tree node with children, CSR requests, states
+                 gathered on the device (nmt_score_forest);
+      edge rows  the paper's batching: one row per tree edge at each depth
+                 (H_{i-1} repeats a node's state once per outgoing edge);
+      naive      one single-row query per word of every expansion (timed on a
+                 sample of words and scaled to all of them).
+    """
+    import torch
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS, make_workload, make_forest
+
+    cfg = CONFIGS[args.config]
+    wl = make_workload(cfg, B=1)
+    fw = make_forest(cfg, n_hyp=args.forest_hyps, seed=11, max_phrases=4, max_len=4, branch=3)
+    model = nb.Model.from_workload(wl)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    src = nb.nmt_encode(model, cu(wl.src_ids), wl.src_len)
+    f = nb.Forest(fw.hyp_word, fw.hyp_sent, fw.pair_hyp, fw.phrases)
+    sh = f.shape()
+    hs = cu(fw.hyp_state)
+    pair_logp = torch.empty(len(fw.phrases), device="cuda")
+    ws = torch.empty(nb.nmt_forest_workspace_bytes(model, f), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    ms_forest = timed(lambda: nb.nmt_score_forest(model, src, f, hs, pair_logp, workspace=ws, stream=stream),
+                      args.steps)
+    # The paper's edge rows: each tree edge of a level is a row of its own,
+    # repeating its source node's input (Section 5.1: H_0 = [h0; h0; h1; h1]).
+    # An edge row's new state is the input state of its child edges, so a
+    # deeper edge gathers its state from its parent edge's output row.
+    levels = [f.level(d) for d in range(1, sh["depth"] + 1)]
+    H = cfg.H
+    paths = f.pair_paths()
+    src_edge = np.full(sh["n_req"], -1, np.int64)
+    for k in range(1, sh["depth"]):
+        live = paths[:, k] >= 0
+        src_edge[paths[live, k]] = paths[live, k - 1]
+    edge_in, q0 = [], 0
+    for d, lv in enumerate(levels):
+        rows = np.repeat(np.arange(lv["y_prev"].size), np.diff(lv["req_off"]))
+        state_row = lv["state_row"][rows] if d == 0 else src_edge[q0:q0 + rows.size]
+        edge_in.append(dict(state_row=cu(state_row.astype(np.int32)), y=cu(lv["y_prev"][rows]),
+                            sent=cu(lv["sent_id"][rows]), off=cu(np.arange(rows.size + 1, dtype=np.int32)),
+                            req=cu(lv["req"]), n=rows.size, q0=q0))
+        q0 += rows.size
+    max_e = max(e["n"] for e in edge_in)
+    edge_states = torch.empty((sh["n_req"], H), device="cuda")
+    e_logp = torch.empty(sh["n_req"], device="cuda")
+    ws_e = torch.empty(nb.nmt_score_workspace_bytes(model, max_e), dtype=torch.uint8, device="cuda")
+
+    def edge_rows():
+        for d, e in enumerate(edge_in):
+            pool = hs if d == 0 else edge_states
+            nb.nmt_score_forest_step(model, src, pool, e["state_row"], e["y"], e["sent"], e["off"], e["req"],
+                                     e_logp[e["q0"]:e["q0"] + e["n"]], edge_states[e["q0"]:e["q0"] + e["n"]],
+                                     workspace=ws_e, stream=stream)
+    ms_edges = timed(edge_rows, max(2, args.steps // 2))
+    # both batchings must give every edge the same log-probability
+    req_logp = torch.empty(sh["n_req"], device="cuda")
+    nb.nmt_score_forest(model, src, f, hs, pair_logp, req_logp=req_logp, workspace=ws, stream=stream)
+    edge_rows()
+    torch.cuda.synchronize()
+    same = float((req_logp - e_logp).abs().max())
+    # naive: one single-row query per word, on a sample
+    n_words = sum(len(p) for p in fw.phrases)
+    sample = min(64, n_words)
+    s1 = hs[:1].contiguous()
+    y1, sid1, r1 = cu(fw.hyp_word[:1]), cu(fw.hyp_sent[:1]), cu(np.array([fw.phrases[0][0]], np.int32))
+    lp1, sn1 = torch.empty(1, device="cuda"), torch.empty((1, H), device="cuda")
+    ws1 = torch.empty(nb.nmt_score_workspace_bytes(model, 1), dtype=torch.uint8, device="cuda")
+    ms_one = timed(lambda: nb.nmt_score_batch(model, src, s1, y1, sid1, r1, lp1, sn1, workspace=ws1, stream=stream),
+                   sample)
+    out = {"metric": "ScoreBatch scored (hypothesis, phrase) pairs/s", "value": len(fw.phrases) / (ms_forest * 1e-3),
+           "unit": "pairs/s", "higher_is_better": True, "dtype": cfg.wtype, "data": "synthetic",
+           "config": {"workload": f"forest on {cfg.name}", "hypotheses": args.forest_hyps, "pairs": len(fw.phrases),
+                      "words": n_words, "edges": sh["n_req"], "forest_rows": sh["n_rows"], "depth": sh["depth"],
+                      "rows_per_level": [int(lv["y_prev"].size) for lv in levels],
+                      "edges_per_level": [int(lv["req"].size) for lv in levels]},
+           "ms_forest": ms_forest, "ms_edge_rows": ms_edges,
+           "ms_naive_per_word_estimate": ms_one * n_words, "naive_queries": n_words,
+           "forest_queries": sh["depth"],
+           "speedup_vs_edge_rows": ms_edges / ms_forest, "speedup_vs_naive": ms_one * n_words / ms_forest,
+           "max_abs_diff_forest_vs_edge_rows": same}
+    f.close()
+    src.close()
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +241,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--print-kernel-hash", action="store_true")
+    ap.add_argument("--forest", action="store_true")
+    ap.add_argument("--forest-hyps", type=int, default=1000)
     args = ap.parse_args()
     if args.print_kernel_hash:
         print(kernel_source_hash())
@@ -152,6 +260,9 @@ def main():
         sys.exit(1)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.forest:
+        forest_bench(args)
         return
 
     from paper_1605_04809_amd import binding as nb
