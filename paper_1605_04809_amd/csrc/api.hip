@@ -270,7 +270,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * 2 * d.H * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.nS = vocab_slices((int)B, m->out.Npad);
+  L.nS = vocab_slices((int)B, m->out.Npad, m->bf16);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay

@@ -13,8 +13,8 @@
 //  * B operand (weights): packed once at model creation into
 //    [Kpad/KV][Npad][KV], so one 16-byte load fetches a whole vector.
 //  * A workgroup owns a TM x TN output tile and walks K in chunks of
-//    KC = 8 * KV (8 vectors per row per chunk), double-buffered in LDS laid
-//    out as [8][rows][16 B].
+//    KC = KQ * KV (KQ vectors per row per chunk), double-buffered in LDS laid
+//    out as [KQ][rows][16 B].
 //  * MFMA: lane l of a wave supplies row (or column) l%32; lane half
 //    h = l/32 supplies vector 2*kg + h of k group kg.  fp32 issues four
 //    v_mfma_f32_32x32x2f32 per vector pair (k = 4h + j on the j-th);
@@ -53,10 +53,16 @@ __device__ __forceinline__ f32x4 pack_bf16(const f32x4& x0, const f32x4& x1) {
   return __builtin_bit_cast(f32x4, v);
 }
 
+// Vectors per row per K chunk of the LDS-staged GEMM tiles.
+#ifndef NMT_KQ
+#define NMT_KQ 8
+#endif
+constexpr int KQ = NMT_KQ;
+
 struct PrecF32 {
   static constexpr bool kBF16 = false;
-  static constexpr int KV = 4;       // k per 16-byte vector
-  static constexpr int KC = 8 * KV;  // k per chunk
+  static constexpr int KV = 4;        // k per 16-byte vector
+  static constexpr int KC = KQ * KV;  // k per chunk
   __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
@@ -66,7 +72,7 @@ struct PrecF32 {
 struct PrecBF16 {
   static constexpr bool kBF16 = true;
   static constexpr int KV = 8;
-  static constexpr int KC = 8 * KV;
+  static constexpr int KC = KQ * KV;
   __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
                                                   0, 0, 0);
@@ -147,7 +153,6 @@ __device__ __forceinline__ f32x4 load_a_vec(const char* row, int bf16src, int K,
 // Each thread owns one tile row for A (NT % TM == 0) and strided vectors of B.
 template <int TM, int TN, int NT, class P>
 struct Stager {
-  static constexpr int KQ = 8;  // vectors per row per chunk
   static constexpr int NA = TM * KQ / NT;
   static constexpr int NB = TN * KQ / NT;
   static_assert(NT % TM == 0, "one A row per thread");
@@ -196,12 +201,12 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 // The generic main loop: walks chunks [c_begin, c_end) of the A segments
 // (all chunks by default), staging the next chunk while `compute(As, Bs)`
 // runs on the current one.  Chunk c covers packed weight vector rows
-// 8c .. 8c+7, whichever segment it falls in.
+// KQ*c .. KQ*c+KQ-1, whichever segment it falls in.
 template <int TM, int TN, int NT, class P, class Compute>
 __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __restrict__ Wp, int64_t Npad, int m0,
                                               int n0, f32x4* lds, Compute&& compute, int c_begin = 0,
                                               int c_end = 1 << 30) {
-  constexpr int ASZ = TM * 8, BSZ = TN * 8;  // vectors per stage
+  constexpr int ASZ = TM * KQ, BSZ = TN * KQ;  // vectors per stage
   f32x4* As[2] = {lds, lds + ASZ + BSZ};
   f32x4* Bs[2] = {lds + ASZ, lds + 2 * ASZ + BSZ};
   Stager<TM, TN, NT, P> st;
@@ -218,7 +223,7 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
     sg = seg_at(A, ++seg);
   }
   const char* arow = seg_row(sg, row, A.M);
-  st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)c_begin * 8, n0);
+  st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)c_begin * KQ, n0);
   st.store(As[0], Bs[0]);
   __syncthreads();
 
@@ -231,7 +236,7 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
         do { sg = seg_at(A, ++seg); } while (sg.nchunk == 0);
         arow = seg_row(sg, row, A.M);
       }
-      st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)(c + 1) * 8, n0);
+      st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)(c + 1) * KQ, n0);
     }
     compute(As[buf], Bs[buf]);
     if (more) st.store(As[buf ^ 1], Bs[buf ^ 1]);

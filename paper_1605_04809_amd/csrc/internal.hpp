@@ -87,7 +87,7 @@ hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const P
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
-int vocab_slices(int M, int64_t Npad);
+int vocab_slices(int M, int64_t Npad, bool bf16);
 int vocab_max_kpad(bool bf16);
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
                             int nS, hipStream_t st);

@@ -26,7 +26,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
                                                                            int64_t Npad, PlainEpi ep) {
   constexpr int NT = (TM / WM) * (TN / WN) * 64;
   constexpr int FM = WM / 32, FN = WN / 32;
-  __shared__ f32x4 lds[2 * (TM + TN) * 8];
+  __shared__ f32x4 lds[2 * (TM + TN) * KQ];
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm0 = (wave % (TM / WM)) * WM, wn0 = (wave / (TM / WM)) * WN;
@@ -46,7 +46,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
       A, Wp, Npad, m0, n0, lds,
       [&](const f32x4* As, const f32x4* Bs) {
 #pragma unroll
-        for (int kg = 0; kg < 4; ++kg) {
+        for (int kg = 0; kg < KQ / 2; ++kg) {
           f32x4 a[FM], b[FN];
 #pragma unroll
           for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
@@ -147,7 +147,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
-  __shared__ f32x4 lds[2 * (TM + TN) * 8];
+  __shared__ f32x4 lds[2 * (TM + TN) * KQ];
   const GruProblem& Pb = batch.p[blockIdx.z];
   const f32x4* Wp = (const f32x4*)Pb.Wp;
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
@@ -159,7 +159,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
 
   auto chunk = [&](const f32x4* As, const f32x4* Bs, auto state_side) {
 #pragma unroll
-    for (int kg = 0; kg < 4; ++kg) {
+    for (int kg = 0; kg < KQ / 2; ++kg) {
       f32x4 a[FM];
 #pragma unroll
       for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
@@ -247,42 +247,63 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
 
 // ------------------------------------------------ vocabulary projection
 
+constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
+
+// Per precision (measured on MI355X): VTM rows per block, VNW waves, VFN
+// 32-column blocks per wave step and up to VPF_MAX k groups of weight
+// fragments in flight.  fp32: 64 rows, 8 waves, one block, 16 deep.  bf16
+// (MFMAs 8x faster per k): 128 rows so each weight fragment feeds four
+// MFMAs, halving the L1 traffic per flop.
+#ifndef NMT_BF16_VTM
+#define NMT_BF16_VTM 128
+#endif
+#ifndef NMT_BF16_VFN
+#define NMT_BF16_VFN 1
+#endif
+#ifndef NMT_BF16_VNW
+#define NMT_BF16_VNW 8
+#endif
+#ifndef NMT_BF16_VPF
+#define NMT_BF16_VPF 8
+#endif
+template <class P>
+struct VocabTune {
+  static constexpr int VTM = P::kBF16 ? NMT_BF16_VTM : 64;
+  static constexpr int VNW = P::kBF16 ? NMT_BF16_VNW : 8;
+  static constexpr int VFN = P::kBF16 ? NMT_BF16_VFN : 1;
+  static constexpr int VPF_MAX = P::kBF16 ? NMT_BF16_VPF : 16;
+};
+
 // Streaming vocabulary projection with an online log-sum-exp.
 //
-// A block owns VTM = 64 rows and one slice of the vocabulary.  Its rows of
-// the readout t stay in LDS for the whole kernel as 16-byte vectors
-// [Kpad/KV][64] (128 KB fp32 / 64 KB bf16 at E = 500); the packed output
-// weights stream straight from HBM/L2 into registers, four k groups ahead,
-// so the main loop has no barrier.  Wave w of the 8 takes the slice's
-// 32-column blocks w, w+8, ...; each lane keeps a running (max, sum of exp)
-// for each of its 32 row slots, and the 32 lanes and 8 waves are merged
-// once at the end.  One (max, sum) pair per row and slice goes to HBM as
-// float2 [slice][row]; the logits never do.
+// A block owns VTM rows and one slice of the vocabulary.  Its rows of the
+// readout t stay in LDS for the whole kernel as 16-byte vectors
+// [Kpad/KV][VTM]; the packed output weights stream straight from HBM/L2 into
+// registers, VPF k groups ahead, so the main loop has no barrier.  Wave w
+// takes the slice's 32-column blocks in groups of VFN (groups w, w+VNW, ...),
+// each for all VTM rows; each lane keeps a running (max, sum of exp) for each
+// of its row slots, and the 32 lanes and the waves are merged once at the
+// end.  One (max, sum) pair per row and slice goes to HBM as float2
+// [slice][row]; the logits never do.
 //
 // Slices are spread over XCDs: blocks with ids congruent mod 8 run on one
 // XCD, and that XCD takes slices xcd, xcd+8, ... for every row tile, so the
 // row tiles of a slice read the same weights from that XCD's L2 and the
 // weights cross HBM once.
-constexpr int VTM = 64;                 // rows per block
-constexpr int VNW = 8;                  // waves per block
-constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
-// Per precision (measured on MI355X): VFN 32-column blocks per wave step
-// and up to VPF_MAX k groups of weight fragments in flight.  fp32: one block,
-// 16 deep; bf16: two blocks (each A fragment feeds two MFMAs), 8 deep.
-template <class P>
-struct VocabTune {
-  static constexpr int VFN = P::kBF16 ? 2 : 1;
-  static constexpr int VPF_MAX = P::kBF16 ? 8 : 16;
-};
-
-// VPF (ring depth) must divide the k groups per column block; the launcher
-// picks the deepest that does.
+//
+// Register discipline (checked in the ISA): the wave index is scalar
+// (readfirstlane), loads are unconditional (clamped past the end), a ring
+// slot is refilled only after its MFMAs, and A fragments ping-pong between
+// two named register sets; otherwise the compiler drains every load and
+// rotates registers at each loop back-edge.
 template <class P, int VPF>
-__global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E, int Kpad,
-                                                        const f32x4* __restrict__ Wp, int64_t Npad,
-                                                        const float* __restrict__ bias, int V, int nM, int nS,
-                                                        float2* __restrict__ part) {
-  constexpr int VFN = VocabTune<P>::VFN;
+__global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E,
+                                                                      int Kpad, const f32x4* __restrict__ Wp,
+                                                                      int64_t Npad, const float* __restrict__ bias,
+                                                                      int V, int nM, int nS,
+                                                                      float2* __restrict__ part) {
+  constexpr int VTM = VocabTune<P>::VTM, VNW = VocabTune<P>::VNW, VFN = VocabTune<P>::VFN;
+  constexpr int FM = VTM / 32;
   __shared__ f32x4 As[VQMAX];
   __shared__ float red[VNW][VTM][2];
   const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
@@ -301,17 +322,16 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   }
   __syncthreads();
 
-  // This slice's 32-column blocks, balanced over the slices, taken in groups
-  // of VFN consecutive blocks; wave w takes groups w, w+8, ...
+  // This slice's 32-column blocks, balanced over the slices, in groups of VFN.
   const int NB = (int)(Npad / 32);
   const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
   const int ngrp = (cb_end - cb_begin + VFN - 1) / VFN;
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
   const int nmine = ngrp > wave ? (ngrp - wave + VNW - 1) / VNW : 0;
 
-  float run_m[2][16], run_s[2][16];
+  float run_m[FM][16], run_s[FM][16];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       run_m[i][r] = -INFINITY;
@@ -321,8 +341,7 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   // Weight fragments are read in (group, k group) order through a scalar
   // cursor; ring slot p always holds step q with q % VPF == p.  Loads past
   // this wave's last step, or of a group's missing last blocks, re-read
-  // fragment 0 of the matrix (always in bounds) so that no load sits behind
-  // a branch.
+  // fragment 0 of the matrix (always in bounds).
   const int total = nmine * NKG;
   const f32x4* wlane = Wp + (int64_t)h * Npad + l32;
   int pg = wave, pkg = 0, issued = 0;
@@ -342,39 +361,42 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   f32x4 ring[VPF][VFN];
 #pragma unroll
   for (int p = 0; p < VPF; ++p) load_next(ring[p]);
-  // A fragments ping-pong between an even and an odd register set (VPF is
-  // even), so neither ring needs register moves at the loop back-edge.
   const f32x4* arow = As + h * VTM + l32;  // + 2*kg*VTM per k group
-  f32x4 ae0 = arow[0], ae1 = arow[32], ao0, ao1;
+  f32x4 ae[FM], ao[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) ae[i] = arow[32 * i];
   static_assert(VPF % 2 == 0, "even/odd fragment sets");
 
   for (int gi = 0; gi < nmine; ++gi) {
-    f32x16 acc[2][VFN];
+    f32x16 acc[FM][VFN];
 #pragma unroll
-    for (int f = 0; f < VFN; ++f) acc[0][f] = acc[1][f] = f32x16{};
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int f = 0; f < VFN; ++f) acc[i][f] = f32x16{};
     for (int kg0 = 0; kg0 < NKG; kg0 += VPF) {
 #pragma unroll
       for (int p = 0; p < VPF; ++p) {
         const int kg = kg0 + p;
         const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
         const f32x4* an = arow + kn * 2 * VTM;
-        f32x4 a0, a1;
+        f32x4 a[FM];
         if (p % 2 == 0) {
-          ao0 = an[0];
-          ao1 = an[32];
-          a0 = ae0;
-          a1 = ae1;
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            ao[i] = an[32 * i];
+            a[i] = ae[i];
+          }
         } else {
-          ae0 = an[0];
-          ae1 = an[32];
-          a0 = ao0;
-          a1 = ao1;
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            ae[i] = an[32 * i];
+            a[i] = ao[i];
+          }
         }
 #pragma unroll
-        for (int f = 0; f < VFN; ++f) {
-          P::mma(a0, ring[p][f], acc[0][f]);
-          P::mma(a1, ring[p][f], acc[1][f]);
-        }
+        for (int f = 0; f < VFN; ++f)
+#pragma unroll
+          for (int i = 0; i < FM; ++i) P::mma(a[i], ring[p][f], acc[i][f]);
         load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
       }
     }
@@ -386,7 +408,7 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
       if (cb < cb_end && n < V) {
         const float bn = bias[n];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const float z = acc[i][f][r] + bn;
@@ -401,7 +423,7 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
 
   // merge the 32 lanes of each half-wave (they hold different columns of the same rows)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float mx = half_max(run_m[i][r]);
@@ -415,8 +437,8 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
     }
   __syncthreads();
   // merge the waves and write this slice's partial for each row
-  if (threadIdx.x < VTM) {
-    const int rl = threadIdx.x, row = m0 + rl;
+  for (int rl = threadIdx.x; rl < VTM; rl += VNW * 64) {
+    const int row = m0 + rl;
     float mx = -INFINITY;
 #pragma unroll
     for (int w = 0; w < VNW; ++w) mx = fmaxf(mx, red[w][rl][0]);
@@ -432,33 +454,35 @@ __global__ __launch_bounds__(VNW * 64) void k_vocab_lse(const float* __restrict_
   }
 }
 
-int vocab_slices(int M, int64_t Npad) {
-  const int nM = ceil_div(M, VTM);
+int vocab_slices(int M, int64_t Npad, bool bf16) {
+  const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
   int nS = 8 * ceil_div(ceil_div(256, nM), 8);  // fill the 256 CUs (one block per CU)
   const int NB = (int)(Npad / 32);
   while (nS > 8 && nS > NB) nS -= 8;
   return nS;
 }
 
-int vocab_max_kpad(bool bf16) { return VQMAX / VTM * (bf16 ? PrecBF16::KV : PrecF32::KV); }
+int vocab_max_kpad(bool bf16) {
+  return bf16 ? VQMAX / VocabTune<PrecBF16>::VTM * PrecBF16::KV : VQMAX / VocabTune<PrecF32>::VTM * PrecF32::KV;
+}
 
 template <class P>
 hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part, int nS,
                      hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
-  const int nM = ceil_div(M, VTM);
-  dim3 grid((unsigned)(nS / 8 * 8 * nM));
+  const int nM = ceil_div(M, VocabTune<P>::VTM);
+  dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
   const f32x4* Wp = (const f32x4*)W.d;
   constexpr int PF = VocabTune<P>::VPF_MAX;
   if (PF >= 16 && nkg % 16 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp,
-                       W.Npad, bias, V, nM, nS, part);
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad,
+                       bias, V, nM, nS, part);
   else if (PF >= 8 && nkg % 8 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp,
-                       W.Npad, bias, V, nM, nS, part);
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad,
+                       bias, V, nM, nS, part);
   else if (nkg % 4 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, dim3(VNW * 64), 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad, bias, V,
-                       nM, nS, part);
+    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad, bias, V, nM, nS,
+                       part);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
