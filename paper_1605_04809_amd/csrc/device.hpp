@@ -134,6 +134,48 @@ __device__ __forceinline__ const char* seg_row(const ASeg& s, int row, int M) {
   return (const char*)s.p + r * s.ld * (s.bf16 ? 2 : 4);
 }
 
+// This thread's row of segment s for the GEMM main loop.  The address is
+// always loadable (row 0 of the segment's matrix stands in for a row past M
+// or an out-of-range id) and `ok` says whether the values count, so the
+// per-chunk loads need no branch.
+struct ARow {
+  const char* p;
+  bool ok;
+};
+__device__ __forceinline__ ARow seg_arow(const ASeg& s, int row, int M) {
+  const char* base = (const char*)s.p;
+  if (row >= M) return {base, false};
+  int64_t r = row;
+  if (s.gather) {
+    const int g = s.gather[row];
+    if (g < 0 || g >= s.gmax) return {base, false};
+    r = g;
+  }
+  return {base + r * s.ld * (s.bf16 ? 2 : 4), true};
+}
+
+// Branch-free form of load_a_vec over an ARow: columns past K are clamped
+// to column 0 for the load and zeroed after it.
+template <class P>
+__device__ __forceinline__ f32x4 load_a_vec_clamped(const ARow& r, int bf16src, int K, int k) {
+  const bool in = r.ok && k < K;
+  const int kc = k < K ? k : 0;
+  if constexpr (P::kBF16) {
+    if (bf16src) {
+      const f32x4 v = *(const f32x4*)(r.p + 2 * (int64_t)kc);  // rows padded to whole vectors
+      return in ? v : zero4();
+    }
+    const float* f = (const float*)r.p;
+    const bool in1 = in && k + 4 < K;
+    const f32x4 x0 = *(const f32x4*)(f + kc);
+    const f32x4 x1 = *(const f32x4*)(f + (in1 ? k + 4 : 0));
+    return pack_bf16(in ? x0 : zero4(), in1 ? x1 : zero4());
+  } else {
+    const f32x4 v = *(const f32x4*)((const float*)r.p + kc);
+    return in ? v : zero4();
+  }
+}
+
 // The 16-byte A vector at column k of a row, in precision P.
 template <class P>
 __device__ __forceinline__ f32x4 load_a_vec(const char* row, int bf16src, int K, int k) {
@@ -160,21 +202,22 @@ struct Stager {
   f32x4 ra[NA];
   f32x4 rb[NB];
 
-  // arow: this thread's row of the current segment (nullptr = zeros);
-  // kseg: k offset of the chunk within the segment; vq_glob: chunk start in
-  // packed-weight vector rows.
-  __device__ __forceinline__ void load(const char* arow, int bf16src, int segK, int kseg,
+  // arow: this thread's row of the current segment; kseg: k offset of the
+  // chunk within the segment; vq_glob: chunk start in packed-weight vector
+  // rows.  Weights first: their loads carry no condition.
+  __device__ __forceinline__ void load(const ARow& arow, int bf16src, int segK, int kseg,
                                        const f32x4* __restrict__ Wp, int64_t Npad, int64_t vq_glob, int n0) {
     const int tid = threadIdx.x;
     const int kq0 = tid / TM;
-#pragma unroll
-    for (int i = 0; i < NA; ++i) ra[i] = load_a_vec<P>(arow, bf16src, segK, kseg + P::KV * (kq0 + i * (NT / TM)));
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + i * NT;
       const int n = idx % TN, kq = idx / TN;
       rb[i] = Wp[(vq_glob + kq) * Npad + n0 + n];
     }
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      ra[i] = load_a_vec_clamped<P>(arow, bf16src, segK, kseg + P::KV * (kq0 + i * (NT / TM)));
   }
 
   __device__ __forceinline__ void store(f32x4* As, f32x4* Bs) const {
@@ -198,49 +241,51 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
   return S[(2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)];
 }
 
-// The generic main loop: walks chunks [c_begin, c_end) of the A segments
-// (all chunks by default), staging the next chunk while `compute(As, Bs)`
-// runs on the current one.  Chunk c covers packed weight vector rows
-// KQ*c .. KQ*c+KQ-1, whichever segment it falls in.
+// Main loop over chunks [cb, ce) of one A segment (chunk indices local to
+// the segment; vq0 = packed weight vector row of the segment's chunk 0),
+// staging the next chunk while `compute(As, Bs)` runs on the current one.
+// Ends with a barrier, so a following call may reuse the LDS stages.
+template <int TM, int TN, int NT, class P, class Compute>
+__device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
+                                             int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
+                                             int ce) {
+  // Stage s holds A at lds + s*STG and B right after it.  Stage bases are
+  // formed as offsets from `lds` itself: a runtime-indexed array of stage
+  // pointers hides the LDS address space from the compiler, which then emits
+  // flat loads that share the global-load counter, so every fragment wait
+  // would also wait for the next chunk's prefetch.
+  constexpr int ASZ = TM * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
+  if (cb >= ce) return;
+  Stager<TM, TN, NT, P> st;
+  const ARow arow = seg_arow(sg, m0 + (int)threadIdx.x % TM, M);
+  st.load(arow, sg.bf16, sg.K, cb * P::KC, Wp, Npad, vq0 + (int64_t)cb * KQ, n0);
+  st.store(lds, lds + ASZ);
+  __syncthreads();
+
+  for (int c = cb; c < ce; ++c) {
+    const bool more = c + 1 < ce;
+    const int cur = ((c - cb) & 1) * STG, nxt = STG - cur;
+    if (more) st.load(arow, sg.bf16, sg.K, (c + 1) * P::KC, Wp, Npad, vq0 + (int64_t)(c + 1) * KQ, n0);
+    compute(lds + cur, lds + cur + ASZ);
+    if (more) st.store(lds + nxt, lds + nxt + ASZ);
+    __syncthreads();
+  }
+}
+
+// All segments of A, restricted to global chunks [c_begin, c_end) (chunk c
+// covers packed weight vector rows KQ*c .. KQ*c+KQ-1, whichever segment it
+// falls in).
 template <int TM, int TN, int NT, class P, class Compute>
 __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __restrict__ Wp, int64_t Npad, int m0,
                                               int n0, f32x4* lds, Compute&& compute, int c_begin = 0,
                                               int c_end = 1 << 30) {
-  constexpr int ASZ = TM * KQ, BSZ = TN * KQ;  // vectors per stage
-  f32x4* As[2] = {lds, lds + ASZ + BSZ};
-  f32x4* Bs[2] = {lds + ASZ, lds + 2 * ASZ + BSZ};
-  Stager<TM, TN, NT, P> st;
-  const int row = m0 + (int)threadIdx.x % TM;
-
-  const int nc = total_chunks(A);
-  if (c_end > nc) c_end = nc;
-  if (c_begin >= c_end) return;
-
-  int seg = 0, ch = c_begin;
-  ASeg sg = seg_at(A, 0);
-  while (ch >= sg.nchunk) {
-    ch -= sg.nchunk;
-    sg = seg_at(A, ++seg);
-  }
-  const char* arow = seg_row(sg, row, A.M);
-  st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)c_begin * KQ, n0);
-  st.store(As[0], Bs[0]);
-  __syncthreads();
-
-  for (int c = c_begin; c < c_end; ++c) {
-    const bool more = c + 1 < c_end;
-    const int buf = (c - c_begin) & 1;
-    if (more) {
-      if (++ch == sg.nchunk) {
-        ch = 0;
-        do { sg = seg_at(A, ++seg); } while (sg.nchunk == 0);
-        arow = seg_row(sg, row, A.M);
-      }
-      st.load(arow, sg.bf16, sg.K, ch * P::KC, Wp, Npad, (int64_t)(c + 1) * KQ, n0);
-    }
-    compute(As[buf], Bs[buf]);
-    if (more) st.store(As[buf ^ 1], Bs[buf ^ 1]);
-    __syncthreads();
+  int s0 = 0;
+  for (int i = 0; i < A.nseg; ++i) {
+    const ASeg sg = seg_at(A, i);
+    const int s1 = s0 + sg.nchunk;
+    const int cb = c_begin > s0 ? c_begin : s0, ce = c_end < s1 ? c_end : s1;
+    gemm_segment<TM, TN, NT, P>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
+    s0 = s1;
   }
 }
 

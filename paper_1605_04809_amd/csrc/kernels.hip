@@ -131,8 +131,17 @@ hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi
   return hipGetLastError();
 }
 
+// The main loop loads every segment's row 0 in place of absent rows, so each
+// segment with work needs a matrix behind it.
+static bool segments_loadable(const AOperand& A) {
+  for (int i = 0; i < A.nseg; ++i)
+    if (A.seg[i].nchunk > 0 && (!A.seg[i].p || (A.seg[i].gather && A.seg[i].gmax < 1))) return false;
+  return true;
+}
+
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
   if (A.M <= 0 || ep.N <= 0) return hipSuccess;
+  if (!segments_loadable(A)) return hipErrorInvalidValue;
   return W.bf16 ? gemm_plain<PrecBF16>(t, A, W, ep, st) : gemm_plain<PrecF32>(t, A, W, ep, st);
 }
 
@@ -180,19 +189,18 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   // One main loop per A segment, each with its side fixed at compile time:
   // a per-chunk branch between the two candidate accumulators would make the
   // compiler shuttle every accumulator between AGPRs and VGPRs each chunk.
-  int c0 = 0;
+  int64_t vq0 = 0;
   for (int sg = 0; sg < Pb.A.nseg; ++sg) {
     const ASeg seg = seg_at(Pb.A, sg);
-    const int c1 = c0 + seg.nchunk;
     if (seg.side)
-      gemm_mainloop<TM, TN, NT, P>(
-          Pb.A, Wp, Pb.Npad, m0, n0, lds, [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); },
-          c0, c1);
+      gemm_segment<TM, TN, NT, P>(
+          seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
+          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); }, vq0, 0, seg.nchunk);
     else
-      gemm_mainloop<TM, TN, NT, P>(
-          Pb.A, Wp, Pb.Npad, m0, n0, lds, [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); },
-          c0, c1);
-    c0 = c1;
+      gemm_segment<TM, TN, NT, P>(
+          seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
+          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); }, vq0, 0, seg.nchunk);
+    vq0 += (int64_t)seg.nchunk * KQ;
   }
 
   const GruEpi& ep = Pb.ep;
@@ -236,6 +244,8 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   int M = probs[0].A.M;
   for (int i = 1; i < nprob; ++i) M = M > probs[i].A.M ? M : probs[i].A.M;
   if (M <= 0) return hipSuccess;
+  for (int i = 0; i < nprob; ++i)
+    if (!segments_loadable(probs[i].A)) return hipErrorInvalidValue;
   dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
   constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
   if (bf16)
