@@ -18,6 +18,7 @@ bounded row sample on the host cores.
   python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
   python bench.py --copy-probe BYTES   # plain copy kernel for counter calibration
   python bench.py --forest             # ScoreBatch over a prefix-tree forest (separate line)
+  python bench.py --ensemble K         # K models per step and their parameter average (separate line)
 """
 from __future__ import annotations
 
@@ -232,6 +233,76 @@ def forest_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def ensemble_bench(args):
+    """Several models per step (Sections 5 and 6.2): K models of the workload's
+    shape as separate features scoring the same rows in one
+    nmt_score_ensemble call, and the element-wise parameter average of the
+    same K models (Section 6.3, nmt_model_average)."""
+    import torch
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS, make_workload
+
+    cfg = CONFIGS[args.config]
+    K = args.ensemble
+    wl = make_workload(cfg)
+    B = cfg.B
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    models = [nb.Model.from_workload(wl)]
+    for k in range(1, K):
+        other = make_workload(cfg.replace(seed=cfg.seed + 1000 * k), B=1)
+        models.append(nb.Model(other.params, cfg.V_src, cfg.V, cfg.E, cfg.H, cfg.A, cfg.wtype))
+    srcs = [nb.nmt_encode(m, cu(wl.src_ids), wl.src_len) for m in models]
+    s_prev = [cu(wl.s_prev) for _ in range(K)]
+    s_new = [torch.empty_like(x) for x in s_prev]
+    y_prev, sent_id, req = cu(wl.y_prev), cu(wl.sent_id), cu(wl.req)
+    logp = torch.empty((K, B), device="cuda")
+    score = torch.empty(B, device="cuda")
+    ws = torch.empty(nb.nmt_ensemble_workspace_bytes(models, B), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    weights = [1.0 / K] * K
+
+    def step():
+        nb.nmt_score_ensemble(models, srcs, s_prev, y_prev, sent_id, req, logp, s_new, weights=weights,
+                              score=score, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    if not bool(torch.isfinite(score).all()):
+        raise SystemExit("non-finite ensemble scores")
+    # parameter averaging: read K models, write one (host clock; the call waits for its stream)
+    avg = nb.nmt_model_average(models, stream=stream)
+    avg.close()
+    reps = 3
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        nb.nmt_model_average(models, stream=stream).close()
+    ms_avg = (time.perf_counter() - t0) / reps * 1e3
+    wbytes = (2 if cfg.wtype == "bf16" else 4) * sum(
+        int(np.prod(v.shape)) for v in wl.params.values())
+    out = {"metric": f"ensemble of {K} models as separate features: scored hypothesis-words/s",
+           "value": B / (ms * 1e-3), "unit": "hypothesis-words/s (each scored by every model)",
+           "higher_is_better": True, "dtype": cfg.wtype, "data": "synthetic",
+           "config": {"workload": f"{K} x {cfg.name}", "models": K, "B": B, "V": cfg.V, "H": cfg.H},
+           "ms_per_step": ms, "model_words_per_s": K * B / (ms * 1e-3),
+           "average": {"ms": ms_avg, "models": K, "param_bytes_per_model": wbytes,
+                       "GBps_read_plus_write": (K + 1) * wbytes / (ms_avg * 1e-3) / 1e9,
+                       "timing": "host clock around the call, which allocates the new model and waits"}}
+    for x in srcs:
+        x.close()
+    for m in models:
+        m.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -243,6 +314,7 @@ def main():
     ap.add_argument("--print-kernel-hash", action="store_true")
     ap.add_argument("--forest", action="store_true")
     ap.add_argument("--forest-hyps", type=int, default=1000)
+    ap.add_argument("--ensemble", type=int, default=0, help="K models per step (separate line)")
     args = ap.parse_args()
     if args.print_kernel_hash:
         print(kernel_source_hash())
@@ -263,6 +335,9 @@ def main():
         return
     if args.forest:
         forest_bench(args)
+        return
+    if args.ensemble:
+        ensemble_bench(args)
         return
 
     from paper_1605_04809_amd import binding as nb

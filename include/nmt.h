@@ -251,6 +251,55 @@ nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_fores
 /* Free a forest.  NULL is a no-op. */
 void nmt_forest_destroy(nmt_forest* f);
 
+/* ---------------------------------------------------------- several models
+ *
+ * Section 5: one or several models enter the phrase-based log-linear model
+ * as separate instances of the same feature, each with its own tuned
+ * weight, which makes several models behave like an ensemble (Section 6.2
+ * uses two and three).  Section 6.3 replaces an ensemble by one model whose
+ * parameters are the element-wise average of the members'. */
+
+/* A new model whose every parameter is the weighted element-wise average
+ * sum_k h_coef[k] * models[k] (h_coef NULL: 1/K each, as fp32).  The models
+ * must have been created with identical nmt_dims on the current device.
+ * Accumulation is fp32 in model order; results are stored in the models'
+ * weight type (bf16 models keep every parameter, biases included, at a bf16
+ * value, rounded to nearest even).  Runs on `stream` and waits for it; the
+ * inputs stay untouched and owned by the caller; free the result with
+ * nmt_model_destroy.  1 <= K <= 32.
+ * Errors: NMT_EINVAL (NULL, mismatched models, non-finite coefficient),
+ * NMT_ERANGE (K), NMT_ENOMEM, NMT_EDEVICE. */
+nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h_coef, void* stream,
+                             nmt_model** out);
+
+/* Workspace bytes nmt_score_ensemble needs for these K models and B rows
+ * (the largest single-model step workspace; 0 for invalid arguments). */
+size_t nmt_ensemble_workspace_bytes(int32_t K, nmt_model* const* models, int32_t B);
+
+/* One batched step of the same B rows under K models (1 <= K <= 32), each
+ * a separate feature: the models share the target vocabulary, the previous
+ * words, the sentence ids and the requested words, and each has its own
+ * encoded source and its own states.
+ *   srcs[k]          model k's nmt_source (all with the same sentences)
+ *   d_s_prev[k]      [B x H_k] model k's input states
+ *   d_logp [K x B]   out: row k holds model k's log p of the requested word
+ *   d_s_new[k]       [B x H_k] out: model k's new states (may alias d_s_prev[k])
+ *   d_logZ [K x B]   out, nullable
+ *   h_weights [K]    nullable (all 1): feature weights for d_score
+ *   d_score [B]      out, nullable: sum_k h_weights[k] * d_logp[k][b], in
+ *                    model order (the ensemble's share of the log-linear score)
+ *   d_workspace      nmt_ensemble_workspace_bytes(K, models, B) bytes, 256-byte
+ *                    aligned; the models run one after another on `stream` and
+ *                    reuse it.
+ * Row semantics, id checks and allocation behaviour are those of
+ * nmt_score_batch for each model (check each model with nmt_stream_status).
+ * Errors: NMT_EINVAL, NMT_ERANGE (K), NMT_EWORKSPACE, NMT_EDEVICE. */
+nmt_status nmt_score_ensemble(int32_t K, nmt_model* const* models, const nmt_source* const* srcs, int32_t B,
+                              const float* const* d_s_prev, const int32_t* d_y_prev, const int32_t* d_sent_id,
+                              const int32_t* d_req, float* d_logp, float* const* d_s_new, float* d_logZ,
+                              const float* h_weights, float* d_score, void* d_workspace, size_t ws_bytes,
+                              void* stream);
+
 /* Wait for `stream`, then report and clear the model's device error flag:
  * NMT_ERANGE if any call since the last check met an out-of-range id,
  * NMT_EDEVICE on a HIP error, else NMT_OK. */

@@ -250,3 +250,42 @@ def vocab_logsoftmax(t: np.ndarray, out_W: np.ndarray, out_b: np.ndarray,
     _chk(lib.oracle_vocab_logsoftmax(B, E, V, tp, wp, bp, rp, lpp, lzp, lap),
          "oracle_vocab_logsoftmax")
     return logp, logZ, la
+
+
+# --------------------------------------------------------------- several models
+
+def _nearest_bf16(x32: np.ndarray) -> np.ndarray:
+    """fp32 values rounded to the nearest bf16 value, ties to even (kept as fp32)."""
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
+def average_params(params_list, coef=None, bf16: bool = False) -> Dict[str, np.ndarray]:
+    """Section 6.3: a model whose parameters are the element-wise (weighted)
+    average of K models' parameters.
+
+    Each parameter is sum_k coef[k] * p_k in fp64, then stored the way the
+    models store parameters: rounded to fp32, and for bf16 models further to
+    the nearest bf16 value (ties to even).  ``coef`` defaults to 1/K taken as
+    an fp32 number, the value the library uses.
+    """
+    K = len(params_list)
+    if coef is None:
+        coef = [float(np.float32(1.0 / K))] * K
+    out = {}
+    for name in PARAM_FIELDS:
+        acc = np.zeros(np.shape(params_list[0][name]), dtype=np.float64)
+        for k in range(K):
+            acc += np.float64(coef[k]) * np.asarray(params_list[k][name], dtype=np.float64)
+        a32 = acc.astype(np.float32)
+        out[name] = _nearest_bf16(a32) if bf16 else a32
+    return out
+
+
+def log_linear(logp: np.ndarray, weights=None) -> np.ndarray:
+    """Section 5: K models as separate features of the log-linear model; their
+    share of a hypothesis score is sum_k weight_k * logp_k (fp64).  logp: [K, B]."""
+    logp = np.asarray(logp, dtype=np.float64)
+    w = np.ones(logp.shape[0]) if weights is None else np.asarray(weights, dtype=np.float64)
+    return (w[:, None] * logp).sum(axis=0)

@@ -35,7 +35,7 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_score_batch_debug", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
            "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
-           "nmt_forest_destroy")
+           "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -101,12 +101,18 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_score_forest.argtypes = [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]
     lib.nmt_forest_destroy.argtypes = [_VP]
     lib.nmt_forest_destroy.restype = None
+    lib.nmt_model_average.argtypes = [_I32, P(_VP), P(ctypes.c_float), _VP, P(_VP)]
+    lib.nmt_ensemble_workspace_bytes.argtypes = [_I32, P(_VP), _I32]
+    lib.nmt_ensemble_workspace_bytes.restype = ctypes.c_size_t
+    lib.nmt_score_ensemble.argtypes = [_I32, P(_VP), P(_VP), _I32, P(_VP), _VP, _VP, _VP, _VP, P(_VP), _VP,
+                                       P(ctypes.c_float), _VP, _VP, ctypes.c_size_t, _VP]
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
               "nmt_score_batch", "nmt_score_batch_debug", "nmt_stream_status", "nmt_profile_begin",
               "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
-              "nmt_forest_level", "nmt_forest_pair_paths", "nmt_score_forest"):
+              "nmt_forest_level", "nmt_forest_pair_paths", "nmt_score_forest", "nmt_model_average",
+              "nmt_score_ensemble"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -158,6 +164,13 @@ class Model:
     def from_workload(cls, wl) -> "Model":
         c = wl.cfg
         return cls(wl.params, c.V_src, c.V, c.E, c.H, c.A, c.wtype)
+
+    @classmethod
+    def _wrap(cls, handle, like: "Model") -> "Model":
+        m = cls.__new__(cls)
+        m.V_src, m.V, m.E, m.H, m.A, m.C, m.wtype = like.V_src, like.V, like.E, like.H, like.A, like.C, like.wtype
+        m.handle = handle
+        return m
 
     def close(self):
         if getattr(self, "handle", None):
@@ -266,6 +279,40 @@ def nmt_score_batch(model: Model, src: Source, s_prev, y_prev, sent_id, req, log
         _check(lib.nmt_score_batch_debug(*args, _ptr(alpha), _ptr(c), _ptr(s1), _ptr(t)))
     else:
         _check(lib.nmt_score_batch(*args))
+
+
+def _handles(objs):
+    return (_VP * len(objs))(*[o.handle for o in objs])
+
+
+def nmt_model_average(models, coef=None, stream=None) -> Model:
+    """Element-wise weighted average of K models with identical dimensions."""
+    lib = load_library()
+    K = len(models)
+    c = None if coef is None else (ctypes.c_float * K)(*[float(x) for x in coef])
+    h = _VP()
+    _check(lib.nmt_model_average(K, _handles(models), c, _stream(stream), ctypes.byref(h)))
+    return Model._wrap(h, models[0])
+
+
+def nmt_ensemble_workspace_bytes(models, B: int) -> int:
+    return int(load_library().nmt_ensemble_workspace_bytes(len(models), _handles(models), B))
+
+
+def nmt_score_ensemble(models, srcs, s_prev, y_prev, sent_id, req, logp, s_new, logZ=None, weights=None,
+                       score=None, workspace=None, stream=None):
+    """One batched step of the same rows under K models; logp is [K, B]."""
+    import torch
+    lib = load_library()
+    K, B = len(models), int(y_prev.shape[0])
+    if workspace is None:
+        workspace = torch.empty(max(nmt_ensemble_workspace_bytes(models, B), 256), dtype=torch.uint8, device="cuda")
+    sp = (_VP * K)(*[_ptr(x) for x in s_prev])
+    sn = (_VP * K)(*[_ptr(x) for x in s_new])
+    w = None if weights is None else (ctypes.c_float * K)(*[float(x) for x in weights])
+    _check(lib.nmt_score_ensemble(K, _handles(models), _handles(srcs), B, sp, _ptr(y_prev), _ptr(sent_id),
+                                  _ptr(req), _ptr(logp), sn, _ptr(logZ), w, _ptr(score), _ptr(workspace),
+                                  workspace.numel(), _stream(stream)))
 
 
 def nmt_stream_status(model: Model, stream=None) -> int:

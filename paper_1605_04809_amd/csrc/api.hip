@@ -7,7 +7,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <cmath>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/nmt.h"
@@ -38,16 +40,28 @@ nmt_status ok() {
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // Device allocations owned by a model or a source.
+// A model's parameter buffers are tagged so that nmt_model_average can walk
+// them without knowing what each one holds.
+enum AllocKind : uint8_t { kOther = 0, kParamF32 = 1, kParamBF16 = 2 };
+
 struct Allocs {
   std::vector<void*> ptrs;
-  hipError_t alloc(void** p, size_t bytes) {
-    hipError_t e = hipMalloc(p, bytes < 256 ? 256 : bytes);
-    if (e == hipSuccess) ptrs.push_back(*p);
+  std::vector<size_t> bytes;
+  std::vector<uint8_t> kind;
+  hipError_t alloc(void** p, size_t n, uint8_t k = kOther) {
+    hipError_t e = hipMalloc(p, n < 256 ? 256 : n);
+    if (e == hipSuccess) {
+      ptrs.push_back(*p);
+      bytes.push_back(n);
+      kind.push_back(k);
+    }
     return e;
   }
   void release() {
     for (void* p : ptrs) (void)hipFree(p);
     ptrs.clear();
+    bytes.clear();
+    kind.clear();
   }
 };
 
@@ -129,7 +143,7 @@ std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, int kc,
 }
 
 hipError_t upload(Allocs& mem, float** d, const float* h, size_t n) {
-  hipError_t e = mem.alloc((void**)d, n * sizeof(float));
+  hipError_t e = mem.alloc((void**)d, n * sizeof(float), kParamF32);
   if (e != hipSuccess) return e;
   return hipMemcpy(*d, h, n * sizeof(float), hipMemcpyHostToDevice);
 }
@@ -139,7 +153,7 @@ hipError_t upload_w(Allocs& mem, void** d, const std::vector<float>& h, bool bf1
   if (!bf16) return upload(mem, (float**)d, h.data(), h.size());
   std::vector<uint16_t> b(h.size());
   for (size_t i = 0; i < h.size(); ++i) b[i] = to_bf16(h[i]);
-  hipError_t e = mem.alloc(d, b.size() * 2);
+  hipError_t e = mem.alloc(d, b.size() * 2, kParamBF16);
   if (e != hipSuccess) return e;
   return hipMemcpy(*d, b.data(), b.size() * 2, hipMemcpyHostToDevice);
 }
@@ -663,6 +677,159 @@ nmt_status nmt_score_forest_step(nmt_model* m, const nmt_source* src, int32_t B,
   Requests rq{d_req_off, d_req, nreq, d_state_row, pool_rows};
   return score_step(m, src, B, d_state_pool, pool_rows, d_state_row, d_y_prev, d_sent_id, rq, d_logp, d_s_new, d_logZ,
                     d_workspace, ws_bytes, (hipStream_t)stream, nullptr, nullptr, nullptr, nullptr);
+}
+
+// ------------------------------------------------------ several models
+
+// Every device pointer field of a model that refers to a parameter buffer.
+static std::vector<void**> param_fields(nmt_model* m) {
+  std::vector<void**> f = {&m->emb_src, &m->emb_tgt};
+  for (Packed* P : {&m->enc_in, &m->enc_U[0], &m->enc_U[1], &m->att_Wc, &m->init_W, &m->g1, &m->att_Wq, &m->g2,
+                    &m->ro, &m->out})
+    f.push_back(&P->d);
+  for (float** b : {&m->enc_in_b, &m->att_b, &m->init_b, &m->att_v, &m->ro_b, &m->out_b}) f.push_back((void**)b);
+  for (GruBias* g : {&m->enc_bias, &m->g1_bias, &m->g2_bias}) {
+    f.push_back((void**)&g->brz);
+    f.push_back((void**)&g->bni);
+    f.push_back((void**)&g->bns);
+  }
+  return f;
+}
+
+static bool same_layout(const nmt_model* a, const nmt_model* b) {
+  return memcmp(&a->dims, &b->dims, sizeof(nmt_dims)) == 0 && a->device == b->device && a->kc == b->kc &&
+         a->emb_ld == b->emb_ld && a->mem.bytes == b->mem.bytes && a->mem.kind == b->mem.kind;
+}
+
+nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h_coef, void* stream,
+                             nmt_model** out) {
+  if (!out) return fail(NMT_EINVAL, "NULL argument");
+  *out = nullptr;
+  if (K < 1 || K > kMaxModels) return fail(NMT_ERANGE, "K must be in [1, %d] (got %d)", kMaxModels, K);
+  if (!models) return fail(NMT_EINVAL, "NULL argument");
+  for (int k = 0; k < K; ++k) {
+    if (!models[k]) return fail(NMT_EINVAL, "models[%d] is NULL", k);
+    if (!same_layout(models[0], models[k]))
+      return fail(NMT_EINVAL, "models[%d] differs from models[0] in dimensions, weight type or device", k);
+  }
+  ModelTable tab{};
+  for (int k = 0; k < K; ++k) {
+    tab.w[k] = h_coef ? h_coef[k] : 1.f / (float)K;
+    if (!std::isfinite(tab.w[k])) return fail(NMT_EINVAL, "coefficient %d is not finite", k);
+  }
+  const nmt_model* m0 = models[0];
+  nmt_status rc = check_device(m0);
+  if (rc != NMT_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+
+  // Same dimensions and packing as models[0], fresh parameter buffers.
+  nmt_model* a = new nmt_model(*m0);
+  a->mem = Allocs{};
+  a->prof_events.clear();
+  a->prof_on = false;
+  a->prof_max = a->prof_used = 0;
+  a->err = nullptr;
+  std::unordered_map<void*, void*> remap;
+  hipError_t e = hipSuccess;
+  size_t n_param = 0;
+  for (size_t i = 0; i < m0->mem.ptrs.size() && e == hipSuccess; ++i) {
+    const uint8_t kind = m0->mem.kind[i];
+    if (kind == kOther) continue;
+    void* p = nullptr;
+    e = a->mem.alloc(&p, m0->mem.bytes[i], kind);
+    if (e != hipSuccess) break;
+    remap[m0->mem.ptrs[i]] = p;
+    ++n_param;
+    for (int k = 0; k < K; ++k) tab.p[k] = models[k]->mem.ptrs[i];
+    const int64_t n = (int64_t)(m0->mem.bytes[i] / (kind == kParamBF16 ? 2 : 4));
+    e = launch_average(K, n, tab, kind, a->bf16, p, st);
+  }
+  if (e == hipSuccess) {
+    // every parameter field must move to a buffer of its own
+    const std::vector<void**> fields = param_fields(a);
+    bool complete = fields.size() == n_param;
+    for (void** f : fields) {
+      auto it = remap.find(*f);
+      if (it == remap.end()) {
+        complete = false;
+        break;
+      }
+      *f = it->second;
+    }
+    if (!complete) {
+      (void)hipStreamSynchronize(st);
+      a->mem.release();
+      delete a;
+      return fail(NMT_EDEVICE, "nmt_model_average: parameter table does not match the model's buffers");
+    }
+    e = a->mem.alloc((void**)&a->err, sizeof(int));
+  }
+  if (e == hipSuccess) e = hipMemsetAsync(a->err, 0, sizeof(int), st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    (void)hipStreamSynchronize(st);
+    a->mem.release();
+    delete a;
+    return hip_fail(e, "nmt_model_average");
+  }
+  *out = a;
+  return ok();
+}
+
+size_t nmt_ensemble_workspace_bytes(int32_t K, nmt_model* const* models, int32_t B) {
+  if (!models || K < 1 || K > kMaxModels || B <= 0) return 0;
+  size_t mx = 0;
+  for (int k = 0; k < K; ++k) {
+    if (!models[k]) return 0;
+    const size_t b = ws_layout(models[k], B).total;
+    mx = b > mx ? b : mx;
+  }
+  return mx;
+}
+
+nmt_status nmt_score_ensemble(int32_t K, nmt_model* const* models, const nmt_source* const* srcs, int32_t B,
+                              const float* const* d_s_prev, const int32_t* d_y_prev, const int32_t* d_sent_id,
+                              const int32_t* d_req, float* d_logp, float* const* d_s_new, float* d_logZ,
+                              const float* h_weights, float* d_score, void* d_workspace, size_t ws_bytes,
+                              void* stream) {
+  if (K < 1 || K > kMaxModels) return fail(NMT_ERANGE, "K must be in [1, %d] (got %d)", kMaxModels, K);
+  if (!models || !srcs || !d_s_prev || !d_s_new) return fail(NMT_EINVAL, "NULL argument");
+  if (B < 0) return fail(NMT_EINVAL, "B must be >= 0 (got %d)", B);
+  for (int k = 0; k < K; ++k) {
+    if (!models[k] || !srcs[k]) return fail(NMT_EINVAL, "model or source %d is NULL", k);
+    if (models[k]->dims.V != models[0]->dims.V || models[k]->device != models[0]->device)
+      return fail(NMT_EINVAL, "model %d has another target vocabulary or device", k);
+    if (srcs[k]->S != srcs[0]->S) return fail(NMT_EINVAL, "source %d holds another number of sentences", k);
+    if (B > 0 && (!d_s_prev[k] || !d_s_new[k])) return fail(NMT_EINVAL, "state pointers of model %d are NULL", k);
+  }
+  if (B == 0) return ok();
+  if (!d_y_prev || !d_sent_id || !d_req || !d_logp) return fail(NMT_EINVAL, "a required device pointer is NULL");
+  ModelTable tab{};
+  for (int k = 0; k < K; ++k) {
+    tab.w[k] = h_weights ? h_weights[k] : 1.f;
+    if (!std::isfinite(tab.w[k])) return fail(NMT_EINVAL, "weight %d is not finite", k);
+  }
+  // validate everything before the first launch: a failed call enqueues nothing
+  const size_t need = nmt_ensemble_workspace_bytes(K, models, B);
+  if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < need) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  for (int k = 0; k < K; ++k)
+    if (!aligned16(d_s_prev[k]) || !aligned16(d_s_new[k]))
+      return fail(NMT_EINVAL, "state arrays of model %d must be 16-byte aligned", k);
+  nmt_status rc0 = check_device(models[0]);
+  if (rc0 != NMT_OK) return rc0;
+  for (int k = 0; k < K; ++k) {
+    // one step per model on the caller's stream; the workspace is reused in stream order
+    const nmt_status rc = nmt_score_batch(models[k], srcs[k], B, d_s_prev[k], d_y_prev, d_sent_id, d_req,
+                                          d_logp + (int64_t)k * B, d_s_new[k],
+                                          d_logZ ? d_logZ + (int64_t)k * B : nullptr, d_workspace, ws_bytes, stream);
+    if (rc != NMT_OK) return rc;
+  }
+  if (d_score) {
+    const hipError_t e = launch_weighted_sum(K, B, d_logp, tab, d_score, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "nmt_score_ensemble");
+  }
+  return ok();
 }
 
 }  // extern "C"

@@ -115,6 +115,17 @@ hipError_t launch_masked_copy(int S, int Tpad, int C, const float* src, const in
 hipError_t launch_masked_mean(int S, int Tpad, int C, const float* ctx, const int32_t* len, float* mean,
                               hipStream_t st);
 
+// Several models at once: buffer pointers and weights, passed by value.
+constexpr int kMaxModels = 32;
+struct ModelTable {
+  const void* p[kMaxModels];
+  float w[kMaxModels];
+};
+// kind 1: fp32 buffer, 2: bf16 buffer; round_bf16 rounds fp32 results to bf16 values.
+hipError_t launch_average(int K, int64_t n, const ModelTable& tab, int kind, bool round_bf16, void* dst,
+                          hipStream_t st);
+hipError_t launch_weighted_sum(int K, int B, const float* logp, const ModelTable& tab, float* out, hipStream_t st);
+
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 

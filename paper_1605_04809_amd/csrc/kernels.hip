@@ -746,4 +746,63 @@ hipError_t launch_masked_mean(int S, int Tpad, int C, const float* ctx, const in
   return hipGetLastError();
 }
 
+// ------------------------------------------------- several models
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+// Nearest bf16, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// One parameter buffer of the weighted model average: element i is
+// sum_k coef[k] * src[k][i], accumulated in fp32 in model order with fused
+// multiply-adds, then stored in the buffer's type (bf16 nearest-even; fp32,
+// or fp32 rounded to a bf16 value when the model keeps bf16 parameters).
+// The model loop is unrolled to the table size so the table stays in
+// registers.
+__global__ void k_average(int K, int64_t n, ModelTable tab, int kind, int round_bf16, void* __restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    float acc = 0.f;
+#pragma unroll
+    for (int k = 0; k < kMaxModels; ++k)
+      if (k < K) {
+        const float x = kind == 2 ? bf16_bits_to_f32(((const uint16_t*)tab.p[k])[i]) : ((const float*)tab.p[k])[i];
+        acc = fmaf(tab.w[k], x, acc);
+      }
+    if (kind == 2)
+      ((uint16_t*)dst)[i] = f32_to_bf16_bits(acc);
+    else
+      ((float*)dst)[i] = round_bf16 ? bf16_bits_to_f32(f32_to_bf16_bits(acc)) : acc;
+  }
+}
+
+hipError_t launch_average(int K, int64_t n, const ModelTable& tab, int kind, bool round_bf16, void* dst,
+                          hipStream_t st) {
+  if (K < 1 || K > kMaxModels || (kind != 1 && kind != 2)) return hipErrorInvalidValue;
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = ceil_div(n, 256) < 8192 ? ceil_div(n, 256) : 8192;
+  hipLaunchKernelGGL(k_average, dim3((unsigned)blocks), dim3(256), 0, st, K, n, tab, kind, round_bf16 ? 1 : 0, dst);
+  return hipGetLastError();
+}
+
+// out[b] = sum_k w[k] * logp[k*B + b], in model order.
+__global__ void k_weighted_sum(int K, int B, const float* __restrict__ logp, ModelTable tab, float* __restrict__ out) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  float acc = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMaxModels; ++k)
+    if (k < K) acc = fmaf(tab.w[k], logp[(int64_t)k * B + b], acc);
+  out[b] = acc;
+}
+
+hipError_t launch_weighted_sum(int K, int B, const float* logp, const ModelTable& tab, float* out, hipStream_t st) {
+  if (K < 1 || K > kMaxModels) return hipErrorInvalidValue;
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_weighted_sum, dim3(ceil_div(B, 256)), dim3(256), 0, st, K, B, logp, tab, out);
+  return hipGetLastError();
+}
+
 }  // namespace nmt

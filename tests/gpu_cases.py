@@ -20,11 +20,11 @@ def cuda(a, dtype=None):
 class GpuRun:
     """A model and source on the GPU for one workload."""
 
-    def __init__(self, wl: Workload, ctx_f32: np.ndarray = None):
+    def __init__(self, wl: Workload, ctx_f32: np.ndarray = None, model=None):
         import torch
         self.wl = wl
         c = wl.cfg
-        self.model = nb.Model.from_workload(wl)
+        self.model = nb.Model.from_workload(wl) if model is None else model
         if ctx_f32 is None:
             self.s0 = torch.empty((c.S, c.H), dtype=torch.float32, device="cuda")
             self.src = nb.nmt_encode(self.model, cuda(wl.src_ids), wl.src_len, self.s0)
