@@ -19,6 +19,7 @@ bounded row sample on the host cores.
   python bench.py --copy-probe BYTES   # plain copy kernel for counter calibration
   python bench.py --forest             # ScoreBatch over a prefix-tree forest (separate line)
   python bench.py --ensemble K         # K models per step and their parameter average (separate line)
+  python bench.py --rescore            # stack rescoring of one sentence's synthetic stacks (separate line)
 """
 from __future__ import annotations
 
@@ -303,6 +304,60 @@ def ensemble_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def rescore_bench(args):
+    """Stack rescoring (Section 5.3, Figure 4) of one sentence's synthetic
+    stacks (stack limit 1000, the paper's setting) with the workload's model:
+    each stack's predecessors go through one nmt_rescore_stack call, which
+    returns the scores to the host as the decoder needs them."""
+    import torch
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS, make_workload, make_stacks
+
+    cfg = CONFIGS[args.config]
+    wl = make_workload(cfg, B=1)
+    sent = 0
+    J = int(wl.src_len[sent])
+    sw = make_stacks(cfg, src_len=J, stack_size=args.stack_size, seed=13, sent=sent)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    model = nb.Model.from_workload(wl)
+    s0 = torch.empty((cfg.S, cfg.H), device="cuda")
+    src = nb.nmt_encode(model, cu(wl.src_ids), wl.src_len, s0)
+    n_total = sw.n_roots + sum(len(p) for p, _ in sw.stacks)
+
+    def run():
+        r = nb.Rescorer([model], [src], [s0], n_total)
+        per = []
+        for parents, phrases in sw.stacks:
+            t0 = time.perf_counter()
+            lp, _ = r.rescore(parents, phrases)
+            per.append((time.perf_counter() - t0) * 1e3)
+            if not np.all(np.isfinite(lp)):
+                raise SystemExit("non-finite rescoring scores")
+        shape = r.info()
+        r.close()
+        return per, shape
+
+    run()  # warm-up (also grows the scratch buffers once)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    per, _ = run()
+    ms = (time.perf_counter() - t0) * 1e3
+    hyps = sum(len(p) for p, _ in sw.stacks)
+    words = sum(len(ph) for _, phr in sw.stacks for ph in phr)
+    pairs = sum(len({(int(a), tuple(b)) for a, b in zip(p, phr)}) for p, phr in sw.stacks)
+    out = {"metric": "stack rescoring: rescored hypotheses/s", "value": hyps / (ms * 1e-3),
+           "unit": "hypotheses/s", "higher_is_better": True, "dtype": cfg.wtype, "data": "synthetic",
+           "config": {"workload": f"stack rescoring on {cfg.name}", "source_len": J, "stacks": len(sw.stacks),
+                      "stack_limit": args.stack_size, "hypotheses": hyps, "distinct_predecessors": pairs,
+                      "phrase_words": words},
+           "ms_sentence": ms, "ms_per_stack_max": max(per), "ms_per_stack_mean": ms / len(sw.stacks),
+           "phrase_words_per_s": words / (ms * 1e-3),
+           "timing": "host clock around each nmt_rescore_stack call (it returns the scores to the host)"}
+    src.close()
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -315,6 +370,8 @@ def main():
     ap.add_argument("--forest", action="store_true")
     ap.add_argument("--forest-hyps", type=int, default=1000)
     ap.add_argument("--ensemble", type=int, default=0, help="K models per step (separate line)")
+    ap.add_argument("--rescore", action="store_true", help="stack rescoring of one sentence (separate line)")
+    ap.add_argument("--stack-size", type=int, default=1000)
     args = ap.parse_args()
     if args.print_kernel_hash:
         print(kernel_source_hash())
@@ -338,6 +395,9 @@ def main():
         return
     if args.ensemble:
         ensemble_bench(args)
+        return
+    if args.rescore:
+        rescore_bench(args)
         return
 
     from paper_1605_04809_amd import binding as nb

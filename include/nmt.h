@@ -251,6 +251,56 @@ nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_fores
 /* Free a forest.  NULL is a no-op. */
 void nmt_forest_destroy(nmt_forest* f);
 
+/* ------------------------------------------------------- stack rescoring
+ *
+ * Section 5.3 (Figure 4): the decoder expands hypotheses with the NMT
+ * feature set to 0; once a stack is complete, the direct predecessor of each
+ * of its hypotheses -- (parent hypothesis, target phrase) -- is scored with
+ * one ScoreBatch and the 0 is replaced by the model's log-probability.  A
+ * rescorer keeps what that needs between stacks: for each of K models (the
+ * models as separate features of Section 5), the decoder state that goes
+ * with every hypothesis' last word, on the device, indexed by hypothesis id.
+ * Hypotheses are numbered in creation order: 0..S-1 are the empty
+ * hypotheses of the source's S sentences (state s0, sentence start), and
+ * each nmt_rescore_stack call numbers its n hypotheses next. */
+typedef struct nmt_rescorer nmt_rescorer;
+
+/* models[k], srcs[k]: model k and its encoding of the S sentences (all
+ * sources with the same S; all models with the same target vocabulary, on
+ * the current device).  d_s0[k] [S x H_k]: model k's initial states (from
+ * nmt_encode), copied.  capacity: most hypotheses the rescorer will hold,
+ * S included; the state pools ([capacity x H_k] fp32 per model) are
+ * allocated here.  The models and sources must outlive the rescorer.
+ * Waits for `stream`.  Errors: NMT_EINVAL, NMT_ERANGE (K outside [1, 32],
+ * capacity < S), NMT_ENOMEM, NMT_EDEVICE. */
+nmt_status nmt_rescorer_create(int32_t K, nmt_model* const* models, const nmt_source* const* srcs,
+                               const float* const* d_s0, int32_t capacity, void* stream, nmt_rescorer** out);
+
+/* Rescore one stack of n hypotheses: hypothesis j expands existing
+ * hypothesis h_parent[j] by the target words h_words[h_off[j] .. h_off[j+1])
+ * (h_off[0] = 0; an empty phrase scores 0 and keeps the parent's state).
+ * Identical (parent, phrase) predecessors are scored once; all of them go
+ * through one prefix forest (nmt_score_forest) per model.
+ *   h_logp [K x n]  out (host): h_logp[k*n + j] = log p(phrase_j | parent_j)
+ *                   under model k (natural log, full vocabulary)
+ *   h_ids [n]       out (host), nullable: the ids given to the n hypotheses
+ * Each new hypothesis' states are stored for later stacks.  Runs on `stream`
+ * and returns when the work is done (the decoder needs the scores); grows the
+ * rescorer's own device scratch when a stack needs more.  Not thread-safe per
+ * rescorer.  Errors: NMT_EINVAL, NMT_ERANGE (unknown parent, word outside the
+ * vocabulary, pool full: nothing is scored then), NMT_ENOMEM, NMT_EDEVICE. */
+nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent, const int32_t* h_off,
+                             const int32_t* h_words, float* h_logp, int32_t* h_ids, void* stream);
+
+/* Model k's state pool (device, [capacity x H_k], row = hypothesis id), the
+ * number of hypotheses so far, and the shape of the last stack's forest
+ * (unique predecessors, step rows, tree edges, depth).  Outputs nullable. */
+nmt_status nmt_rescorer_info(const nmt_rescorer* r, int32_t k, const float** d_states, int32_t* n_hyp,
+                             int32_t* last_pairs, int32_t* last_rows, int32_t* last_edges, int32_t* last_depth);
+
+/* Free a rescorer and its state pools.  NULL is a no-op. */
+void nmt_rescorer_destroy(nmt_rescorer* r);
+
 /* ---------------------------------------------------------- several models
  *
  * Section 5: one or several models enter the phrase-based log-linear model

@@ -289,3 +289,51 @@ def log_linear(logp: np.ndarray, weights=None) -> np.ndarray:
     logp = np.asarray(logp, dtype=np.float64)
     w = np.ones(logp.shape[0]) if weights is None else np.asarray(weights, dtype=np.float64)
     return (w[:, None] * logp).sum(axis=0)
+
+
+# ------------------------------------------------------------- stack rescoring
+
+def rescore_stacks(m: Model, ctx, pctx, src_len, s0, stacks):
+    """Section 5.3 (Figure 4) in plain form, one predecessor at a time.
+
+    Hypotheses are numbered 0..S-1 (the empty hypothesis of each sentence:
+    state s0, sentence start) and then in stack order.  For each stack, the
+    set L of distinct predecessors (parent, phrase) is scored word by word:
+    log p(phrase | parent) = sum_t log p(w_t | parent, w_<t), each word one
+    decoder step from the state and last word reached so far (no prefix
+    sharing, no batching beyond rows being independent).  Each hypothesis
+    gets its predecessor's score; its state is the one reached after the
+    phrase's last word (the parent's for an empty phrase), kept in fp64.
+
+    Returns (per-stack lists of fp64 scores, fp64 states [n_hyp, H]).
+    """
+    S = s0.shape[0]
+    states = [np.asarray(s0[s], np.float64) for s in range(S)]
+    last = [-1] * S
+    sent = list(range(S))
+    scores = []
+    for parents, phrases in stacks:
+        index = {}
+        for p, ph in zip(parents, phrases):
+            index.setdefault((int(p), tuple(int(w) for w in ph)), len(index))
+        pairs = list(index.keys())
+        cur = np.stack([states[p] for p, _ in pairs]) if pairs else np.zeros((0, m.H))
+        word = np.array([last[p] for p, _ in pairs], np.int32)
+        sid = np.array([sent[p] for p, _ in pairs], np.int32)
+        logp = np.zeros(len(pairs))
+        for t in range(max((len(ph) for _, ph in pairs), default=0)):
+            live = np.array([i for i, (_, ph) in enumerate(pairs) if len(ph) > t], np.int64)
+            req = np.array([pairs[i][1][t] for i in live], np.int32)
+            r = score_batch(m, ctx, pctx, src_len, cur[live], word[live], sid[live], req, intermediates=False)
+            logp[live] += r["logp"]
+            cur[live] = r["s_new"]
+            word[live] = req
+        out = np.empty(len(parents))
+        for j, (p, ph) in enumerate(zip(parents, phrases)):
+            i = index[(int(p), tuple(int(w) for w in ph))]
+            out[j] = logp[i]
+            states.append(cur[i].copy())
+            last.append(int(ph[-1]) if len(ph) else last[int(p)])
+            sent.append(sent[int(p)])
+        scores.append(out)
+    return scores, np.stack(states)

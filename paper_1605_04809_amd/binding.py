@@ -35,7 +35,8 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_score_batch_debug", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
            "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
-           "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble")
+           "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
+           "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -106,13 +107,18 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_ensemble_workspace_bytes.restype = ctypes.c_size_t
     lib.nmt_score_ensemble.argtypes = [_I32, P(_VP), P(_VP), _I32, P(_VP), _VP, _VP, _VP, _VP, P(_VP), _VP,
                                        P(ctypes.c_float), _VP, _VP, ctypes.c_size_t, _VP]
+    lib.nmt_rescorer_create.argtypes = [_I32, P(_VP), P(_VP), P(_VP), _I32, _VP, P(_VP)]
+    lib.nmt_rescore_stack.argtypes = [_VP, _I32, IP, IP, IP, P(ctypes.c_float), IP, _VP]
+    lib.nmt_rescorer_info.argtypes = [_VP, _I32, P(_VP), IP, IP, IP, IP, IP]
+    lib.nmt_rescorer_destroy.argtypes = [_VP]
+    lib.nmt_rescorer_destroy.restype = None
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
               "nmt_score_batch", "nmt_score_batch_debug", "nmt_stream_status", "nmt_profile_begin",
               "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
               "nmt_forest_level", "nmt_forest_pair_paths", "nmt_score_forest", "nmt_model_average",
-              "nmt_score_ensemble"):
+              "nmt_score_ensemble", "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -223,14 +229,22 @@ class Source:
 _hip = None
 
 
-def _hip_memcpy_d2d(dst: int, src: int, nbytes: int):
+def _hip_memcpy(dst: int, src: int, nbytes: int, kind: int):
     global _hip
     if _hip is None:
         _hip = ctypes.CDLL("libamdhip64.so")
         _hip.hipMemcpy.argtypes = [_VP, _VP, ctypes.c_size_t, ctypes.c_int]
-    rc = _hip.hipMemcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
+    rc = _hip.hipMemcpy(dst, src, nbytes, kind)
     if rc != 0:
         raise RuntimeError(f"hipMemcpy failed ({rc})")
+
+
+def _hip_memcpy_d2d(dst: int, src: int, nbytes: int):
+    _hip_memcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
+
+
+def _hip_memcpy_d2h(out: np.ndarray, src: int):
+    _hip_memcpy(out.ctypes.data, src, out.nbytes, 2)  # hipMemcpyDeviceToHost
 
 
 def _len_array(src_len):
@@ -422,3 +436,61 @@ def nmt_score_forest(model: Model, src: Source, forest: Forest, hyp_states, pair
     _check(lib.nmt_score_forest(model.handle, src.handle, forest.handle, _ptr(hyp_states), _ptr(pair_logp),
                                 _ptr(req_logp), _ptr(node_states), _ptr(workspace), workspace.numel(),
                                 _stream(stream)))
+
+
+class Rescorer:
+    """Stack rescoring state (nmt_rescorer): per-model hypothesis states on the device."""
+
+    def __init__(self, models, srcs, s0, capacity: int, stream=None):
+        lib = load_library()
+        self.K = len(models)
+        self._keep = (list(models), list(srcs), list(s0))
+        s0p = (_VP * self.K)(*[_ptr(x) for x in s0])
+        h = _VP()
+        _check(lib.nmt_rescorer_create(self.K, _handles(models), _handles(srcs), s0p, capacity, _stream(stream),
+                                       ctypes.byref(h)))
+        self.handle = h
+
+    def rescore(self, parents, phrases, stream=None):
+        """-> (logp [K, n] float32, ids [n] int32) for hypotheses (parents[j], phrases[j])."""
+        lib = load_library()
+        n = len(parents)
+        par = np.ascontiguousarray(parents, dtype=np.int32)
+        off = np.zeros(n + 1, np.int32)
+        off[1:] = np.cumsum([len(p) for p in phrases])
+        words = np.ascontiguousarray(np.concatenate([np.asarray(p, np.int64) for p in phrases])
+                                     if n else np.zeros(0), dtype=np.int32)
+        logp = np.empty((self.K, n), np.float32)
+        ids = np.empty(n, np.int32)
+        _check(lib.nmt_rescore_stack(self.handle, n, _i32p(par), _i32p(off), _i32p(words) if words.size else None,
+                                     logp.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), _i32p(ids),
+                                     _stream(stream)))
+        return logp, ids
+
+    def info(self, k: int = 0) -> dict:
+        lib = load_library()
+        d = _VP()
+        v = [_I32() for _ in range(5)]
+        _check(lib.nmt_rescorer_info(self.handle, k, ctypes.byref(d), *[ctypes.byref(x) for x in v]))
+        return {"d_states": d.value, "n_hyp": v[0].value, "last_pairs": v[1].value, "last_rows": v[2].value,
+                "last_edges": v[3].value, "last_depth": v[4].value}
+
+    def states(self, k: int = 0, H: int = None):
+        """Host copy of model k's states of all hypotheses so far."""
+        inf = self.info(k)
+        H = H or self._keep[0][k].H
+        out = np.empty((inf["n_hyp"], H), np.float32)
+        if out.size:
+            _hip_memcpy_d2h(out, inf["d_states"])
+        return out
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().nmt_rescorer_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

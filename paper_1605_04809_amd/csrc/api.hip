@@ -850,6 +850,8 @@ nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t 
 }
 
 int32_t nmt_internal_hidden(const nmt_model* m) { return m->dims.H; }
+int32_t nmt_internal_vocab(const nmt_model* m) { return m->dims.V; }
+int nmt_internal_device(const nmt_model* m) { return m->device; }
 
 extern "C" {
 

@@ -84,6 +84,8 @@ nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t 
                                    const int32_t* sent_id, const int32_t* req_off, const int32_t* req, int32_t nreq,
                                    float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st);
 int32_t nmt_internal_hidden(const nmt_model* m);
+int32_t nmt_internal_vocab(const nmt_model* m);
+int nmt_internal_device(const nmt_model* m);
 
 static ForestWs forest_ws(const nmt_model* m, const nmt_forest* f) {
   ForestWs L{};
@@ -291,6 +293,249 @@ nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_fores
                      logp, d_pair_logp);
   e = hipGetLastError();
   if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
+  return NMT_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------- stack rescoring
+//
+// Section 5.3 (Figure 4): hypotheses are expanded without the NMT feature,
+// and when a stack is complete the direct predecessor of each of its
+// hypotheses -- (parent hypothesis, target phrase) -- is scored with one
+// ScoreBatch over all of them; identical predecessors are scored once.  The
+// rescorer keeps, per model, the decoder state that goes with every
+// hypothesis' last word in a device pool indexed by hypothesis id, so a
+// stack's forest reads its roots' states straight from the pool and the new
+// hypotheses' states are gathered into it from the forest's output rows.
+
+namespace {
+
+// dst[dst_row[j]] = src_row[j] >= 0 ? nodes[src_row[j]] : pool[-src_row[j] - 1], one block per row.
+__global__ void k_gather_states(int n, int H, const int32_t* __restrict__ src_row, const int32_t* __restrict__ dst_row,
+                                const float* __restrict__ nodes, float* __restrict__ pool) {
+  const int j = blockIdx.x;
+  if (j >= n) return;
+  const int32_t s = src_row[j];
+  const float* from = s >= 0 ? nodes + (int64_t)s * H : pool + (int64_t)(-s - 1) * H;
+  float* to = pool + (int64_t)dst_row[j] * H;
+  for (int k = threadIdx.x * 4; k < H; k += blockDim.x * 4) *(float4*)(to + k) = *(const float4*)(from + k);
+}
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t cap = 0;
+  // Grows to at least `bytes` (contents are not kept); the stream is idle here.
+  hipError_t ensure(size_t bytes) {
+    if (bytes <= cap) return hipSuccess;
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+    const size_t want = bytes + bytes / 4 + 4096;
+    hipError_t e = hipMalloc(&p, want);
+    if (e == hipSuccess) cap = want;
+    return e;
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+  }
+};
+
+}  // namespace
+
+struct nmt_rescorer {
+  int32_t K = 0, S = 0, capacity = 0, n_hyp = 0;
+  std::vector<nmt_model*> models;
+  std::vector<const nmt_source*> srcs;
+  std::vector<int32_t> H;
+  std::vector<float*> pool;            // per model [capacity x H_k], owned
+  std::vector<int32_t> last_word, sent;  // per hypothesis (host)
+  DevBuf ws, nodes, pair_logp, gather;
+  std::vector<float> h_pair_logp;
+  std::vector<int32_t> h_gather;
+  int32_t last_pairs = 0, last_rows = 0, last_depth = 0, last_edges = 0;
+};
+
+extern "C" {
+
+nmt_status nmt_rescorer_create(int32_t K, nmt_model* const* models, const nmt_source* const* srcs,
+                               const float* const* d_s0, int32_t capacity, void* stream, nmt_rescorer** out) {
+  if (!out) return forest_fail(NMT_EINVAL, "NULL output");
+  *out = nullptr;
+  if (K < 1 || K > 32) return forest_fail(NMT_ERANGE, "K must be in [1, 32]");
+  if (!models || !srcs || !d_s0) return forest_fail(NMT_EINVAL, "NULL argument");
+  int32_t S = 0;
+  for (int k = 0; k < K; ++k) {
+    if (!models[k] || !srcs[k] || !d_s0[k]) return forest_fail(NMT_EINVAL, "a model, source or s0 is NULL");
+    if (((uintptr_t)d_s0[k] & 15)) return forest_fail(NMT_EINVAL, "s0 arrays must be 16-byte aligned");
+    int32_t Sk = 0;
+    nmt_source_info(srcs[k], &Sk, nullptr, nullptr, nullptr);
+    if (k == 0) S = Sk;
+    if (Sk != S) return forest_fail(NMT_EINVAL, "sources hold different numbers of sentences");
+    if (nmt_internal_vocab(models[k]) != nmt_internal_vocab(models[0]) ||
+        nmt_internal_device(models[k]) != nmt_internal_device(models[0]))
+      return forest_fail(NMT_EINVAL, "models differ in target vocabulary or device");
+  }
+  if (capacity < S) return forest_fail(NMT_ERANGE, "capacity must hold at least the S empty hypotheses");
+  hipStream_t st = (hipStream_t)stream;
+  nmt_rescorer* r = new nmt_rescorer();
+  r->K = K;
+  r->S = S;
+  r->capacity = capacity;
+  r->n_hyp = S;
+  r->models.assign(models, models + K);
+  r->srcs.assign(srcs, srcs + K);
+  hipError_t e = hipSuccess;
+  for (int k = 0; k < K && e == hipSuccess; ++k) {
+    const int32_t H = nmt_internal_hidden(models[k]);
+    r->H.push_back(H);
+    float* p = nullptr;
+    e = hipMalloc((void**)&p, (size_t)capacity * H * 4);
+    if (e == hipSuccess) {
+      r->pool.push_back(p);
+      // hypotheses 0..S-1: the empty hypothesis of each sentence, state s0
+      e = hipMemcpyAsync(p, d_s0[k], (size_t)S * H * 4, hipMemcpyDeviceToDevice, st);
+    }
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    nmt_rescorer_destroy(r);
+    return forest_fail(e == hipErrorOutOfMemory ? NMT_ENOMEM : NMT_EDEVICE, hipGetErrorString(e));
+  }
+  r->last_word.assign(S, -1);  // sentence start
+  r->sent.resize(S);
+  for (int32_t s = 0; s < S; ++s) r->sent[s] = s;
+  *out = r;
+  return NMT_OK;
+}
+
+void nmt_rescorer_destroy(nmt_rescorer* r) {
+  if (!r) return;
+  (void)hipDeviceSynchronize();
+  for (float* p : r->pool) (void)hipFree(p);
+  r->ws.release();
+  r->nodes.release();
+  r->pair_logp.release();
+  r->gather.release();
+  delete r;
+}
+
+nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent, const int32_t* h_off,
+                             const int32_t* h_words, float* h_logp, int32_t* h_ids, void* stream) {
+  if (!r) return forest_fail(NMT_EINVAL, "NULL rescorer");
+  if (n < 0) return forest_fail(NMT_EINVAL, "negative stack size");
+  if (n == 0) return NMT_OK;
+  if (!h_parent || !h_off || !h_logp) return forest_fail(NMT_EINVAL, "a required host array is NULL");
+  if (h_off[0] != 0) return forest_fail(NMT_EINVAL, "phrase offsets must start at 0");
+  if (n > r->capacity - r->n_hyp) return forest_fail(NMT_ERANGE, "the state pool is full");
+  const int32_t V = nmt_internal_vocab(r->models[0]);
+  for (int32_t j = 0; j < n; ++j) {
+    if (h_parent[j] < 0 || h_parent[j] >= r->n_hyp) return forest_fail(NMT_ERANGE, "parent is not an existing hypothesis");
+    if (h_off[j + 1] < h_off[j]) return forest_fail(NMT_EINVAL, "phrase offsets must not decrease");
+  }
+  if (h_off[n] > 0 && !h_words) return forest_fail(NMT_EINVAL, "phrase words are NULL");
+  for (int32_t i = 0; i < h_off[n]; ++i)
+    if (h_words[i] < 0 || h_words[i] >= V) return forest_fail(NMT_ERANGE, "phrase word out of the vocabulary");
+  hipStream_t st = (hipStream_t)stream;
+
+  // Predecessor extraction: identical (parent, phrase) pairs are one entry of L.
+  std::unordered_map<std::string, int32_t> seen;
+  std::vector<int32_t> pair_of(n), pair_hyp, pair_off{0}, pair_words;
+  for (int32_t j = 0; j < n; ++j) {
+    const int32_t len = h_off[j + 1] - h_off[j];
+    std::string key((const char*)&h_parent[j], 4);
+    key.append((const char*)(h_words + h_off[j]), (size_t)len * 4);
+    auto it = seen.find(key);
+    if (it != seen.end()) {
+      pair_of[j] = it->second;
+      continue;
+    }
+    const int32_t p = (int32_t)pair_hyp.size();
+    seen.emplace(std::move(key), p);
+    pair_of[j] = p;
+    pair_hyp.push_back(h_parent[j]);
+    pair_words.insert(pair_words.end(), h_words + h_off[j], h_words + h_off[j + 1]);
+    pair_off.push_back((int32_t)pair_words.size());
+  }
+  const int32_t np = (int32_t)pair_hyp.size();
+  // ScoreBatch over all predecessors: hypothesis ids index the forest's roots and the pools.
+  nmt_forest* f = nullptr;
+  nmt_status rc = nmt_forest_build(r->n_hyp, r->last_word.data(), r->sent.data(), np, pair_hyp.data(),
+                                   pair_off.data(), pair_words.data(), &f);
+  if (rc != NMT_OK) return rc;
+  const int32_t depth = f->depth, n_rows = f->n_rows;
+  int32_t maxH = 0;
+  size_t ws_need = 0;
+  for (int k = 0; k < r->K; ++k) {
+    maxH = r->H[k] > maxH ? r->H[k] : maxH;
+    const size_t b = nmt_forest_workspace_bytes(r->models[k], f);
+    ws_need = b > ws_need ? b : ws_need;
+  }
+  hipError_t e = hipStreamSynchronize(st);  // buffers may be reallocated below
+  if (e == hipSuccess) e = r->ws.ensure(ws_need);
+  if (e == hipSuccess) e = r->nodes.ensure((size_t)n_rows * maxH * 4);
+  if (e == hipSuccess) e = r->pair_logp.ensure((size_t)r->K * np * 4);
+  if (e == hipSuccess) e = r->gather.ensure((size_t)2 * n * 4);
+  if (e != hipSuccess) {
+    nmt_forest_destroy(f);
+    return forest_fail(e == hipErrorOutOfMemory ? NMT_ENOMEM : NMT_EDEVICE, hipGetErrorString(e));
+  }
+  // Where each new hypothesis' state comes from: the forest row that requested
+  // its phrase's last word, or its parent's state for an empty phrase.
+  r->h_gather.resize((size_t)2 * n);
+  for (int32_t j = 0; j < n; ++j) {
+    const int32_t p = pair_of[j], len = pair_off[p + 1] - pair_off[p];
+    r->h_gather[j] = len == 0 ? -(pair_hyp[p] + 1) : f->req_row[f->pair_path[(size_t)p * depth + len - 1]];
+    r->h_gather[n + j] = r->n_hyp + j;
+  }
+  int32_t* d_gather = (int32_t*)r->gather.p;
+  float* d_pair_logp = (float*)r->pair_logp.p;
+  e = hipMemcpyAsync(d_gather, r->h_gather.data(), (size_t)2 * n * 4, hipMemcpyHostToDevice, st);
+  for (int k = 0; k < r->K && e == hipSuccess && rc == NMT_OK; ++k) {
+    rc = nmt_score_forest(r->models[k], r->srcs[k], f, r->pool[k], d_pair_logp + (size_t)k * np, nullptr,
+                          (float*)r->nodes.p, r->ws.p, r->ws.cap, stream);
+    if (rc != NMT_OK) break;
+    hipLaunchKernelGGL(k_gather_states, dim3(n), dim3(256), 0, st, n, r->H[k], d_gather, d_gather + n,
+                       (const float*)r->nodes.p, r->pool[k]);
+    e = hipGetLastError();
+  }
+  r->h_pair_logp.resize((size_t)r->K * np);
+  if (e == hipSuccess && rc == NMT_OK)
+    e = hipMemcpyAsync(r->h_pair_logp.data(), d_pair_logp, (size_t)r->K * np * 4, hipMemcpyDeviceToHost, st);
+  const hipError_t es = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = es;
+  r->last_pairs = np;
+  r->last_rows = n_rows;
+  r->last_depth = depth;
+  r->last_edges = f->n_req;
+  nmt_forest_destroy(f);
+  if (rc != NMT_OK) return rc;
+  if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
+  // Look up p for each hypothesis' predecessor; number the new hypotheses.
+  for (int k = 0; k < r->K; ++k)
+    for (int32_t j = 0; j < n; ++j) h_logp[(size_t)k * n + j] = r->h_pair_logp[(size_t)k * np + pair_of[j]];
+  for (int32_t j = 0; j < n; ++j) {
+    const int32_t len = h_off[j + 1] - h_off[j];
+    r->last_word.push_back(len > 0 ? h_words[h_off[j + 1] - 1] : r->last_word[h_parent[j]]);
+    r->sent.push_back(r->sent[h_parent[j]]);
+    if (h_ids) h_ids[j] = r->n_hyp + j;
+  }
+  r->n_hyp += n;
+  return NMT_OK;
+}
+
+nmt_status nmt_rescorer_info(const nmt_rescorer* r, int32_t k, const float** d_states, int32_t* n_hyp,
+                             int32_t* last_pairs, int32_t* last_rows, int32_t* last_edges, int32_t* last_depth) {
+  if (!r) return forest_fail(NMT_EINVAL, "NULL rescorer");
+  if (k < 0 || k >= r->K) return forest_fail(NMT_ERANGE, "model index out of range");
+  if (d_states) *d_states = r->pool[k];
+  if (n_hyp) *n_hyp = r->n_hyp;
+  if (last_pairs) *last_pairs = r->last_pairs;
+  if (last_rows) *last_rows = r->last_rows;
+  if (last_edges) *last_edges = r->last_edges;
+  if (last_depth) *last_depth = r->last_depth;
   return NMT_OK;
 }
 

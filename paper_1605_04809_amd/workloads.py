@@ -225,3 +225,65 @@ def make_forest(cfg: Config, n_hyp: int, seed: int, max_phrases: int = 6, max_le
             phrases.append([int(cand[i, pick[i]]) for i in range(n)])
             pair_hyp.append(h)
     return ForestWorkload(hyp_word, hyp_sent, hyp_state, np.asarray(pair_hyp, np.int32), phrases)
+
+
+@dataclass
+class StackWorkload:
+    """Synthetic stacks of a phrase-based search over one source sentence.
+
+    Hypotheses are numbered in creation order: 0..n_roots-1 are the empty
+    hypotheses of the n_roots source sentences; stack c (c = 1..src_len
+    covered words) numbers its hypotheses next.  stacks[c-1] = (parents
+    [n_c] int32, phrases: n_c lists of target word ids)."""
+    n_roots: int
+    sent: int
+    stacks: list
+
+
+def make_stacks(cfg: Config, src_len: int, stack_size: int, seed: int, sent: int = 0, max_src_phrase: int = 3,
+                max_len: int = 4, options: int = 6, branch: int = 3, dup_rate: float = 0.05) -> StackWorkload:
+    """Stacks shaped like a phrase-based decoder's: every source span of up
+    to max_src_phrase words has `options` target phrases of 1..max_len words,
+    drawn position by position from `branch` candidate words (so options
+    share prefixes as phrase-table entries do); a hypothesis in stack c
+    extends a hypothesis of stack c-m by an option of a length-m span.  Stack
+    sizes grow with the number of expansions until the stack limit; a
+    fraction dup_rate of each stack repeats an earlier (parent, phrase) pair
+    of the same stack, as different coverages with the same target do."""
+    rng = np.random.default_rng(seed)
+    table = {}
+    for i in range(src_len):
+        for m in range(1, max_src_phrase + 1):
+            if i + m > src_len:
+                break
+            cand = rng.integers(0, cfg.V, size=(max_len, branch), dtype=np.int64)
+            opts = []
+            for _ in range(options):
+                n = int(rng.integers(1, max_len + 1))
+                pick = rng.integers(0, branch, size=n)
+                opts.append([int(cand[t, pick[t]]) for t in range(n)])
+            table[(i, m)] = opts
+    ids = [[sent]]            # hypothesis ids per stack; stack 0 is the empty hypothesis
+    next_id = cfg.S
+    stacks = []
+    for c in range(1, src_len + 1):
+        ms = [m for m in range(1, min(max_src_phrase, c) + 1)]
+        w = np.array([len(ids[c - m]) for m in ms], np.float64)
+        n_c = int(min(stack_size, 4 * options * w.sum()))
+        parents, phrases = [], []
+        for j in range(n_c):
+            if j > 0 and rng.random() < dup_rate:
+                k = int(rng.integers(0, j))
+                parents.append(parents[k])
+                phrases.append(list(phrases[k]))
+                continue
+            m = ms[int(rng.choice(len(ms), p=w / w.sum()))]
+            par = ids[c - m][int(rng.integers(0, len(ids[c - m])))]
+            start = int(rng.integers(0, src_len - m + 1))
+            opt = table[(start, m)][int(rng.integers(0, options))]
+            parents.append(par)
+            phrases.append(list(opt))
+        stacks.append((np.asarray(parents, np.int32), phrases))
+        ids.append(list(range(next_id, next_id + n_c)))
+        next_id += n_c
+    return StackWorkload(cfg.S, sent, stacks)
