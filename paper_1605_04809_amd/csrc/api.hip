@@ -266,7 +266,7 @@ int plain_ksplit(int M, int N, int K_total, int kc) {
 
 // Workspace layout of one step (offsets in bytes, 256-aligned).
 struct WsLayout {
-  size_t s1, q, c, t, part, kpart, total;
+  size_t s1, q, c, t, part, kpart, perm, tiles, ntiles, total;
   int nS;           // vocabulary slices
   int ks_q, ks_ro;  // K splits of the query and readout GEMMs
 };
@@ -295,6 +295,13 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
   L.kpart = off;
   off += al(kp * 4);
+  // attention's grouping of rows by sentence (at most one tile per row)
+  L.perm = off;
+  off += al((size_t)B * 4);
+  L.tiles = off;
+  off += al((size_t)B * 16);
+  L.ntiles = off;
+  off += al(4);
   L.total = off;
   return L;
 }
@@ -595,9 +602,11 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   }
   mark(NMT_PHASE_QUERY + 1);
   // masked attention and context
-  if (e == hipSuccess)
+  if (e == hipSuccess) {
+    const AttnGroups grp{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
     e = launch_attention(B, Aw, C, src->Tpad, q, src->pctx, src->ctx, src->len, d_sent_id, src->S, m->att_v, c,
-                         d_alpha, st);
+                         d_alpha, grp, st);
+  }
   mark(NMT_PHASE_ATTENTION + 1);
   // second GRU: s_new = GRU(c, s1)
   if (e == hipSuccess) {

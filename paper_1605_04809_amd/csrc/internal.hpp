@@ -105,9 +105,25 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
                               const float* bias, int V, const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
                               hipStream_t st);
+// Attention groups rows by sentence through workspace arrays: perm [B]
+// int32, tiles [B] int4, n_tiles [1] int32 (perm NULL: one block per row).
+constexpr int kGroupMaxS = 8192;  // sentences the grouping kernel can count in LDS
+#ifndef NMT_ATTN_GROUP
+#define NMT_ATTN_GROUP 4
+#endif
+constexpr int kAttnGroup = NMT_ATTN_GROUP;
+#ifndef NMT_ATTN_WAVES
+#define NMT_ATTN_WAVES 8
+#endif
+constexpr int kAttnWaves = NMT_ATTN_WAVES;
+struct AttnGroups {
+  int32_t* perm;
+  int4* tiles;
+  int32_t* n_tiles;
+};
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx,
                             const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
-                            const float* v, float* c, float* alpha, hipStream_t st);
+                            const float* v, float* c, float* alpha, const AttnGroups& grp, hipStream_t st);
 hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src,
                                 int* err, hipStream_t st);
 hipError_t launch_masked_copy(int S, int Tpad, int C, const float* src, const int32_t* len, float* dst,

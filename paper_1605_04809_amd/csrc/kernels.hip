@@ -14,7 +14,12 @@
 //                  fused with an online log-sum-exp; logits never reach HBM.
 //   k_lse_combine  merges the per-slice partials, scores the requested word
 //                  and checks the row's ids.
-//   k_attention    masked MLP attention and context for one row per block.
+//   k_group_rows, k_attention_grouped
+//                  masked MLP attention and context, rows grouped by
+//                  sentence so a block reads each key and annotation once
+//                  for several rows (k_attention: one row per block).
+#include <algorithm>
+
 #include "internal.hpp"
 
 namespace nmt {
@@ -591,10 +596,18 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
 
 // ------------------------------------------------------------ attention
 
-// One block (4 waves) per row.  Wave w scores source positions w, w+4, ...
-// (each lane covers float4 pieces of the attention width), the block
-// normalises the scores over the row's sentence length, then every thread
-// accumulates float4 pieces of the context over the unmasked positions.
+// tanh x = 1 - 2 / (e^{2x} + 1), with the hardware base-2 exponential and
+// reciprocal: about 1e-7 absolute error, saturating to +-1 for large |x|.
+__device__ __forceinline__ float tanh_fast(float x) {
+  const float ex = __builtin_amdgcn_exp2f(x * (2.f * kLog2e));
+  return 1.f - 2.f * __builtin_amdgcn_rcpf(ex + 1.f);
+}
+
+// Fallback for more sentences than the grouping kernel counts: one block
+// (4 waves) per row.  Wave w scores source positions w, w+4, ... (each lane
+// covers float4 pieces of the attention width), the block normalises the
+// scores over the row's sentence length, then every thread accumulates
+// float4 pieces of the context over the unmasked positions.
 template <int NQ>
 __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, const float* __restrict__ q,
                                                    const float* __restrict__ pctx, const float* __restrict__ ctx,
@@ -631,8 +644,8 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
       const int a4 = lane + 64 * k;
       if (a4 < A4) {
         const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
-        acc += vv[k][0] * tanhf(p[0] + qv[k][0]) + vv[k][1] * tanhf(p[1] + qv[k][1]) +
-               vv[k][2] * tanhf(p[2] + qv[k][2]) + vv[k][3] * tanhf(p[3] + qv[k][3]);
+        acc += vv[k][0] * tanh_fast(p[0] + qv[k][0]) + vv[k][1] * tanh_fast(p[1] + qv[k][1]) +
+               vv[k][2] * tanh_fast(p[2] + qv[k][2]) + vv[k][3] * tanh_fast(p[3] + qv[k][3]);
       }
     }
     acc = wave_sum(acc);
@@ -672,23 +685,227 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
   }
 }
 
+// Rows grouped by sentence, so that a block scores up to G rows of one
+// sentence and reads that sentence's keys and annotations once for all of
+// them.  k_group_rows (one block) counts the rows of each sentence in LDS
+// (rows with an invalid sentence id go to an extra bucket, scored as zeros),
+// lists the rows sentence by sentence in perm, and cuts each sentence's rows
+// into tiles (sentence or -1, first index into perm, row count).  The order
+// of rows inside a sentence does not matter: each row's arithmetic is the
+// same in any tile.
+__global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const int32_t* __restrict__ sent_id,
+                                                     int32_t* __restrict__ perm, int4* __restrict__ tiles,
+                                                     int32_t* __restrict__ n_tiles) {
+  __shared__ int cnt[kGroupMaxS + 1];
+  __shared__ int part[2][1024];
+  const int tid = threadIdx.x, NB = S + 1;
+  for (int i = tid; i < NB; i += 1024) cnt[i] = 0;
+  __syncthreads();
+  for (int b = tid; b < B; b += 1024) {
+    const int s = sent_id[b];
+    atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1);
+  }
+  __syncthreads();
+  // exclusive scans of the row and tile counts; thread tid owns buckets [lo, hi)
+  const int per = (NB + 1023) / 1024, lo = tid * per < NB ? tid * per : NB, hi = lo + per < NB ? lo + per : NB;
+  int rs = 0, ts = 0;
+  for (int i = lo; i < hi; ++i) {
+    rs += cnt[i];
+    ts += (cnt[i] + G - 1) / G;
+  }
+  part[0][tid] = rs;
+  part[1][tid] = ts;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int a0 = tid >= o ? part[0][tid - o] : 0, a1 = tid >= o ? part[1][tid - o] : 0;
+    __syncthreads();
+    part[0][tid] += a0;
+    part[1][tid] += a1;
+    __syncthreads();
+  }
+  int roff = part[0][tid] - rs, toff = part[1][tid] - ts;
+  if (tid == 1023) *n_tiles = part[1][1023];
+  for (int i = lo; i < hi; ++i) {
+    const int n = cnt[i];
+    for (int k = 0; k * G < n; ++k) tiles[toff + k] = make_int4(i < S ? i : -1, roff + k * G, min(G, n - k * G), 0);
+    toff += (n + G - 1) / G;
+    cnt[i] = roff;  // becomes the bucket's write cursor
+    roff += n;
+  }
+  __syncthreads();
+  for (int b = tid; b < B; b += 1024) {
+    const int s = sent_id[b];
+    perm[atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1)] = b;
+  }
+}
+
+// Sums G values (G a power of two, 2 <= G <= 64) over the 64 lanes of a
+// wave: each butterfly step halves the values a lane keeps, so the G sums
+// cost about log2(64) + G shuffles instead of G * log2(64).  On return the
+// sum of value g sits in every lane whose bits 5, 4, ... (the top log2(G)
+// lane bits, most significant first) spell g; the caller reads it from lane
+// g * (64 / G).
+template <int G>
+__device__ __forceinline__ float wave_sums(float (&v)[G]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int n = G, o = 32; n > 1; n >>= 1, o >>= 1) {
+    const bool hi = (lane & o) != 0;
+#pragma unroll
+    for (int j = 0; j < n / 2; ++j) {
+      const float keep = hi ? v[j + n / 2] : v[j], give = hi ? v[j] : v[j + n / 2];
+      v[j] = keep + __shfl_xor(give, o, 64);
+    }
+  }
+  float r = v[0];
+#pragma unroll
+  for (int o = 32 / G; o >= 1; o >>= 1) r += __shfl_xor(r, o, 64);
+  return r;
+}
+
+// One block (NW waves) per tile of up to G rows of one sentence.  The rows'
+// queries sit in LDS; wave w takes source positions w, w+NW, ..., loads the
+// position's key once and scores it against all G rows at once (rows past
+// the tile's count score zero queries and are dropped), each lane covering
+// float4 pieces of the attention width; then one wave per row normalises the
+// scores; finally every thread accumulates a float4 piece of the context of
+// all rows, reading each annotation once.
+template <int G, int NQ>
+__global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
+    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ pctx, const float* __restrict__ ctx,
+    const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
+    const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
+    float* __restrict__ alpha) {
+  constexpr int NW = kAttnWaves, NT = NW * 64;
+  extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
+  __shared__ int rows[G];
+  if ((int)blockIdx.x >= *n_tiles) return;
+  const int4 tl = tiles[blockIdx.x];
+  const int s = tl.x, n = tl.z;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int A4 = A / 4, C4 = C / 4;
+  f32x4* qs = dyn;
+  float* e = (float*)(dyn + G * A4);
+  if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? perm[tl.y + threadIdx.x] : 0;
+  __syncthreads();
+  if (s < 0) {  // rows with an invalid sentence: flagged and NaN-ed by the combine kernel
+    for (int g = 0; g < n; ++g) {
+      for (int k4 = threadIdx.x; k4 < C4; k4 += NT) *(f32x4*)(c + (int64_t)rows[g] * C + 4 * k4) = zero4();
+      if (alpha)
+        for (int i = threadIdx.x; i < Tpad; i += NT) alpha[(int64_t)rows[g] * Tpad + i] = 0.f;
+    }
+    return;
+  }
+  for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
+    const int g = idx / A4, a4 = idx - g * A4;
+    qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+  }
+  f32x4 vv[NQ];
+#pragma unroll
+  for (int k = 0; k < NQ; ++k) {
+    const int a4 = lane + 64 * k;
+    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) : zero4();
+  }
+  __syncthreads();
+  const int L = len[s];
+  const float* P = pctx + (int64_t)s * Tpad * A;
+  for (int i = wave; i < L; i += NW) {
+    float acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NQ; ++k) {
+      const int a4 = lane + 64 * k;
+      if (a4 < A4) {
+        const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const f32x4 qq = qs[g * A4 + a4];
+          acc[g] += vv[k][0] * tanh_fast(p[0] + qq[0]) + vv[k][1] * tanh_fast(p[1] + qq[1]) +
+                    vv[k][2] * tanh_fast(p[2] + qq[2]) + vv[k][3] * tanh_fast(p[3] + qq[3]);
+        }
+      }
+    }
+    const float r = wave_sums<G>(acc);
+    if ((lane & (64 / G - 1)) == 0) e[(lane / (64 / G)) * Tpad + i] = r;
+  }
+  __syncthreads();
+  for (int g = wave; g < n; g += NW) {
+    float* eg = e + g * Tpad;
+    float mx = -INFINITY;
+    for (int i = lane; i < L; i += 64) mx = fmaxf(mx, eg[i]);
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int i = lane; i < L; i += 64) sum += expf(eg[i] - mx);
+    const float inv = 1.f / wave_sum(sum);
+    for (int i = lane; i < L; i += 64) eg[i] = expf(eg[i] - mx) * inv;
+    if (alpha)
+      for (int i = lane; i < Tpad; i += 64) alpha[(int64_t)rows[g] * Tpad + i] = i < L ? eg[i] : 0.f;
+  }
+  __syncthreads();
+  const f32x4* X = (const f32x4*)(ctx + (int64_t)s * Tpad * C);
+  for (int k4 = threadIdx.x; k4 < C4; k4 += NT) {
+    f32x4 acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = zero4();
+    for (int i = 0; i < L; ++i) {
+      const f32x4 x = X[(int64_t)i * C4 + k4];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float a = e[g * Tpad + i];
+        acc[g][0] += a * x[0];
+        acc[g][1] += a * x[1];
+        acc[g][2] += a * x[2];
+        acc[g][3] += a * x[3];
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (g < n) *(f32x4*)(c + (int64_t)rows[g] * C + 4 * k4) = acc[g];
+  }
+}
+
+template <int G, int NQ>
+static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+                              const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
+                              float* alpha, hipStream_t st) {
+  const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);
+  const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
+  hipLaunchKernelGGL((k_attention_grouped<G, NQ>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C, Tpad, q, pctx, ctx, len,
+                     grp.perm, grp.tiles, grp.n_tiles, v, c, alpha);
+}
+
+template <int NQ>
+static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+                         const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
+                         float* c, float* alpha, hipStream_t st) {
+  if (S > kGroupMaxS || !grp.perm) {
+    hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v,
+                       c, alpha);
+    return;
+  }
+  // rows per tile: kAttnGroup when their queries and scores fit 64 KB of LDS, else 4
+  const int G = ((size_t)kAttnGroup * (A + Tpad) * 4 <= 65536) ? kAttnGroup : 4;
+  hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, grp.perm, grp.tiles, grp.n_tiles);
+  if (G == kAttnGroup)
+    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, pctx, ctx, len, grp, S, v, c, alpha, st);
+  else
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, pctx, ctx, len, grp, S, v, c, alpha, st);
+}
+
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
                             const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
-                            hipStream_t st) {
+                            const AttnGroups& grp, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    hipLaunchKernelGGL(k_attention<1>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
-                       alpha);
+    attention_nq<1>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 2)
-    hipLaunchKernelGGL(k_attention<2>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
-                       alpha);
+    attention_nq<2>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 4)
-    hipLaunchKernelGGL(k_attention<4>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
-                       alpha);
+    attention_nq<4>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 8)
-    hipLaunchKernelGGL(k_attention<8>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v, c,
-                       alpha);
+    attention_nq<8>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
