@@ -296,7 +296,7 @@ struct VocabTune {
 // [Kpad/KV][VTM]; the packed output weights stream straight from HBM/L2 into
 // registers, VPF k groups ahead, so the main loop has no barrier.  Wave w
 // takes the slice's 32-column blocks in groups of VFN (groups w, w+VNW, ...),
-// each for all VTM rows; each lane keeps a running (max, sum of exp) for each
+// each for all VTM rows; each lane keeps a running base-2 log-sum-exp for each
 // of its row slots, and the 32 lanes and the waves are merged once at the
 // end.  One (max, sum) pair per row and slice goes to HBM as float2
 // [slice][row]; the logits never do.
@@ -344,6 +344,8 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
   const int nmine = ngrp > wave ? (ngrp - wave + VNW - 1) / VNW : 0;
 
+  // Running log-sum-exp of each row slot in base 2: run_m is the largest
+  // t = z*log2(e) seen so far, run_s the sum of 2^(t - run_m).
   float run_m[FM][16], run_s[FM][16];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -415,22 +417,25 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
         load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
       }
     }
-    // fold the group's columns into the running (max, sum) of each row slot
+    // fold the group's columns into the running log-sum-exp of each row slot
 #pragma unroll
     for (int f = 0; f < VFN; ++f) {
       const int cb = cb_begin + (wave + VNW * gi) * VFN + f;
       const int n = cb * 32 + l32;
       if (cb < cb_end && n < V) {
-        const float bn = bias[n];
+        const float b2 = bias[n] * kLog2e;
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const float z = acc[i][f][r] + bn;
-            const float mn = fmaxf(run_m[i][r], z);
-            run_s[i][r] = run_s[i][r] * __builtin_amdgcn_exp2f((run_m[i][r] - mn) * kLog2e) +
-                          __builtin_amdgcn_exp2f((z - mn) * kLog2e);
-            run_m[i][r] = mn;
+            // One exp per logit: with d = t - m, 2^-|d| is the new term when
+            // t <= m, and the factor that rescales the old sum to t when t > m.
+            const float t = fmaf(acc[i][f][r], kLog2e, b2);
+            const float d = t - run_m[i][r];
+            const float e = __builtin_amdgcn_exp2f(-fabsf(d));
+            const bool up = d > 0.f;
+            run_s[i][r] = up ? fmaf(run_s[i][r], e, 1.f) : run_s[i][r] + e;
+            run_m[i][r] = up ? t : run_m[i][r];
           }
       }
     }
@@ -442,7 +447,7 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float mx = half_max(run_m[i][r]);
-      const float s = mx == -INFINITY ? 0.f : run_s[i][r] * __builtin_amdgcn_exp2f((run_m[i][r] - mx) * kLog2e);
+      const float s = mx == -INFINITY ? 0.f : run_s[i][r] * __builtin_amdgcn_exp2f(run_m[i][r] - mx);
       const float st = half_sum(s);
       if (l32 == 0) {
         const int rl = 32 * i + acc_row(r, h);
@@ -462,10 +467,11 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 #pragma unroll
       for (int w = 0; w < VNW; ++w) {
         const float mw = red[w][rl][0];
-        if (mw != -INFINITY) s += red[w][rl][1] * __builtin_amdgcn_exp2f((mw - mx) * kLog2e);
+        if (mw != -INFINITY) s += red[w][rl][1] * __builtin_amdgcn_exp2f(mw - mx);
       }
     }
-    if (row < M) part[(int64_t)slice * M + row] = float2{mx, s};
+    // partials leave in natural-log units: (max logit, sum of e^(z - max))
+    if (row < M) part[(int64_t)slice * M + row] = float2{mx * kLn2, s};
   }
 }
 
