@@ -356,23 +356,31 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     }
 
   // Weight fragments are read in (group, k group) order through a scalar
-  // cursor; ring slot p always holds step q with q % VPF == p.  Loads past
-  // this wave's last step, or of a group's missing last blocks, re-read
-  // fragment 0 of the matrix (always in bounds).
-  const int total = nmine * NKG;
+  // cursor; ring slot p always holds step q with q % VPF == p.  The cursor
+  // keeps a 64-bit offset that advances by one k group per step and is reset
+  // when the group changes; loads past this wave's last group, or of a
+  // group's missing last blocks, re-read fragment 0 of the matrix (always in
+  // bounds).  Keeping this to a few scalar instructions per step matters in
+  // bf16, whose MFMAs are short.
   const f32x4* wlane = Wp + (int64_t)h * Npad + l32;
-  int pg = wave, pkg = 0, issued = 0;
+  const int64_t kstride = 2 * Npad;
+  int pg = wave, pkg = 0;
+  int64_t off = (int64_t)(cb_begin + pg * VFN) * 32;
+  bool okf[VFN];
+  auto set_group = [&]() {
+#pragma unroll
+    for (int f = 0; f < VFN; ++f) okf[f] = pg < ngrp && cb_begin + pg * VFN + f < cb_end;
+  };
+  set_group();
   auto load_next = [&](f32x4 (&dst)[VFN]) {
 #pragma unroll
-    for (int f = 0; f < VFN; ++f) {
-      const int cb = cb_begin + pg * VFN + f;
-      const int64_t off = issued < total && cb < cb_end ? (int64_t)(2 * pkg) * Npad + (int64_t)cb * 32 : 0;
-      dst[f] = wlane[off];
-    }
-    ++issued;
+    for (int f = 0; f < VFN; ++f) dst[f] = wlane[okf[f] ? off + 32 * f : 0];
+    off += kstride;
     if (++pkg == NKG) {
       pkg = 0;
       pg += VNW;
+      off = (int64_t)(cb_begin + pg * VFN) * 32;
+      set_group();
     }
   };
   f32x4 ring[VPF][VFN];
@@ -415,6 +423,14 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 #pragma unroll
           for (int i = 0; i < FM; ++i) P::mma(a[i], ring[p][f], acc[i][f]);
         load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
+        // Instruction order within the step: one MFMA, the next step's A
+        // fragment reads (so they have the remaining MFMAs to land), the rest
+        // of the MFMAs, then the refill.
+        constexpr int kMfmaPerStep = FM * VFN * (P::kBF16 ? 1 : 4);  // fp32: four MFMAs per fragment pair
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, FM, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
       }
     }
     // fold the group's columns into the running log-sum-exp of each row slot
