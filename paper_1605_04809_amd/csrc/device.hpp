@@ -28,6 +28,7 @@
 #include <stdint.h>
 
 #include <type_traits>
+#include <utility>
 
 namespace nmt {
 
@@ -68,6 +69,13 @@ struct PrecF32 {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
   }
+  // a*b with a zero accumulator (encoded as an inline constant, no clearing moves)
+  __device__ static __forceinline__ f32x16 mma0(const f32x4& a, const f32x4& b) {
+    f32x16 acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], f32x16{}, 0, 0, 0);
+#pragma unroll
+    for (int j = 1; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
+    return acc;
+  }
 };
 
 struct PrecBF16 {
@@ -77,6 +85,10 @@ struct PrecBF16 {
   __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
                                                   0, 0, 0);
+  }
+  __device__ static __forceinline__ f32x16 mma0(const f32x4& a, const f32x4& b) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   f32x16{}, 0, 0, 0);
   }
 };
 
@@ -288,6 +300,16 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
     gemm_segment<TM, TN, NT, P>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
     s0 = s1;
   }
+}
+
+// f(std::integral_constant<int, i>{}) for i = 0 .. N-1, unrolled at compile time.
+template <int N, class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
 }
 
 // Reductions within each 32-lane half of a wave (the lanes that share a

@@ -394,45 +394,49 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 
   for (int gi = 0; gi < nmine; ++gi) {
     f32x16 acc[FM][VFN];
+    // One k-group step; `zc` (compile time) starts the accumulators from an
+    // inline zero instead of clearing them with register moves.
+    auto kstep = [&](int kg0, auto pc, auto zc) {
+      constexpr int p = decltype(pc)::value;
+      const int kg = kg0 + p;
+      const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
+      const f32x4* an = arow + kn * 2 * VTM;
+      f32x4 a[FM];
+      if constexpr (p % 2 == 0) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int f = 0; f < VFN; ++f) acc[i][f] = f32x16{};
-    for (int kg0 = 0; kg0 < NKG; kg0 += VPF) {
-#pragma unroll
-      for (int p = 0; p < VPF; ++p) {
-        const int kg = kg0 + p;
-        const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
-        const f32x4* an = arow + kn * 2 * VTM;
-        f32x4 a[FM];
-        if (p % 2 == 0) {
-#pragma unroll
-          for (int i = 0; i < FM; ++i) {
-            ao[i] = an[32 * i];
-            a[i] = ae[i];
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < FM; ++i) {
-            ae[i] = an[32 * i];
-            a[i] = ao[i];
-          }
+        for (int i = 0; i < FM; ++i) {
+          ao[i] = an[32 * i];
+          a[i] = ae[i];
         }
+      } else {
 #pragma unroll
-        for (int f = 0; f < VFN; ++f)
-#pragma unroll
-          for (int i = 0; i < FM; ++i) P::mma(a[i], ring[p][f], acc[i][f]);
-        load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
-        // Instruction order within the step: one MFMA, the next step's A
-        // fragment reads (so they have the remaining MFMAs to land), the rest
-        // of the MFMAs, then the refill.
-        constexpr int kMfmaPerStep = FM * VFN * (P::kBF16 ? 1 : 4);  // fp32: four MFMAs per fragment pair
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, FM, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
+        for (int i = 0; i < FM; ++i) {
+          ae[i] = an[32 * i];
+          a[i] = ao[i];
+        }
       }
-    }
+#pragma unroll
+      for (int f = 0; f < VFN; ++f)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          if constexpr (decltype(zc)::value)
+            acc[i][f] = P::mma0(a[i], ring[p][f]);
+          else
+            P::mma(a[i], ring[p][f], acc[i][f]);
+        }
+      load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
+      // Instruction order within the step: one MFMA, the next step's A
+      // fragment reads (so they have the remaining MFMAs to land), the rest
+      // of the MFMAs, then the refill.
+      constexpr int kMfmaPerStep = FM * VFN * (P::kBF16 ? 1 : 4);  // fp32: four MFMAs per fragment pair
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, FM, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
+    };
+    // the first VPF steps, whose first step starts from zero, then the rest
+    static_for<VPF>([&](auto pc) { kstep(0, pc, std::bool_constant<decltype(pc)::value == 0>{}); });
+    for (int kg0 = VPF; kg0 < NKG; kg0 += VPF) static_for<VPF>([&](auto pc) { kstep(kg0, pc, std::false_type{}); });
     // fold the group's columns into the running log-sum-exp of each row slot
 #pragma unroll
     for (int f = 0; f < VFN; ++f) {
