@@ -105,6 +105,22 @@ def test_high_signal_every_row(gpu, cfg):
     g2.close()
 
 
+@pytest.mark.parametrize("S", [8192, 8200], ids=["grouped_at_limit", "per_row_fallback"])
+def test_many_sentences_every_row(gpu, S):
+    """Attention groups rows by sentence with per-sentence counters in LDS for
+    up to 8192 sentences and falls back to one block per row beyond that; both
+    paths against the oracle, with rows spread over the whole range."""
+    _torch()
+    cfg = high_signal(CONFIGS["tiny"]).replace(B=300, S=S, len_lo=1, len_hi=3, Tpad=3)
+    wl = make_workload(cfg)
+    wl.sent_id[:4] = [0, S - 1, S - 1, 8191]
+    ctx = random_annotations(cfg, seed=21)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+
+
 def test_padding_contents_are_ignored(gpu):
     torch = _torch()
     cfg = high_signal(CONFIGS["tiny"]).replace(B=64, S=3, len_lo=2, len_hi=7, Tpad=10)
