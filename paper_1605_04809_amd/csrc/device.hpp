@@ -36,6 +36,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
+// f(std::integral_constant<int, i>{}) for i = 0 .. N-1, unrolled at compile time.
+template <int N, class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
+}
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -204,24 +214,37 @@ __device__ __forceinline__ f32x4 load_a_vec(const char* row, int bf16src, int K,
   }
 }
 
+// Rows of an A stage in LDS: TM plus one vector of padding, so that the
+// transposed stores of the staging (consecutive lanes writing consecutive
+// vectors of one row, a stage row apart) fall in different banks.
+template <int TM>
+constexpr int a_rows() {
+  return TM + 1;
+}
+
 // Global -> register -> LDS staging of one K chunk of the A and B tiles.
-// Each thread owns one tile row for A (NT % TM == 0) and strided vectors of B.
+// Vector v of the chunk's TM x KQ A vectors is row v / KQ, vector v % KQ, so
+// consecutive lanes read consecutive 16-byte pieces of one row (KQ lanes per
+// row: one contiguous 128-byte fp32 or 256-byte bf16-from-fp32 stretch).
+// B vectors are consecutive columns of one packed row.
 template <int TM, int TN, int NT, class P>
 struct Stager {
   static constexpr int NA = TM * KQ / NT;
   static constexpr int NB = TN * KQ / NT;
-  static_assert(NT % TM == 0, "one A row per thread");
   static_assert((TM * KQ) % NT == 0 && (TN * KQ) % NT == 0, "whole vectors per thread");
   f32x4 ra[NA];
   f32x4 rb[NB];
 
-  // arow: this thread's row of the current segment; kseg: k offset of the
-  // chunk within the segment; vq_glob: chunk start in packed-weight vector
-  // rows.  Weights first: their loads carry no condition.
-  __device__ __forceinline__ void load(const ARow& arow, int bf16src, int segK, int kseg,
+  // Tile row of this thread's i-th A vector (the rows it reads: see rows()).
+  __device__ static __forceinline__ int a_row(int i) { return ((int)threadIdx.x + i * NT) / KQ; }
+  __device__ static __forceinline__ int a_vec(int i) { return ((int)threadIdx.x + i * NT) % KQ; }
+
+  // arow[i]: segment row of this thread's i-th A vector; kseg: k offset of
+  // the chunk within the segment; vq_glob: chunk start in packed-weight
+  // vector rows.  Weights first: their loads carry no condition.
+  __device__ __forceinline__ void load(const ARow (&arow)[NA], int bf16src, int segK, int kseg,
                                        const f32x4* __restrict__ Wp, int64_t Npad, int64_t vq_glob, int n0) {
     const int tid = threadIdx.x;
-    const int kq0 = tid / TM;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + i * NT;
@@ -229,15 +252,13 @@ struct Stager {
       rb[i] = Wp[(vq_glob + kq) * Npad + n0 + n];
     }
 #pragma unroll
-    for (int i = 0; i < NA; ++i)
-      ra[i] = load_a_vec_clamped<P>(arow, bf16src, segK, kseg + P::KV * (kq0 + i * (NT / TM)));
+    for (int i = 0; i < NA; ++i) ra[i] = load_a_vec_clamped<P>(arow[i], bf16src, segK, kseg + P::KV * a_vec(i));
   }
 
   __device__ __forceinline__ void store(f32x4* As, f32x4* Bs) const {
     const int tid = threadIdx.x;
-    const int m = tid % TM, kq0 = tid / TM;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) As[(kq0 + i * (NT / TM)) * TM + m] = ra[i];
+    for (int i = 0; i < NA; ++i) As[a_vec(i) * a_rows<TM>() + a_row(i)] = ra[i];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + i * NT;
@@ -254,10 +275,19 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
   return S[(2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)];
 }
 
+// Global-load lookahead of the tile GEMMs: chunks whose loads are in
+// flight in registers while a chunk is computed from LDS.
+#ifndef NMT_GEMM_LA
+#define NMT_GEMM_LA 1
+#endif
+
 // Main loop over chunks [cb, ce) of one A segment (chunk indices local to
-// the segment; vq0 = packed weight vector row of the segment's chunk 0),
-// staging the next chunk while `compute(As, Bs)` runs on the current one.
-// Ends with a barrier, so a following call may reuse the LDS stages.
+// the segment; vq0 = packed weight vector row of the segment's chunk 0).
+// Chunk i's global loads are issued LA iterations before it is computed
+// (into register set i % LA), it is stored to LDS stage i % 2 at the end of
+// iteration i - 1, and `compute(As, Bs)` runs on it at iteration i.  The
+// loop is unrolled by LA so register sets are picked at compile time.  Ends
+// with a barrier, so a following call may reuse the LDS stages.
 template <int TM, int TN, int NT, class P, class Compute>
 __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
                                              int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
@@ -267,21 +297,35 @@ __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4*
   // pointers hides the LDS address space from the compiler, which then emits
   // flat loads that share the global-load counter, so every fragment wait
   // would also wait for the next chunk's prefetch.
-  constexpr int ASZ = TM * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
-  if (cb >= ce) return;
-  Stager<TM, TN, NT, P> st;
-  const ARow arow = seg_arow(sg, m0 + (int)threadIdx.x % TM, M);
-  st.load(arow, sg.bf16, sg.K, cb * P::KC, Wp, Npad, vq0 + (int64_t)cb * KQ, n0);
-  st.store(lds, lds + ASZ);
+  constexpr int ASZ = a_rows<TM>() * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
+  constexpr int LA = NMT_GEMM_LA;
+  using St = Stager<TM, TN, NT, P>;
+  const int n = ce - cb;
+  if (n <= 0) return;
+  St st[LA];
+  ARow arow[St::NA];
+#pragma unroll
+  for (int i = 0; i < St::NA; ++i) arow[i] = seg_arow(sg, m0 + St::a_row(i), M);
+  auto load = [&](Stager<TM, TN, NT, P>& s, int i) {
+    s.load(arow, sg.bf16, sg.K, (cb + i) * P::KC, Wp, Npad, vq0 + (int64_t)(cb + i) * KQ, n0);
+  };
+  static_for<LA>([&](auto j) {
+    if (j < n) load(st[j], j);
+  });
+  st[0].store(lds, lds + ASZ);
   __syncthreads();
-
-  for (int c = cb; c < ce; ++c) {
-    const bool more = c + 1 < ce;
-    const int cur = ((c - cb) & 1) * STG, nxt = STG - cur;
-    if (more) st.load(arow, sg.bf16, sg.K, (c + 1) * P::KC, Wp, Npad, vq0 + (int64_t)(c + 1) * KQ, n0);
-    compute(lds + cur, lds + cur + ASZ);
-    if (more) st.store(lds + nxt, lds + nxt + ASZ);
-    __syncthreads();
+  for (int i0 = 0; i0 < n; i0 += LA) {
+    static_for<LA>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;  // this iteration's register set
+      const int i = i0 + j;
+      if (i < n) {
+        const int cur = (i & 1) * STG, nxt = STG - cur;
+        if (i + LA < n) load(st[j], i + LA);
+        compute(lds + cur, lds + cur + ASZ);
+        if (i + 1 < n) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
+        __syncthreads();
+      }
+    });
   }
 }
 
@@ -300,16 +344,6 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
     gemm_segment<TM, TN, NT, P>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
     s0 = s1;
   }
-}
-
-// f(std::integral_constant<int, i>{}) for i = 0 .. N-1, unrolled at compile time.
-template <int N, class F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
 }
 
 // Reductions within each 32-lane half of a wave (the lanes that share a

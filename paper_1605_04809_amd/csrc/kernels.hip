@@ -31,7 +31,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
                                                                            int64_t Npad, PlainEpi ep) {
   constexpr int NT = (TM / WM) * (TN / WN) * 64;
   constexpr int FM = WM / 32, FN = WN / 32;
-  __shared__ f32x4 lds[2 * (TM + TN) * KQ];
+  __shared__ f32x4 lds[2 * (a_rows<TM>() + TN) * KQ];
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm0 = (wave % (TM / WM)) * WM, wn0 = (wave / (TM / WM)) * WN;
@@ -54,7 +54,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
         for (int kg = 0; kg < KQ / 2; ++kg) {
           f32x4 a[FM], b[FN];
 #pragma unroll
-          for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+          for (int i = 0; i < FM; ++i) a[i] = lds_frag<a_rows<TM>()>(As, kg, wm0 + 32 * i);
 #pragma unroll
           for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
 #pragma unroll
@@ -161,7 +161,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
-  __shared__ f32x4 lds[2 * (TM + TN) * KQ];
+  __shared__ f32x4 lds[2 * (a_rows<TM>() + TN) * KQ];
   const GruProblem& Pb = batch.p[blockIdx.z];
   const f32x4* Wp = (const f32x4*)Pb.Wp;
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
@@ -176,7 +176,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
     for (int kg = 0; kg < KQ / 2; ++kg) {
       f32x4 a[FM];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = lds_frag<TM>(As, kg, wm0 + 32 * i);
+      for (int i = 0; i < FM; ++i) a[i] = lds_frag<a_rows<TM>()>(As, kg, wm0 + 32 * i);
       const f32x4 br = lds_frag<TN>(Bs, kg, wu0);
       const f32x4 bz = lds_frag<TN>(Bs, kg, HB + wu0);
       const f32x4 bn = lds_frag<TN>(Bs, kg, 2 * HB + wu0);
