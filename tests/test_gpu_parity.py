@@ -121,6 +121,26 @@ def test_many_sentences_every_row(gpu, S):
     g.close()
 
 
+@pytest.mark.parametrize("V,wtype", [(1, "f32"), (2, "f32"), (33, "f32"), (1, "bf16"), (33, "bf16")])
+def test_minimal_dimensions(gpu, V, wtype):
+    """Every dimension far below its tile: E = H = A = 4, one source position,
+    and vocabularies of 1, 2 and 33 words.  A single word has log p = 0; the
+    kernel's base-2 running maximum converted back to natural units costs one
+    fp32 rounding of the logit, so |log p| stays within a few ulp of it."""
+    _torch()
+    cfg = Config("minimal", V=V, V_src=3, E=4, H=4, A=4, B=5, S=2, len_lo=1, len_hi=1, Tpad=1,
+                 sigma_w=0.5, sigma_emb=0.5, seed=17, wtype=wtype)
+    wl = make_workload(cfg)
+    g, o = gpu.GpuRun(wl), gpu.OracleRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    gr = g.step(*args)
+    tol_logp, tol = (1e-4, TOL_INTER_HS) if wtype == "f32" else (2e-2, 1e-2)
+    compare(gr, o.step(*args), tol_logp=tol_logp, tol=tol)
+    if V == 1:
+        assert np.all(np.abs(gr["logp"]) <= 1e-6), gr["logp"]
+    g.close()
+
+
 def test_padding_contents_are_ignored(gpu):
     torch = _torch()
     cfg = high_signal(CONFIGS["tiny"]).replace(B=64, S=3, len_lo=2, len_hi=7, Tpad=10)
