@@ -177,26 +177,35 @@ __device__ __forceinline__ ARow seg_arow(const ASeg& s, int row, int M) {
   return {base + r * s.ld * (s.bf16 ? 2 : 4), true};
 }
 
-// Branch-free form of load_a_vec over an ARow: columns past K are clamped
-// to column 0 for the load and zeroed after it.
-template <class P>
-__device__ __forceinline__ f32x4 load_a_vec_clamped(const ARow& r, int bf16src, int K, int k) {
+// The raw global data behind one A vector of an ARow, for the staging:
+// one 16-byte load (fp32, or a bf16 source whose rows are padded to whole
+// vectors) or, for bf16 from an fp32 source, two (x1 past K stays zero).
+// Absent rows and columns leave zeros.  Nothing here consumes the loaded
+// values, so the loads stay in flight until the values are stored to LDS
+// (a conversion at load time would make the compiler wait for them here).
+template <class P, bool SRC16>
+__device__ __forceinline__ void load_a_raw(const ARow& r, int K, int k, f32x4& x0, f32x4& x1) {
+  x0 = zero4();
+  x1 = zero4();
   const bool in = r.ok && k < K;
-  const int kc = k < K ? k : 0;
   if constexpr (P::kBF16) {
-    if (bf16src) {
-      const f32x4 v = *(const f32x4*)(r.p + 2 * (int64_t)kc);  // rows padded to whole vectors
-      return in ? v : zero4();
+    if constexpr (SRC16) {
+      if (in) x0 = *(const f32x4*)(r.p + 2 * (int64_t)k);
+    } else {
+      const float* f = (const float*)r.p;
+      if (in) x0 = *(const f32x4*)(f + k);
+      if (in && k + 4 < K) x1 = *(const f32x4*)(f + k + 4);
     }
-    const float* f = (const float*)r.p;
-    const bool in1 = in && k + 4 < K;
-    const f32x4 x0 = *(const f32x4*)(f + kc);
-    const f32x4 x1 = *(const f32x4*)(f + (in1 ? k + 4 : 0));
-    return pack_bf16(in ? x0 : zero4(), in1 ? x1 : zero4());
   } else {
-    const f32x4 v = *(const f32x4*)((const float*)r.p + kc);
-    return in ? v : zero4();
+    if (in) x0 = *(const f32x4*)((const float*)r.p + k);
   }
+}
+
+// The A vector from load_a_raw's data, in precision P.
+template <class P, bool SRC16>
+__device__ __forceinline__ f32x4 a_from_raw(const f32x4& x0, const f32x4& x1) {
+  if constexpr (P::kBF16 && !SRC16) return pack_bf16(x0, x1);
+  return x0;
 }
 
 // The 16-byte A vector at column k of a row, in precision P.
@@ -227,12 +236,14 @@ constexpr int a_rows() {
 // consecutive lanes read consecutive 16-byte pieces of one row (KQ lanes per
 // row: one contiguous 128-byte fp32 or 256-byte bf16-from-fp32 stretch).
 // B vectors are consecutive columns of one packed row.
-template <int TM, int TN, int NT, class P>
+// SRC16: the A segment is stored in bf16 (only with bf16 weights).
+template <int TM, int TN, int NT, class P, bool SRC16>
 struct Stager {
   static constexpr int NA = TM * KQ / NT;
   static constexpr int NB = TN * KQ / NT;
   static_assert((TM * KQ) % NT == 0 && (TN * KQ) % NT == 0, "whole vectors per thread");
-  f32x4 ra[NA];
+  static constexpr bool kTwo = P::kBF16 && !SRC16;  // bf16 from an fp32 source: two raw vectors
+  f32x4 ra[NA], rx[kTwo ? NA : 1];
   f32x4 rb[NB];
 
   // Tile row of this thread's i-th A vector (the rows it reads: see rows()).
@@ -242,8 +253,8 @@ struct Stager {
   // arow[i]: segment row of this thread's i-th A vector; kseg: k offset of
   // the chunk within the segment; vq_glob: chunk start in packed-weight
   // vector rows.  Weights first: their loads carry no condition.
-  __device__ __forceinline__ void load(const ARow (&arow)[NA], int bf16src, int segK, int kseg,
-                                       const f32x4* __restrict__ Wp, int64_t Npad, int64_t vq_glob, int n0) {
+  __device__ __forceinline__ void load(const ARow (&arow)[NA], int segK, int kseg, const f32x4* __restrict__ Wp,
+                                       int64_t Npad, int64_t vq_glob, int n0) {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
@@ -252,13 +263,18 @@ struct Stager {
       rb[i] = Wp[(vq_glob + kq) * Npad + n0 + n];
     }
 #pragma unroll
-    for (int i = 0; i < NA; ++i) ra[i] = load_a_vec_clamped<P>(arow[i], bf16src, segK, kseg + P::KV * a_vec(i));
+    for (int i = 0; i < NA; ++i) {
+      f32x4 x1;
+      load_a_raw<P, SRC16>(arow[i], segK, kseg + P::KV * a_vec(i), ra[i], x1);
+      if constexpr (kTwo) rx[i] = x1;
+    }
   }
 
   __device__ __forceinline__ void store(f32x4* As, f32x4* Bs) const {
     const int tid = threadIdx.x;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) As[a_vec(i) * a_rows<TM>() + a_row(i)] = ra[i];
+    for (int i = 0; i < NA; ++i)
+      As[a_vec(i) * a_rows<TM>() + a_row(i)] = a_from_raw<P, SRC16>(ra[i], rx[kTwo ? i : 0]);
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + i * NT;
@@ -278,7 +294,7 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 // Global-load lookahead of the tile GEMMs: chunks whose loads are in
 // flight in registers while a chunk is computed from LDS.
 #ifndef NMT_GEMM_LA
-#define NMT_GEMM_LA 1
+#define NMT_GEMM_LA 2
 #endif
 
 // Main loop over chunks [cb, ce) of one A segment (chunk indices local to
@@ -288,10 +304,10 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 // iteration i - 1, and `compute(As, Bs)` runs on it at iteration i.  The
 // loop is unrolled by LA so register sets are picked at compile time.  Ends
 // with a barrier, so a following call may reuse the LDS stages.
-template <int TM, int TN, int NT, class P, class Compute>
-__device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
-                                             int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
-                                             int ce) {
+template <int TM, int TN, int NT, class P, bool SRC16, class Compute>
+__device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
+                                               int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
+                                               int ce) {
   // Stage s holds A at lds + s*STG and B right after it.  Stage bases are
   // formed as offsets from `lds` itself: a runtime-indexed array of stage
   // pointers hides the LDS address space from the compiler, which then emits
@@ -299,15 +315,15 @@ __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4*
   // would also wait for the next chunk's prefetch.
   constexpr int ASZ = a_rows<TM>() * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
   constexpr int LA = NMT_GEMM_LA;
-  using St = Stager<TM, TN, NT, P>;
+  using St = Stager<TM, TN, NT, P, SRC16>;
   const int n = ce - cb;
   if (n <= 0) return;
   St st[LA];
   ARow arow[St::NA];
 #pragma unroll
   for (int i = 0; i < St::NA; ++i) arow[i] = seg_arow(sg, m0 + St::a_row(i), M);
-  auto load = [&](Stager<TM, TN, NT, P>& s, int i) {
-    s.load(arow, sg.bf16, sg.K, (cb + i) * P::KC, Wp, Npad, vq0 + (int64_t)(cb + i) * KQ, n0);
+  auto load = [&](St& s, int i) {
+    s.load(arow, sg.K, (cb + i) * P::KC, Wp, Npad, vq0 + (int64_t)(cb + i) * KQ, n0);
   };
   static_for<LA>([&](auto j) {
     if (j < n) load(st[j], j);
@@ -327,6 +343,22 @@ __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4*
       }
     });
   }
+}
+
+// gemm_segment_t with the segment's element type fixed at compile time (a
+// runtime choice between the two load paths made the compiler issue both
+// into the same registers, each waiting for the other).
+template <int TM, int TN, int NT, class P, class Compute>
+__device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
+                                             int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
+                                             int ce) {
+  if constexpr (P::kBF16) {
+    if (sg.bf16) {
+      gemm_segment_t<TM, TN, NT, P, true>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
+      return;
+    }
+  }
+  gemm_segment_t<TM, TN, NT, P, false>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
 }
 
 // All segments of A, restricted to global chunks [c_begin, c_end) (chunk c
