@@ -292,9 +292,13 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 }
 
 // Global-load lookahead of the tile GEMMs: chunks whose loads are in
-// flight in registers while a chunk is computed from LDS.
+// flight in registers while a chunk is computed from LDS (the GRU tile; the
+// plain tiles use NMT_PLAIN_LA).
 #ifndef NMT_GEMM_LA
 #define NMT_GEMM_LA 2
+#endif
+#ifndef NMT_PLAIN_LA
+#define NMT_PLAIN_LA 2
 #endif
 
 // Main loop over chunks [cb, ce) of one A segment (chunk indices local to
@@ -304,7 +308,7 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 // iteration i - 1, and `compute(As, Bs)` runs on it at iteration i.  The
 // loop is unrolled by LA so register sets are picked at compile time.  Ends
 // with a barrier, so a following call may reuse the LDS stages.
-template <int TM, int TN, int NT, class P, bool SRC16, class Compute>
+template <int TM, int TN, int NT, class P, bool SRC16, int LA, class Compute>
 __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
                                                int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
                                                int ce) {
@@ -314,7 +318,6 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
   // flat loads that share the global-load counter, so every fragment wait
   // would also wait for the next chunk's prefetch.
   constexpr int ASZ = a_rows<TM>() * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
-  constexpr int LA = NMT_GEMM_LA;
   using St = Stager<TM, TN, NT, P, SRC16>;
   const int n = ce - cb;
   if (n <= 0) return;
@@ -348,23 +351,23 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
 // gemm_segment_t with the segment's element type fixed at compile time (a
 // runtime choice between the two load paths made the compiler issue both
 // into the same registers, each waiting for the other).
-template <int TM, int TN, int NT, class P, class Compute>
+template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class Compute>
 __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
                                              int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
                                              int ce) {
   if constexpr (P::kBF16) {
     if (sg.bf16) {
-      gemm_segment_t<TM, TN, NT, P, true>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
+      gemm_segment_t<TM, TN, NT, P, true, LA>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
       return;
     }
   }
-  gemm_segment_t<TM, TN, NT, P, false>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
+  gemm_segment_t<TM, TN, NT, P, false, LA>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
 }
 
 // All segments of A, restricted to global chunks [c_begin, c_end) (chunk c
 // covers packed weight vector rows KQ*c .. KQ*c+KQ-1, whichever segment it
 // falls in).
-template <int TM, int TN, int NT, class P, class Compute>
+template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class Compute>
 __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __restrict__ Wp, int64_t Npad, int m0,
                                               int n0, f32x4* lds, Compute&& compute, int c_begin = 0,
                                               int c_end = 1 << 30) {
@@ -373,7 +376,7 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
     const ASeg sg = seg_at(A, i);
     const int s1 = s0 + sg.nchunk;
     const int cb = c_begin > s0 ? c_begin : s0, ce = c_end < s1 ? c_end : s1;
-    gemm_segment<TM, TN, NT, P>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
+    gemm_segment<TM, TN, NT, P, LA>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
     s0 = s1;
   }
 }

@@ -47,7 +47,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
     c_begin = (int)((int64_t)nc * blockIdx.z / ep.ksplit);
     c_end = (int)((int64_t)nc * (blockIdx.z + 1) / ep.ksplit);
   }
-  gemm_mainloop<TM, TN, NT, P>(
+  gemm_mainloop<TM, TN, NT, P, NMT_PLAIN_LA>(
       A, Wp, Npad, m0, n0, lds,
       [&](const f32x4* As, const f32x4* Bs) {
 #pragma unroll
