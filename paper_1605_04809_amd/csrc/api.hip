@@ -80,8 +80,7 @@ struct nmt_model {
   Allocs mem;
   void *emb_src = nullptr, *emb_tgt = nullptr;
   Packed enc_in, enc_U[2], att_Wc, init_W, g1, att_Wq, g2, ro, out;
-  float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr,
-        *out_b = nullptr;
+  float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr;
   GruBias enc_bias, g1_bias, g2_bias;
   int* err = nullptr;  // sticky device error flag
   // event timing of the step's phases (nmt_profile.h); not thread-safe
@@ -108,6 +107,8 @@ struct Seg {
   const float* W;  // [K x ld] row-major
   int K;
   int ld;
+  const float* X = nullptr;  // nullable: nx more rows [nx x ld] appended after the K rows of W
+  int nx = 0;
 };
 
 uint16_t to_bf16(float x) {  // nearest, ties to even (inputs are finite)
@@ -117,26 +118,38 @@ uint16_t to_bf16(float x) {  // nearest, ties to even (inputs are finite)
   return (uint16_t)(u >> 16);
 }
 
+float bf16_value(float x) {  // x rounded to the nearest bf16 value, as fp32
+  const uint32_t u = (uint32_t)to_bf16(x) << 16;
+  float y;
+  memcpy(&y, &u, 4);
+  return y;
+}
+
+// Number of bias rows appended to the packed output weights: fp32 stores
+// the bias in one row; bf16 in three (hi, mid, lo), whose exact sum is the
+// fp32 bias, so the MFMA adds the same bias the fp32 path does.
+int vocab_bias_rows(bool bf16) { return bf16 ? 3 : 1; }
+
 template <class ColMap>
 std::vector<float> pack_host(const std::vector<Seg>& segs, int64_t Npad, int kc, int KV, ColMap colmap,
                              int64_t* Kpad_out) {
   int64_t Kpad = 0;
-  for (const Seg& s : segs) Kpad += round_up(s.K, kc);
+  for (const Seg& s : segs) Kpad += round_up(s.K + s.nx, kc);
   std::vector<float> out((size_t)(Kpad * Npad), 0.f);
   std::vector<int> cols((size_t)Npad);
   for (int64_t np = 0; np < Npad; ++np) cols[(size_t)np] = colmap(np);
   int64_t koff = 0;
   for (const Seg& s : segs) {
-    for (int k = 0; k < s.K; ++k) {
+    for (int k = 0; k < s.K + s.nx; ++k) {
       const int64_t kk = koff + k;
       float* dst = out.data() + (kk / KV) * Npad * KV + (kk % KV);
-      const float* src = s.W + (int64_t)k * s.ld;
+      const float* src = k < s.K ? s.W + (int64_t)k * s.ld : s.X + (int64_t)(k - s.K) * s.ld;
       for (int64_t np = 0; np < Npad; ++np) {
         const int c = cols[(size_t)np];
         if (c >= 0) dst[np * KV] = src[c];
       }
     }
-    koff += round_up(s.K, kc);
+    koff += round_up(s.K + s.nx, kc);
   }
   *Kpad_out = Kpad;
   return out;
@@ -360,8 +373,9 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (d.A > 8 * 256) return fail(NMT_EINVAL, "A must be at most 2048");
   if (d.wtype != NMT_F32 && d.wtype != NMT_BF16) return fail(NMT_EINVAL, "unknown weight type %d", d.wtype);
   const bool bf16 = d.wtype == NMT_BF16;
-  if (round_up(d.E, chunk_k(bf16)) > vocab_max_kpad(bf16))
-    return fail(NMT_EINVAL, "E must be at most %d for this weight type", vocab_max_kpad(bf16));
+  if (round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)) > vocab_max_kpad(bf16))
+    return fail(NMT_EINVAL, "E must be at most %d for this weight type",
+                vocab_max_kpad(bf16) - vocab_bias_rows(bf16));
   const float* const* wp = (const float* const*)w;
   for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
     if (!wp[i]) return fail(NMT_EINVAL, "weight #%zu is NULL", i);
@@ -413,8 +427,26 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (e == hipSuccess)
     step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->ro_b, w->ro_b, E));
-  if (e == hipSuccess) step(pack_plain(m->mem, &m->out, {{w->out_W, E, V}}, V, kVocabTN, kc, bf16));
-  step(upload(m->mem, &m->out_b, w->out_b, V));
+  if (e == hipSuccess) {
+    // output weights with the bias as extra rows (see vocab_bias_rows)
+    const int nb = vocab_bias_rows(bf16);
+    std::vector<float> brows((size_t)nb * V);
+    for (int v = 0; v < V; ++v) {
+      const float b = w->out_b[v];
+      if (!bf16) {
+        brows[(size_t)v] = b;
+      } else {
+        const float hi = bf16_value(b), mid = bf16_value(b - hi);
+        brows[(size_t)v] = hi;
+        brows[(size_t)V + v] = mid;
+        brows[(size_t)2 * V + v] = b - hi - mid;  // exact in bf16: what remains has at most 8 significant bits
+      }
+    }
+    Seg sg{w->out_W, E, V, brows.data(), nb};
+    step(pack_plain(m->mem, &m->out, {sg}, V, kVocabTN, kc, bf16));
+    m->out.Krows = E;
+    m->out.nbias = nb;
+  }
   step(m->mem.alloc((void**)&m->err, sizeof(int)));
   if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
   if (e == hipSuccess) step(hipDeviceSynchronize());
@@ -628,10 +660,10 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   }
   mark(NMT_PHASE_READOUT + 1);
   // vocabulary projection with an online log-sum-exp per slice, then the combine
-  if (e == hipSuccess) e = launch_vocab_lse(t, B, E, m->out, m->out_b, V, part, L.nS, st);
+  if (e == hipSuccess) e = launch_vocab_lse(t, B, E, m->out, V, part, L.nS, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
-    e = launch_lse_combine(B, part, L.nS, t, E, m->out, m->out_b, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
+    e = launch_lse_combine(B, part, L.nS, t, E, m->out, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
                            m->err, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
@@ -696,7 +728,7 @@ static std::vector<void**> param_fields(nmt_model* m) {
   for (Packed* P : {&m->enc_in, &m->enc_U[0], &m->enc_U[1], &m->att_Wc, &m->init_W, &m->g1, &m->att_Wq, &m->g2,
                     &m->ro, &m->out})
     f.push_back(&P->d);
-  for (float** b : {&m->enc_in_b, &m->att_b, &m->init_b, &m->att_v, &m->ro_b, &m->out_b}) f.push_back((void**)b);
+  for (float** b : {&m->enc_in_b, &m->att_b, &m->init_b, &m->att_v, &m->ro_b}) f.push_back((void**)b);
   for (GruBias* g : {&m->enc_bias, &m->g1_bias, &m->g2_bias}) {
     f.push_back((void**)&g->brz);
     f.push_back((void**)&g->bni);

@@ -223,6 +223,26 @@ __device__ __forceinline__ f32x4 load_a_vec(const char* row, int bf16src, int K,
   }
 }
 
+// Vector kq of an activation row with 1 at the bias slots k = E .. E+nb-1
+// (the output weights carry the bias in those rows).
+template <class P>
+__device__ __forceinline__ f32x4 with_bias_ones(f32x4 v, int kq, int E, int nb) {
+  const int k0 = kq * P::KV;
+  if (k0 + P::KV <= E || k0 >= E + nb) return v;
+  if constexpr (P::kBF16) {
+    bf16x8 b = __builtin_bit_cast(bf16x8, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (k0 + e >= E && k0 + e < E + nb) b[e] = (__bf16)1.f;
+    return __builtin_bit_cast(f32x4, b);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (k0 + e >= E && k0 + e < E + nb) v[e] = 1.f;
+    return v;
+  }
+}
+
 // Rows of an A stage in LDS: TM plus one vector of padding, so that the
 // transposed stores of the staging (consecutive lanes writing consecutive
 // vectors of one row, a stage row apart) fall in different banks.

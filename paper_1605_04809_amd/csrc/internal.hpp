@@ -36,6 +36,10 @@ struct Packed {
   int64_t Kpad = 0;  // sum of the padded K of its segments
   int64_t Npad = 0;
   int N = 0;         // valid columns (for GRU: 3H)
+  // Output weights only: rows Krows .. Krows+nbias-1 of the packed matrix
+  // hold the bias (fp32: one row; bf16: hi, mid, lo parts summing to it).
+  int Krows = 0;
+  int nbias = 0;
 };
 
 enum class Tile { Small, Large };
@@ -89,8 +93,8 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
 // largest padded E the vocabulary kernel keeps in LDS.
 int vocab_slices(int M, int64_t Npad, bool bf16);
 int vocab_max_kpad(bool bf16);
-hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
-                            int nS, hipStream_t st);
+hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
+                            hipStream_t st);
 // Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same
 // indices (req_off nullable: one request per row, req[b] -> logp[b]).
 // state_row (nullable) is checked against pool_rows like the other ids.
@@ -101,8 +105,8 @@ struct Requests {
   const int32_t* state_row;
   int32_t pool_rows;
 };
-hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
-                              const float* bias, int V, const Requests& rq, const int32_t* y_prev,
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W, int V,
+                              const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
                               hipStream_t st);
 // Attention groups rows by sentence through workspace arrays: perm [B]

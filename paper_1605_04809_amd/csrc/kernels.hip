@@ -291,15 +291,27 @@ struct VocabTune {
 
 // Streaming vocabulary projection with an online log-sum-exp.
 //
+// The output bias travels inside the packed weights: rows E .. E+nb-1 of the
+// packed matrix hold it (one fp32 row, or a bf16 split hi + mid + lo that
+// sums to the fp32 value), and the activation rows carry 1 at those k, so
+// each MFMA accumulator ends as the full logit z = t . W[:, v] + b[v].
+//
 // A block owns VTM rows and one slice of the vocabulary.  Its rows of the
 // readout t stay in LDS for the whole kernel as 16-byte vectors
 // [Kpad/KV][VTM]; the packed output weights stream straight from HBM/L2 into
 // registers, VPF k groups ahead, so the main loop has no barrier.  Wave w
 // takes the slice's 32-column blocks in groups of VFN (groups w, w+VNW, ...),
-// each for all VTM rows; each lane keeps a running base-2 log-sum-exp for each
-// of its row slots, and the 32 lanes and the waves are merged once at the
-// end.  One (max, sum) pair per row and slice goes to HBM as float2
-// [slice][row]; the logits never do.
+// each for all VTM rows.
+//
+// The MFMA puts the vocabulary on the output's rows and the batch rows on
+// its columns, so the 16 accumulator registers of a lane are 16 logits of
+// one batch row.  The fold of a group into a lane's running (max, sum) is
+// then a block max (three-input maxima), one rescale of the old sum, and one
+// fused multiply-add, one exp and one add per logit; a lane keeps one
+// (max, sum) pair per batch row slot.  The two halves of a wave (same batch
+// rows, other vocabulary rows) and the waves are merged once at the end.
+// One (max, sum) pair per row and slice goes to HBM as float2 [slice][row];
+// the logits never do.
 //
 // Slices are spread over XCDs: blocks with ids congruent mod 8 run on one
 // XCD, and that XCD takes slices xcd, xcd+8, ... for every row tile, so the
@@ -310,17 +322,17 @@ struct VocabTune {
 // (readfirstlane), loads are unconditional (clamped past the end), a ring
 // slot is refilled only after its MFMAs, and A fragments ping-pong between
 // two named register sets; otherwise the compiler drains every load and
-// rotates registers at each loop back-edge.
+// rotates registers at each loop back-edge.  No other vector-memory load is
+// issued in the loop: its wait would drain the prefetch ring.
 template <class P, int VPF>
 __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E,
-                                                                      int Kpad, const f32x4* __restrict__ Wp,
-                                                                      int64_t Npad, const float* __restrict__ bias,
-                                                                      int V, int nM, int nS,
+                                                                      int nb, int Kpad, const f32x4* __restrict__ Wp,
+                                                                      int64_t Npad, int V, int nM, int nS,
                                                                       float2* __restrict__ part) {
   constexpr int VTM = VocabTune<P>::VTM, VNW = VocabTune<P>::VNW, VFN = VocabTune<P>::VFN;
   constexpr int FM = VTM / 32;
   __shared__ f32x4 As[VQMAX];
-  __shared__ float red[VNW][VTM][2];
+  __shared__ float2 red[VNW][VTM];
   const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
   const int slice = (slot / nM) * 8 + xcd, mt = slot % nM;
   if (slice >= nS) return;
@@ -329,11 +341,13 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
 
-  // stationary A tile: As[kq][m] = vector kq of row m0 + m
+  // stationary activation tile: As[kq][m] = vector kq of row m0 + m, with
+  // the bias slots set to 1
   const int KQ = Kpad / P::KV;
   for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
     const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
-    As[kq * VTM + m] = load_a_vec<P>(row < M ? (const char*)(t + (int64_t)row * E) : nullptr, 0, E, kq * P::KV);
+    As[kq * VTM + m] = with_bias_ones<P>(
+        load_a_vec<P>(row < M ? (const char*)(t + (int64_t)row * E) : nullptr, 0, E, kq * P::KV), kq, E, nb);
   }
   __syncthreads();
 
@@ -344,16 +358,15 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
   const int nmine = ngrp > wave ? (ngrp - wave + VNW - 1) / VNW : 0;
 
-  // Running log-sum-exp of each row slot in base 2: run_m is the largest
-  // t = z*log2(e) seen so far, run_s the sum of 2^(t - run_m).
-  float run_m[FM][16], run_s[FM][16];
+  // Running log-sum-exp of each batch row slot i (row m0 + 32 i + l32) over
+  // this lane's logits: run_m the largest logit seen, run_s the sum of
+  // e^(z - run_m).
+  float run_m[FM], run_s[FM];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      run_m[i][r] = -INFINITY;
-      run_s[i][r] = 0.f;
-    }
+  for (int i = 0; i < FM; ++i) {
+    run_m[i] = -INFINITY;
+    run_s[i] = 0.f;
+  }
 
   // Weight fragments are read in (group, k group) order through a scalar
   // cursor; ring slot p always holds step q with q % VPF == p.  The cursor
@@ -415,14 +428,15 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
           a[i] = ao[i];
         }
       }
+      // weights as the MFMA's row operand, activations as its column operand
 #pragma unroll
       for (int f = 0; f < VFN; ++f)
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           if constexpr (decltype(zc)::value)
-            acc[i][f] = P::mma0(a[i], ring[p][f]);
+            acc[i][f] = P::mma0(ring[p][f], a[i]);
           else
-            P::mma(a[i], ring[p][f], acc[i][f]);
+            P::mma(ring[p][f], a[i], acc[i][f]);
         }
       load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
       // Instruction order within the step: one MFMA, the next step's A
@@ -437,61 +451,74 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     // the first VPF steps, whose first step starts from zero, then the rest
     static_for<VPF>([&](auto pc) { kstep(0, pc, std::bool_constant<decltype(pc)::value == 0>{}); });
     for (int kg0 = VPF; kg0 < NKG; kg0 += VPF) static_for<VPF>([&](auto pc) { kstep(kg0, pc, std::false_type{}); });
-    // fold the group's columns into the running log-sum-exp of each row slot
+
+    // Register r of a lane holds vocabulary row 32 cb + acc_row(r, h).  A
+    // group with columns past V or missing blocks (only at the end of a
+    // slice) masks them out; the test is uniform over the wave.
+    const int cb0 = cb_begin + (wave + VNW * gi) * VFN;
+    if ((cb0 + VFN) * 32 > V || cb0 + VFN > cb_end) {
 #pragma unroll
-    for (int f = 0; f < VFN; ++f) {
-      const int cb = cb_begin + (wave + VNW * gi) * VFN + f;
-      const int n = cb * 32 + l32;
-      if (cb < cb_end && n < V) {
-        const float b2 = bias[n] * kLog2e;
+      for (int f = 0; f < VFN; ++f)
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int r = 0; r < 16; ++r) {
+          const bool ok = cb0 + f < cb_end && (cb0 + f) * 32 + acc_row(r, h) < V;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            // One exp per logit: with d = t - m, 2^-|d| is the new term when
-            // t <= m, and the factor that rescales the old sum to t when t > m.
-            const float t = fmaf(acc[i][f][r], kLog2e, b2);
-            const float d = t - run_m[i][r];
-            const float e = __builtin_amdgcn_exp2f(-fabsf(d));
-            const bool up = d > 0.f;
-            run_s[i][r] = up ? fmaf(run_s[i][r], e, 1.f) : run_s[i][r] + e;
-            run_m[i][r] = up ? t : run_m[i][r];
-          }
-      }
+          for (int i = 0; i < FM; ++i) acc[i][f][r] = ok ? acc[i][f][r] : -INFINITY;
+        }
+    }
+    // fold the group into each row slot's running log-sum-exp
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float bm = acc[i][0][0];
+#pragma unroll
+      for (int f = 0; f < VFN; ++f)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) bm = fmaxf(bm, acc[i][f][r]);
+      const float mn = fmaxf(run_m[i], bm);
+      const bool none = mn == -INFINITY;  // nothing but masked logits so far
+      const float sc = none ? 1.f : __builtin_amdgcn_exp2f((run_m[i] - mn) * kLog2e);
+      const float nm = none ? 0.f : -mn * kLog2e;
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+      for (int f = 0; f < VFN; ++f)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          s0 += __builtin_amdgcn_exp2f(fmaf(acc[i][f][r], kLog2e, nm));
+          s1 += __builtin_amdgcn_exp2f(fmaf(acc[i][f][r + 1], kLog2e, nm));
+        }
+      run_s[i] = fmaf(run_s[i], sc, s0 + s1);
+      run_m[i] = mn;
     }
   }
 
-  // merge the 32 lanes of each half-wave (they hold different columns of the same rows)
+  // merge the two halves of the wave (lanes l32 and l32 + 32 hold the same rows)
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float mx = half_max(run_m[i][r]);
-      const float s = mx == -INFINITY ? 0.f : run_s[i][r] * __builtin_amdgcn_exp2f(run_m[i][r] - mx);
-      const float st = half_sum(s);
-      if (l32 == 0) {
-        const int rl = 32 * i + acc_row(r, h);
-        red[wave][rl][0] = mx;
-        red[wave][rl][1] = st;
-      }
-    }
+  for (int i = 0; i < FM; ++i) {
+    const float om = __shfl_xor(run_m[i], 32, 64), os = __shfl_xor(run_s[i], 32, 64);
+    const float mx = fmaxf(run_m[i], om);
+    float s = 0.f;
+    if (mx != -INFINITY)
+      s = run_s[i] * __builtin_amdgcn_exp2f((run_m[i] - mx) * kLog2e) +
+          os * __builtin_amdgcn_exp2f((om - mx) * kLog2e);
+    if (h == 0) red[wave][32 * i + l32] = float2{mx, s};
+  }
   __syncthreads();
   // merge the waves and write this slice's partial for each row
   for (int rl = threadIdx.x; rl < VTM; rl += VNW * 64) {
     const int row = m0 + rl;
     float mx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < VNW; ++w) mx = fmaxf(mx, red[w][rl][0]);
+    for (int w = 0; w < VNW; ++w) mx = fmaxf(mx, red[w][rl].x);
     float s = 0.f;
     if (mx != -INFINITY) {
 #pragma unroll
       for (int w = 0; w < VNW; ++w) {
-        const float mw = red[w][rl][0];
-        if (mw != -INFINITY) s += red[w][rl][1] * __builtin_amdgcn_exp2f(mw - mx);
+        const float mw = red[w][rl].x;
+        if (mw != -INFINITY) s += red[w][rl].y * __builtin_amdgcn_exp2f((mw - mx) * kLog2e);
       }
     }
-    // partials leave in natural-log units: (max logit, sum of e^(z - max))
-    if (row < M) part[(int64_t)slice * M + row] = float2{mx * kLn2, s};
+    // (max logit, sum of e^(z - max)) in natural-log units
+    if (row < M) part[(int64_t)slice * M + row] = float2{mx, s};
   }
 }
 
@@ -508,33 +535,31 @@ int vocab_max_kpad(bool bf16) {
 }
 
 template <class P>
-hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part, int nS,
-                     hipStream_t st) {
+hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS, hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
   const int nM = ceil_div(M, VocabTune<P>::VTM);
   dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
   const f32x4* Wp = (const f32x4*)W.d;
   constexpr int PF = VocabTune<P>::VPF_MAX;
   if (PF >= 16 && nkg % 16 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad,
-                       bias, V, nM, nS, part);
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+                       W.Npad, V, nM, nS, part);
   else if (PF >= 8 && nkg % 8 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad,
-                       bias, V, nM, nS, part);
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+                       W.Npad, V, nM, nS, part);
   else if (nkg % 4 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, M, E, (int)W.Kpad, Wp, W.Npad, bias, V, nM, nS,
+    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
                        part);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, const float* bias, int V, float2* part,
-                            int nS, hipStream_t st) {
+hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
+                            hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (W.Kpad > vocab_max_kpad(W.bf16)) return hipErrorInvalidValue;
-  return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, bias, V, part, nS, st)
-                : vocab_lse<PrecF32>(t, M, E, W, bias, V, part, nS, st);
+  if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1) return hipErrorInvalidValue;
+  return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, V, part, nS, st) : vocab_lse<PrecF32>(t, M, E, W, V, part, nS, st);
 }
 
 // ---------------------------------------------------- partials combine
@@ -554,15 +579,15 @@ __device__ __forceinline__ float dot_vec(const f32x4& a, const f32x4& b) {
 }
 
 // One wave per row: merges the per-slice (max, sum) pairs into logZ, scores
-// each requested word with its own dot product t . out_W[:, w] + out_b[w]
-// (t rounded as the vocabulary kernel's MFMA inputs are), and checks the
-// row's ids.  A row with any id out of range, or with malformed request
+// each requested word with its own dot product over the packed column of w,
+// bias rows included (t rounded, and 1 at the bias slots, as the vocabulary
+// kernel's MFMA inputs are), and checks the row's ids.  A row with any id out of range, or with malformed request
 // offsets, gets NaN outputs and sets the flag.
 template <class P>
 __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __restrict__ part, int nS,
-                                                     const float* __restrict__ t, int E, int Kpad,
-                                                     const f32x4* __restrict__ Wp, int64_t Npad,
-                                                     const float* __restrict__ bias, int V, Requests rq,
+                                                     const float* __restrict__ t, int E, int nb, int Kpad,
+                                                     const f32x4* __restrict__ Wp, int64_t Npad, int V,
+                                                     Requests rq,
                                                      const int32_t* __restrict__ y_prev,
                                                      const int32_t* __restrict__ sent_id, int S, float* logp,
                                                      float* logZ, int* err) {
@@ -600,23 +625,25 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
     const int w = rq.req[j];
     float dot = 0.f;
     for (int kq = lane; kq < Kpad / P::KV; kq += 64)
-      dot += dot_vec<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), Wp[(int64_t)kq * Npad + w]);
+      dot += dot_vec<P>(with_bias_ones<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), kq, E, nb),
+                        Wp[(int64_t)kq * Npad + w]);
     dot = wave_sum(dot);
-    if (lane == 0) logp[j] = dot + bias[w] - lz;
+    if (lane == 0) logp[j] = dot - lz;
   }
   if (lane == 0 && logZ) logZ[row] = lz;
 }
 
-hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W,
-                              const float* bias, int V, const Requests& rq, const int32_t* y_prev,
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W, int V,
+                              const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
   if (B <= 0) return hipSuccess;
+  if (W.Krows != E || W.nbias < 1) return hipErrorInvalidValue;
   if (W.bf16)
     hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
-                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, rq, y_prev, sent_id, S, logp, logZ, err);
+                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
   else
     hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
-                       (int)W.Kpad, (const f32x4*)W.d, W.Npad, bias, V, rq, y_prev, sent_id, S, logp, logZ, err);
+                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
   return hipGetLastError();
 }
 
