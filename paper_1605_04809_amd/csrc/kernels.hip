@@ -268,12 +268,13 @@ constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
 // 32-column blocks per wave step and up to VPF_MAX k groups of weight
 // fragments in flight.  fp32: 64 rows, 8 waves, one block, 16 deep.  bf16
 // (MFMAs 8x faster per k): 128 rows so each weight fragment feeds four
-// MFMAs, halving the L1 traffic per flop.
+// MFMAs, and two column blocks per step so each activation fragment read
+// from LDS feeds two (a 64 x 128 tile per wave, 8 MFMAs per step).
 #ifndef NMT_BF16_VTM
 #define NMT_BF16_VTM 128
 #endif
 #ifndef NMT_BF16_VFN
-#define NMT_BF16_VFN 1
+#define NMT_BF16_VFN 2
 #endif
 #ifndef NMT_BF16_VNW
 #define NMT_BF16_VNW 8
@@ -281,12 +282,21 @@ constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
 #ifndef NMT_BF16_VPF
 #define NMT_BF16_VPF 8
 #endif
+#ifndef NMT_F32_VFN
+#define NMT_F32_VFN 1
+#endif
+#ifndef NMT_F32_VNW
+#define NMT_F32_VNW 8
+#endif
+#ifndef NMT_F32_VPF
+#define NMT_F32_VPF 16
+#endif
 template <class P>
 struct VocabTune {
   static constexpr int VTM = P::kBF16 ? NMT_BF16_VTM : 64;
-  static constexpr int VNW = P::kBF16 ? NMT_BF16_VNW : 8;
-  static constexpr int VFN = P::kBF16 ? NMT_BF16_VFN : 1;
-  static constexpr int VPF_MAX = P::kBF16 ? NMT_BF16_VPF : 16;
+  static constexpr int VNW = P::kBF16 ? NMT_BF16_VNW : NMT_F32_VNW;
+  static constexpr int VFN = P::kBF16 ? NMT_BF16_VFN : NMT_F32_VFN;
+  static constexpr int VPF_MAX = P::kBF16 ? NMT_BF16_VPF : NMT_F32_VPF;
 };
 
 // Streaming vocabulary projection with an online log-sum-exp.
