@@ -92,29 +92,29 @@ def read_traffic(workload: str):
 
 
 def cpu_baseline(wl, min_seconds=10.0, max_seconds=30.0):
-    """The fp64 oracle as it stands, on a bounded sample of rows of the workload."""
+    """The fp64 oracle as it stands, on a bounded sample of rows of the workload:
+    chunks of consecutive rows (wrapping round the batch) until at least
+    min_seconds of scoring, sized to stay under max_seconds."""
     import oracle
     m = oracle.Model.from_workload(wl)
     ctx, pctx, _ = oracle.encode(m, wl.src_ids, wl.src_len)   # source initialisation, not timed
     B = len(wl.y_prev)
     threads = oracle.num_threads()
     done, elapsed, chunk, start_row = 0, 0.0, max(threads, 8), 0
-    while elapsed < min_seconds and done < B:
-        rows = np.arange(start_row, min(start_row + chunk, B))
+    while elapsed < min_seconds:
+        rows = (start_row + np.arange(chunk)) % B
         t0 = time.perf_counter()
         oracle.score_batch(m, ctx, pctx, wl.src_len, wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows],
                            wl.req[rows], intermediates=False)
         dt = time.perf_counter() - t0
         elapsed += dt
         done += len(rows)
-        start_row += len(rows)
+        start_row = (start_row + len(rows)) % B
         rate = len(rows) / dt
-        chunk = int(max(threads, min(B - start_row, rate * min(min_seconds - elapsed, max_seconds - elapsed))))
-        if chunk <= 0:
-            break
+        chunk = int(max(threads, min(4 * B, rate * min(min_seconds - elapsed + 1.0, max_seconds - elapsed))))
     return {"value": done / elapsed, "unit": UNIT, "cores": threads, "kind": "oracle",
-            "sample": f"first {done} of {B} rows of the same workload, one step each, fp64, "
-                      f"{elapsed:.1f} s wall; source encoding excluded"}
+            "sample": f"{done} rows of the same workload (consecutive rows of the {B}-row batch, wrapping "
+                      f"round it), one step each, fp64, {elapsed:.1f} s wall; source encoding excluded"}
 
 
 def copy_probe(nbytes: int, reps: int = 5):

@@ -291,6 +291,9 @@ constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
 #ifndef NMT_F32_VPF
 #define NMT_F32_VPF 16
 #endif
+#ifndef NMT_VOCAB_PRIO
+#define NMT_VOCAB_PRIO 1
+#endif
 template <class P>
 struct VocabTune {
   static constexpr int VTM = P::kBF16 ? NMT_BF16_VTM : 64;
@@ -459,8 +462,12 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
       __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
     };
     // the first VPF steps, whose first step starts from zero, then the rest
+    // MFMA steps at raised priority, the fold at normal priority, so the other
+    // wave on the SIMD keeps issuing MFMAs while this one folds
+    __builtin_amdgcn_s_setprio(NMT_VOCAB_PRIO);
     static_for<VPF>([&](auto pc) { kstep(0, pc, std::bool_constant<decltype(pc)::value == 0>{}); });
     for (int kg0 = VPF; kg0 < NKG; kg0 += VPF) static_for<VPF>([&](auto pc) { kstep(kg0, pc, std::false_type{}); });
+    __builtin_amdgcn_s_setprio(0);
 
     // Register r of a lane holds vocabulary row 32 cb + acc_row(r, h).  A
     // group with columns past V or missing blocks (only at the end of a
