@@ -376,6 +376,8 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)) > vocab_max_kpad(bf16))
     return fail(NMT_EINVAL, "E must be at most %d for this weight type",
                 vocab_max_kpad(bf16) - vocab_bias_rows(bf16));
+  if (!vocab_offsets_fit(round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)), round_up(d.V, kVocabTN), bf16))
+    return fail(NMT_EINVAL, "the packed output weights (E x V) must stay under 2 GiB");
   const float* const* wp = (const float* const*)w;
   for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
     if (!wp[i]) return fail(NMT_EINVAL, "weight #%zu is NULL", i);

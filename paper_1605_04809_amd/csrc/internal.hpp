@@ -93,6 +93,7 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
 // largest padded E the vocabulary kernel keeps in LDS.
 int vocab_slices(int M, int64_t Npad, bool bf16);
 int vocab_max_kpad(bool bf16);
+bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
                             hipStream_t st);
 // Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same

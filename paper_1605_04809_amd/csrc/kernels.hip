@@ -269,7 +269,8 @@ constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
 // fragments in flight.  fp32: 64 rows, 8 waves, one block, 16 deep.  bf16
 // (MFMAs 8x faster per k): 128 rows so each weight fragment feeds four
 // MFMAs, and two column blocks per step so each activation fragment read
-// from LDS feeds two (a 64 x 128 tile per wave, 8 MFMAs per step).
+// from LDS feeds two (a 64 x 128 tile per wave, 8 MFMAs per step); 4 deep,
+// as 8 deep runs out of registers.
 #ifndef NMT_BF16_VTM
 #define NMT_BF16_VTM 128
 #endif
@@ -280,7 +281,7 @@ constexpr int VQMAX = 9216;             // A-tile vectors held in LDS (144 KB)
 #define NMT_BF16_VNW 8
 #endif
 #ifndef NMT_BF16_VPF
-#define NMT_BF16_VPF 8
+#define NMT_BF16_VPF 4
 #endif
 #ifndef NMT_F32_VFN
 #define NMT_F32_VFN 1
@@ -369,7 +370,6 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
   const int ngrp = (cb_end - cb_begin + VFN - 1) / VFN;
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
-  const int nmine = ngrp > wave ? (ngrp - wave + VNW - 1) / VNW : 0;
 
   // Running log-sum-exp of each batch row slot i (row m0 + 32 i + l32) over
   // this lane's logits: run_m the largest logit seen, run_s the sum of
@@ -381,50 +381,45 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     run_s[i] = 0.f;
   }
 
-  // Weight fragments are read in (group, k group) order through a scalar
-  // cursor; ring slot p always holds step q with q % VPF == p.  The cursor
-  // keeps a 64-bit offset that advances by one k group per step and is reset
-  // when the group changes; loads past this wave's last group, or of a
-  // group's missing last blocks, re-read fragment 0 of the matrix (always in
-  // bounds).  Keeping this to a few scalar instructions per step matters in
-  // bf16, whose MFMAs are short.
-  const f32x4* wlane = Wp + (int64_t)h * Npad + l32;
-  const int64_t kstride = 2 * Npad;
-  int pg = wave, pkg = 0;
-  int64_t off = (int64_t)(cb_begin + pg * VFN) * 32;
-  bool okf[VFN];
-  auto set_group = [&]() {
+  // Weight fragments are read through a buffer resource over the packed
+  // matrix: a lane's offset (its column and k half) is fixed, and one scalar
+  // offset per step selects the group's k group, so a step costs one scalar
+  // add and no address arithmetic.  Ring slot p always holds step q with
+  // q % VPF == p; the last VPF steps of a group refill the ring with the
+  // first VPF steps of the wave's next group.  A wave past its last group,
+  // or a group's missing last block, reads other columns of the matrix
+  // (masked at the fold); offsets past the end of the matrix read zeros.
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Wp, (short)0, (int)(KQ * Npad * 16), 0x00020000);
+  const int kbytes = (int)(32 * Npad);             // one k group: two rows of vectors
+  int lane_off[VFN];
 #pragma unroll
-    for (int f = 0; f < VFN; ++f) okf[f] = pg < ngrp && cb_begin + pg * VFN + f < cb_end;
-  };
-  set_group();
-  auto load_next = [&](f32x4 (&dst)[VFN]) {
+  for (int f = 0; f < VFN; ++f) lane_off[f] = (int)((h * Npad + l32 + 32 * f) * 16);
+  auto gbase = [&](int g) { return g < ngrp ? (cb_begin + g * VFN) * 512 : 0; };  // bytes of the group's block 0
+  auto load = [&](f32x4 (&dst)[VFN], int soff) {
 #pragma unroll
-    for (int f = 0; f < VFN; ++f) dst[f] = wlane[okf[f] ? off + 32 * f : 0];
-    off += kstride;
-    if (++pkg == NKG) {
-      pkg = 0;
-      pg += VNW;
-      off = (int64_t)(cb_begin + pg * VFN) * 32;
-      set_group();
-    }
+    for (int f = 0; f < VFN; ++f)
+      dst[f] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, lane_off[f], soff, 0));
   };
+  int sbase = gbase(wave);  // the group whose steps are being loaded
   f32x4 ring[VPF][VFN];
 #pragma unroll
-  for (int p = 0; p < VPF; ++p) load_next(ring[p]);
+  for (int p = 0; p < VPF; ++p) load(ring[p], sbase + p * kbytes);
   const f32x4* arow = As + h * VTM + l32;  // + 2*kg*VTM per k group
   f32x4 ae[FM], ao[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) ae[i] = arow[32 * i];
   static_assert(VPF % 2 == 0, "even/odd fragment sets");
 
-  for (int gi = 0; gi < nmine; ++gi) {
+  // groups wave, wave + VNW, ... of the slice
+  for (int gcur = wave; gcur < ngrp; gcur += VNW) {
     f32x16 acc[FM][VFN];
+    const int nbase = gbase(gcur + VNW);
     // One k-group step; `zc` (compile time) starts the accumulators from an
-    // inline zero instead of clearing them with register moves.
-    auto kstep = [&](int kg0, auto pc, auto zc) {
+    // inline zero instead of clearing them with register moves; `soff` is
+    // the scalar offset of the step that refills this slot.
+    auto kstep = [&](int kg, auto pc, auto zc, int soff) {
       constexpr int p = decltype(pc)::value;
-      const int kg = kg0 + p;
       const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
       const f32x4* an = arow + kn * 2 * VTM;
       f32x4 a[FM];
@@ -451,7 +446,7 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
           else
             P::mma(ring[p][f], a[i], acc[i][f]);
         }
-      load_next(ring[p]);  // refill the slot just consumed, VPF steps ahead
+      load(ring[p], soff);  // refill the slot just consumed, VPF steps ahead
       // Instruction order within the step: one MFMA, the next step's A
       // fragment reads (so they have the remaining MFMAs to land), the rest
       // of the MFMAs, then the refill.
@@ -461,18 +456,33 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
       __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
     };
-    // the first VPF steps, whose first step starts from zero, then the rest
-    // MFMA steps at raised priority, the fold at normal priority, so the other
-    // wave on the SIMD keeps issuing MFMAs while this one folds
+    // Blocks of VPF steps (a group has at least two): the first starts from
+    // zero, the last refills the ring from the next group.  MFMA steps run at raised priority and the
+    // fold at normal priority, so the other wave on the SIMD keeps issuing
+    // MFMAs while this one folds.
     __builtin_amdgcn_s_setprio(NMT_VOCAB_PRIO);
-    static_for<VPF>([&](auto pc) { kstep(0, pc, std::bool_constant<decltype(pc)::value == 0>{}); });
-    for (int kg0 = VPF; kg0 < NKG; kg0 += VPF) static_for<VPF>([&](auto pc) { kstep(kg0, pc, std::false_type{}); });
+    static_for<VPF>([&](auto pc) {
+      constexpr int p = decltype(pc)::value;
+      kstep(p, pc, std::bool_constant<p == 0>{}, sbase + (VPF + p) * kbytes);
+    });
+    for (int kg0 = VPF; kg0 < NKG - VPF; kg0 += VPF) {
+      const int s0 = sbase + (kg0 + VPF) * kbytes;
+      static_for<VPF>([&](auto pc) {
+        constexpr int p = decltype(pc)::value;
+        kstep(kg0 + p, pc, std::false_type{}, s0 + p * kbytes);
+      });
+    }
+    static_for<VPF>([&](auto pc) {
+      constexpr int p = decltype(pc)::value;
+      kstep(NKG - VPF + p, pc, std::false_type{}, nbase + p * kbytes);
+    });
     __builtin_amdgcn_s_setprio(0);
+    sbase = nbase;
 
     // Register r of a lane holds vocabulary row 32 cb + acc_row(r, h).  A
     // group with columns past V or missing blocks (only at the end of a
     // slice) masks them out; the test is uniform over the wave.
-    const int cb0 = cb_begin + (wave + VNW * gi) * VFN;
+    const int cb0 = cb_begin + gcur * VFN;
     if ((cb0 + VFN) * 32 > V || cb0 + VFN > cb_end) {
 #pragma unroll
       for (int f = 0; f < VFN; ++f)
@@ -547,6 +557,11 @@ int vocab_slices(int M, int64_t Npad, bool bf16) {
   return nS;
 }
 
+// The vocabulary kernel addresses the packed weights with 32-bit byte offsets.
+bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16) {
+  return Kpad / (bf16 ? PrecBF16::KV : PrecF32::KV) * Npad * 16 < ((int64_t)1 << 31);
+}
+
 int vocab_max_kpad(bool bf16) {
   return bf16 ? VQMAX / VocabTune<PrecBF16>::VTM * PrecBF16::KV : VQMAX / VocabTune<PrecF32>::VTM * PrecF32::KV;
 }
@@ -558,14 +573,19 @@ hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, int V, float
   dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
   const f32x4* Wp = (const f32x4*)W.d;
   constexpr int PF = VocabTune<P>::VPF_MAX;
-  if (PF >= 16 && nkg % 16 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 4)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+  // the deepest prefetch that divides the k groups into at least two blocks
+  auto fits = [&](int vpf) { return PF >= vpf && nkg % vpf == 0 && nkg >= 2 * vpf; };
+  if (fits(16))
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
                        W.Npad, V, nM, nS, part);
-  else if (PF >= 8 && nkg % 8 == 0)
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 4)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+  else if (fits(8))
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 2)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
                        W.Npad, V, nM, nS, part);
-  else if (nkg % 4 == 0)
+  else if (fits(4))
     hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
+                       part);
+  else if (fits(2))
+    hipLaunchKernelGGL((k_vocab_lse<P, 2>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
                        part);
   else
     return hipErrorInvalidValue;
@@ -576,6 +596,7 @@ hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V
                             hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1) return hipErrorInvalidValue;
+  if (!vocab_offsets_fit(W.Kpad, W.Npad, W.bf16)) return hipErrorInvalidValue;
   return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, V, part, nS, st) : vocab_lse<PrecF32>(t, M, E, W, V, part, nS, st);
 }
 
