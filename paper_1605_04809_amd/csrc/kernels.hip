@@ -417,11 +417,13 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     const int nbase = gbase(gcur + VNW);
     // One k-group step; `zc` (compile time) starts the accumulators from an
     // inline zero instead of clearing them with register moves; `soff` is
-    // the scalar offset of the step that refills this slot.
-    auto kstep = [&](int kg, auto pc, auto zc, int soff) {
+    // the scalar offset of the step that refills this slot; `ablk` is the
+    // LDS address of k group kg0 + 1 for the block starting at kg0, so the
+    // next step's fragments sit at compile-time offsets from it (the last
+    // step of a group wraps to k group 0 of the next one).
+    auto kstep = [&](const f32x4* ablk, auto pc, auto zc, auto last_blk, int soff) {
       constexpr int p = decltype(pc)::value;
-      const int kn = kg + 1 == NKG ? 0 : kg + 1;  // next k group (wraps to the next group)
-      const f32x4* an = arow + kn * 2 * VTM;
+      const f32x4* an = (decltype(last_blk)::value && p == VPF - 1) ? arow : ablk + p * 2 * VTM;
       f32x4 a[FM];
       if constexpr (p % 2 == 0) {
 #pragma unroll
@@ -463,19 +465,23 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     __builtin_amdgcn_s_setprio(NMT_VOCAB_PRIO);
     static_for<VPF>([&](auto pc) {
       constexpr int p = decltype(pc)::value;
-      kstep(p, pc, std::bool_constant<p == 0>{}, sbase + (VPF + p) * kbytes);
+      kstep(arow + 2 * VTM, pc, std::bool_constant<p == 0>{}, std::false_type{}, sbase + (VPF + p) * kbytes);
     });
     for (int kg0 = VPF; kg0 < NKG - VPF; kg0 += VPF) {
       const int s0 = sbase + (kg0 + VPF) * kbytes;
+      const f32x4* ablk = arow + (kg0 + 1) * 2 * VTM;
       static_for<VPF>([&](auto pc) {
         constexpr int p = decltype(pc)::value;
-        kstep(kg0 + p, pc, std::false_type{}, s0 + p * kbytes);
+        kstep(ablk, pc, std::false_type{}, std::false_type{}, s0 + p * kbytes);
       });
     }
-    static_for<VPF>([&](auto pc) {
-      constexpr int p = decltype(pc)::value;
-      kstep(NKG - VPF + p, pc, std::false_type{}, nbase + p * kbytes);
-    });
+    {
+      const f32x4* ablk = arow + (NKG - VPF + 1) * 2 * VTM;
+      static_for<VPF>([&](auto pc) {
+        constexpr int p = decltype(pc)::value;
+        kstep(ablk, pc, std::false_type{}, std::true_type{}, nbase + p * kbytes);
+      });
+    }
     __builtin_amdgcn_s_setprio(0);
     sbase = nbase;
 
