@@ -145,60 +145,51 @@ __device__ __forceinline__ int total_chunks(const AOperand& A) {
          (A.nseg > 2 ? A.seg[2].nchunk : 0);
 }
 
-// Byte address of this thread's row of segment s (nullptr: a zero row).
-__device__ __forceinline__ const char* seg_row(const ASeg& s, int row, int M) {
-  if (row >= M) return nullptr;
-  int64_t r = row;
-  if (s.gather) {
-    const int g = s.gather[row];
-    if (g < 0 || g >= s.gmax) return nullptr;
-    r = g;
-  }
-  return (const char*)s.p + r * s.ld * (s.bf16 ? 2 : 4);
+// Raw buffer resource over `bytes` bytes at p.  The GEMM staging reads
+// through such resources with a per-lane byte offset and a per-chunk scalar
+// offset; a lane offset of kNoLoad is past every resource (all of them stay
+// under 2 GiB, checked on the host), so that load reads zeros without
+// touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)bytes, 0x00020000);
+}
+constexpr int kNoLoad = (int)0x80000000u;
+__device__ __forceinline__ f32x4 buf_load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-// This thread's row of segment s for the GEMM main loop.  The address is
-// always loadable (row 0 of the segment's matrix stands in for a row past M
-// or an out-of-range id) and `ok` says whether the values count, so the
-// per-chunk loads need no branch.
-struct ARow {
-  const char* p;
-  bool ok;
-};
-__device__ __forceinline__ ARow seg_arow(const ASeg& s, int row, int M) {
-  const char* base = (const char*)s.p;
-  if (row >= M) return {base, false};
-  int64_t r = row;
-  if (s.gather) {
-    const int g = s.gather[row];
-    if (g < 0 || g >= s.gmax) return {base, false};
-    r = g;
-  }
-  return {base + r * s.ld * (s.bf16 ? 2 : 4), true};
+// Bytes of the matrix behind segment s (M rows, or gmax rows if gathered).
+__device__ __forceinline__ int64_t seg_bytes(const ASeg& s, int M) {
+  return (int64_t)(s.gather ? s.gmax : M) * s.ld * (s.bf16 ? 2 : 4);
 }
 
-// The raw global data behind one A vector of an ARow, for the staging:
-// one 16-byte load (fp32, or a bf16 source whose rows are padded to whole
-// vectors) or, for bf16 from an fp32 source, two (x1 past K stays zero).
-// Absent rows and columns leave zeros.  Nothing here consumes the loaded
-// values, so the loads stay in flight until the values are stored to LDS
-// (a conversion at load time would make the compiler wait for them here).
+// Byte offset of this thread's row of segment s, or kNoLoad for a row past
+// M or an out-of-range id (a zero row).
+__device__ __forceinline__ int seg_row_off(const ASeg& s, int row, int M) {
+  if (row >= M) return kNoLoad;
+  int r = row;
+  if (s.gather) {
+    r = s.gather[row];
+    if (r < 0 || r >= s.gmax) return kNoLoad;
+  }
+  return (int)((int64_t)r * s.ld * (s.bf16 ? 2 : 4));
+}
+
+// The raw data behind one A vector for the staging: one 16-byte load (fp32,
+// or a bf16 source whose rows are padded to whole vectors) or, for bf16 from
+// an fp32 source, two.  `roff` is the row's byte offset, `k` the vector's
+// column and `soff` the chunk's scalar byte offset (its column times the
+// element size, already part of k).  Absent rows and columns read zeros.
+// Every call issues the same loads whatever the data, so the compiler can
+// count the loads in flight exactly, and nothing consumes the values until
+// they are stored to LDS.
 template <class P, bool SRC16>
-__device__ __forceinline__ void load_a_raw(const ARow& r, int K, int k, f32x4& x0, f32x4& x1) {
-  x0 = zero4();
-  x1 = zero4();
-  const bool in = r.ok && k < K;
-  if constexpr (P::kBF16) {
-    if constexpr (SRC16) {
-      if (in) x0 = *(const f32x4*)(r.p + 2 * (int64_t)k);
-    } else {
-      const float* f = (const float*)r.p;
-      if (in) x0 = *(const f32x4*)(f + k);
-      if (in && k + 4 < K) x1 = *(const f32x4*)(f + k + 4);
-    }
-  } else {
-    if (in) x0 = *(const f32x4*)((const float*)r.p + k);
-  }
+__device__ __forceinline__ void load_a_raw(__amdgpu_buffer_rsrc_t res, int roff, int K, int k, int kin, int soff,
+                                           f32x4& x0, f32x4& x1) {
+  // kin: the vector's column within the chunk (k = chunk column + kin)
+  const int o = roff + kin * (P::kBF16 && SRC16 ? 2 : 4);
+  x0 = buf_load(res, k < K ? o : kNoLoad, soff);
+  if constexpr (P::kBF16 && !SRC16) x1 = buf_load(res, k + 4 < K ? o + 16 : kNoLoad, soff);
 }
 
 // The A vector from load_a_raw's data, in precision P.
@@ -270,24 +261,30 @@ struct Stager {
   __device__ static __forceinline__ int a_row(int i) { return ((int)threadIdx.x + i * NT) / KQ; }
   __device__ static __forceinline__ int a_vec(int i) { return ((int)threadIdx.x + i * NT) % KQ; }
 
-  // arow[i]: segment row of this thread's i-th A vector; kseg: k offset of
-  // the chunk within the segment; vq_glob: chunk start in packed-weight
-  // vector rows.  Weights first: their loads carry no condition.
-  __device__ __forceinline__ void load(const ARow (&arow)[NA], int segK, int kseg, const f32x4* __restrict__ Wp,
-                                       int64_t Npad, int64_t vq_glob, int n0) {
-    const int tid = threadIdx.x;
+  // aoff[i]: byte offset of the row of this thread's i-th A vector in the
+  // segment's resource; kseg: k offset of the chunk within the segment;
+  // bvo[i]: byte offset of its i-th B vector within a chunk of the packed
+  // weights, whose chunk starts at scalar offset bsoff.  Weights first:
+  // their loads carry no condition.
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t ares, const int (&aoff)[NA], int segK, int kseg,
+                                       __amdgpu_buffer_rsrc_t bres, const int (&bvo)[NB], int bsoff) {
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int idx = tid + i * NT;
-      const int n = idx % TN, kq = idx / TN;
-      rb[i] = Wp[(vq_glob + kq) * Npad + n0 + n];
-    }
+    for (int i = 0; i < NB; ++i) rb[i] = buf_load(bres, bvo[i], bsoff);
+    const int asoff = kseg * (P::kBF16 && SRC16 ? 2 : 4);
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       f32x4 x1;
-      load_a_raw<P, SRC16>(arow[i], segK, kseg + P::KV * a_vec(i), ra[i], x1);
+      const int kin = P::KV * a_vec(i);
+      load_a_raw<P, SRC16>(ares, aoff[i], segK, kseg + kin, kin, asoff, ra[i], x1);
       if constexpr (kTwo) rx[i] = x1;
     }
+  }
+
+  // Byte offset of this thread's i-th B vector within a chunk.
+  __device__ static __forceinline__ int b_off(int i, int64_t Npad, int n0) {
+    const int idx = (int)threadIdx.x + i * NT;
+    const int n = idx % TN, kq = idx / TN;
+    return (int)(((int64_t)kq * Npad + n0 + n) * 16);
   }
 
   __device__ __forceinline__ void store(f32x4* As, f32x4* Bs) const {
@@ -342,15 +339,23 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
   const int n = ce - cb;
   if (n <= 0) return;
   St st[LA];
-  ARow arow[St::NA];
+  // the segment's A rows and its packed weights (vector rows vq0 ..), each
+  // through a buffer resource
+  const __amdgpu_buffer_rsrc_t ares = buffer_rsrc(sg.p, seg_bytes(sg, M));
+  const __amdgpu_buffer_rsrc_t bres = buffer_rsrc(Wp + vq0 * Npad, (int64_t)sg.nchunk * KQ * Npad * 16);
+  int aoff[St::NA], bvo[St::NB];
 #pragma unroll
-  for (int i = 0; i < St::NA; ++i) arow[i] = seg_arow(sg, m0 + St::a_row(i), M);
+  for (int i = 0; i < St::NA; ++i) aoff[i] = seg_row_off(sg, m0 + St::a_row(i), M);
+#pragma unroll
+  for (int i = 0; i < St::NB; ++i) bvo[i] = St::b_off(i, Npad, n0);
+  // Loads are unconditional: past the segment's last chunk they re-read it,
+  // so every iteration issues the same loads and the waits before the
+  // stores count them exactly.
   auto load = [&](St& s, int i) {
-    s.load(arow, sg.K, (cb + i) * P::KC, Wp, Npad, vq0 + (int64_t)(cb + i) * KQ, n0);
+    const int c = cb + (i < n ? i : n - 1);
+    s.load(ares, aoff, sg.K, c * P::KC, bres, bvo, (int)((int64_t)c * KQ * Npad * 16));
   };
-  static_for<LA>([&](auto j) {
-    if (j < n) load(st[j], j);
-  });
+  static_for<LA>([&](auto j) { load(st[j], j); });
   st[0].store(lds, lds + ASZ);
   __syncthreads();
   for (int i0 = 0; i0 < n; i0 += LA) {
@@ -359,7 +364,11 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
       const int i = i0 + j;
       if (i < n) {
         const int cur = (i & 1) * STG, nxt = STG - cur;
-        if (i + LA < n) load(st[j], i + LA);
+        load(st[j], i + LA);
+        // keep the loads ahead of the compute: scheduled after it, their
+        // registers get reused by the fragment reads, whose writes must then
+        // wait for the loads at the next iteration
+        __builtin_amdgcn_sched_barrier(0);
         compute(lds + cur, lds + cur + ASZ);
         if (i + 1 < n) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
         __syncthreads();

@@ -136,17 +136,23 @@ hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi
   return hipGetLastError();
 }
 
-// The main loop loads every segment's row 0 in place of absent rows, so each
-// segment with work needs a matrix behind it.
-static bool segments_loadable(const AOperand& A) {
-  for (int i = 0; i < A.nseg; ++i)
-    if (A.seg[i].nchunk > 0 && (!A.seg[i].p || (A.seg[i].gather && A.seg[i].gmax < 1))) return false;
-  return true;
+// Each segment with work needs a matrix behind it, and the staging
+// addresses the segments and the packed weights with 32-bit byte offsets.
+static bool segments_loadable(const AOperand& A, int64_t Npad) {
+  int64_t chunks = 0;
+  for (int i = 0; i < A.nseg; ++i) {
+    const ASeg& s = A.seg[i];
+    if (s.nchunk <= 0) continue;
+    if (!s.p || (s.gather && s.gmax < 1)) return false;
+    if ((int64_t)(s.gather ? s.gmax : A.M) * s.ld * (s.bf16 ? 2 : 4) >= ((int64_t)1 << 31)) return false;
+    chunks += s.nchunk;
+  }
+  return chunks * KQ * Npad * 16 < ((int64_t)1 << 31);
 }
 
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
   if (A.M <= 0 || ep.N <= 0) return hipSuccess;
-  if (!segments_loadable(A)) return hipErrorInvalidValue;
+  if (!segments_loadable(A, W.Npad)) return hipErrorInvalidValue;
   return W.bf16 ? gemm_plain<PrecBF16>(t, A, W, ep, st) : gemm_plain<PrecF32>(t, A, W, ep, st);
 }
 
@@ -250,7 +256,7 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   for (int i = 1; i < nprob; ++i) M = M > probs[i].A.M ? M : probs[i].A.M;
   if (M <= 0) return hipSuccess;
   for (int i = 0; i < nprob; ++i)
-    if (!segments_loadable(probs[i].A)) return hipErrorInvalidValue;
+    if (!segments_loadable(probs[i].A, probs[i].Npad)) return hipErrorInvalidValue;
   dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
   constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
   if (bf16)
