@@ -216,35 +216,62 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
 
   const GruEpi& ep = Pb.ep;
   const int h = lane >> 5, l32 = lane & 31;
-  const int H = ep.H;
+  const int H = ep.H, M = Pb.A.M;
   const int j = blockIdx.y * HB + wu0 + l32;
   if (j >= H) return;
   const float br = ep.brz[j], bz = ep.brz[H + j], bni = ep.bni[j], bns = ep.bns[j];
+  // The cell's other inputs for this lane's FM*16 rows, every load issued
+  // before any value is used (addresses clamped to row 0 where a row is
+  // absent), so the epilogue waits for memory once or twice instead of once
+  // per row.
+  constexpr int NR = FM * 16;
+  int rowq[NR];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int q = 0; q < NR; ++q) rowq[q] = m0 + wm0 + 32 * (q / 16) + acc_row(q % 16, h);
+  auto clamp_row = [&](int row) { return row < M ? row : 0; };
+  float hp[NR], xr[NR], xz[NR], xn[NR];
+  bool keep[NR];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm0 + 32 * i + acc_row(r, h);
-      if (row >= Pb.A.M) continue;
-      float xr = 0.f, xz = 0.f, xn = 0.f;
-      if (ep.xin) {
-        const float* x = ep.xin + (int64_t)row * ep.ldx;
-        xr = x[j];
-        xz = x[H + j];
-        xn = x[2 * H + j];
-      }
-      float hp = 0.f;
-      if (ep.h) {
-        const int hr = ep.hrow ? ep.hrow[row] : row;
-        if (!ep.hrow || (hr >= 0 && hr < ep.hrows)) hp = ep.h[(int64_t)hr * ep.ldh + j];
-      }
-      const float rg = sigmoidf_(ar[i][r] + br + xr);
-      const float zg = sigmoidf_(az[i][r] + bz + xz);
-      const float ng = tanhf(ani[i][r] + bni + xn + rg * (ans[i][r] + bns));
-      float hn = zg * hp + (1.f - zg) * ng;
-      if (ep.mask_len && ep.mask_pos >= ep.mask_len[row]) hn = 0.f;
-      ep.out[(int64_t)row * ep.ldo + j] = hn;
+  for (int q = 0; q < NR; ++q) {
+    hp[q] = xr[q] = xz[q] = xn[q] = 0.f;
+    keep[q] = true;
+  }
+  if (ep.h) {
+    int hr[NR];
+    bool hok[NR];
+#pragma unroll
+    for (int q = 0; q < NR; ++q) hr[q] = ep.hrow ? ep.hrow[clamp_row(rowq[q])] : clamp_row(rowq[q]);
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      hok[q] = !ep.hrow || (hr[q] >= 0 && hr[q] < ep.hrows);
+      hp[q] = ep.h[(int64_t)(hok[q] ? hr[q] : 0) * ep.ldh + j];
     }
+#pragma unroll
+    for (int q = 0; q < NR; ++q) hp[q] = hok[q] ? hp[q] : 0.f;
+  }
+  if (ep.xin) {
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      const float* x = ep.xin + (int64_t)clamp_row(rowq[q]) * ep.ldx;
+      xr[q] = x[j];
+      xz[q] = x[H + j];
+      xn[q] = x[2 * H + j];
+    }
+  }
+  if (ep.mask_len) {
+#pragma unroll
+    for (int q = 0; q < NR; ++q) keep[q] = ep.mask_pos < ep.mask_len[clamp_row(rowq[q])];
+  }
+#pragma unroll
+  for (int q = 0; q < NR; ++q) {
+    const int i = q / 16, r = q % 16;
+    const float rg = sigmoidf_(ar[i][r] + br + xr[q]);
+    const float zg = sigmoidf_(az[i][r] + bz + xz[q]);
+    const float ng = tanhf(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
+    float hn = zg * hp[q] + (1.f - zg) * ng;
+    if (!keep[q]) hn = 0.f;
+    if (rowq[q] < M) ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
+  }
 }
 
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st) {
