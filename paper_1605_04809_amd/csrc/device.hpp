@@ -358,23 +358,32 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
   static_for<LA>([&](auto j) { load(st[j], j); });
   st[0].store(lds, lds + ASZ);
   __syncthreads();
-  for (int i0 = 0; i0 < n; i0 += LA) {
-    static_for<LA>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;  // this iteration's register set
-      const int i = i0 + j;
-      if (i < n) {
-        const int cur = (i & 1) * STG, nxt = STG - cur;
-        load(st[j], i + LA);
-        // keep the loads ahead of the compute: scheduled after it, their
-        // registers get reused by the fragment reads, whose writes must then
-        // wait for the loads at the next iteration
-        __builtin_amdgcn_sched_barrier(0);
-        compute(lds + cur, lds + cur + ASZ);
-        if (i + 1 < n) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
-        __syncthreads();
-      }
-    });
-  }
+  // One step: chunk i's loads went out LA steps ago into register set j; it
+  // is computed from LDS stage i % 2 while chunk i + 1 is stored to the
+  // other stage.
+  auto step = [&](int i, auto jc, bool store_next) {
+    constexpr int j = decltype(jc)::value;  // this step's register set
+    const int cur = (i & 1) * STG, nxt = STG - cur;
+    load(st[j], i + LA);
+    // keep the loads ahead of the compute: scheduled after it, their
+    // registers get reused by the fragment reads, whose writes must then
+    // wait for the loads at the next step
+    __builtin_amdgcn_sched_barrier(0);
+    compute(lds + cur, lds + cur + ASZ);
+    if (store_next) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
+    __syncthreads();
+  };
+  // Whole groups of LA steps with every store unconditional (the last step
+  // of the segment stores a re-read chunk that nobody reads), so no path
+  // round the loop skips the waits that retire a register set's loads; a
+  // skipped store on such a path made the compiler wait for all loads in
+  // flight at the top of every step.  The remaining steps follow.
+  int i0 = 0;
+  for (; i0 + LA <= n; i0 += LA) static_for<LA>([&](auto jc) { step(i0 + decltype(jc)::value, jc, true); });
+  static_for<LA - 1>([&](auto jc) {
+    const int i = i0 + decltype(jc)::value;
+    if (i < n) step(i, jc, i + 1 < n);
+  });
 }
 
 // gemm_segment_t with the segment's element type fixed at compile time (a
