@@ -220,57 +220,59 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   const int j = blockIdx.y * HB + wu0 + l32;
   if (j >= H) return;
   const float br = ep.brz[j], bz = ep.brz[H + j], bni = ep.bni[j], bns = ep.bns[j];
-  // The cell's other inputs for this lane's FM*16 rows, every load issued
-  // before any value is used (addresses clamped to row 0 where a row is
-  // absent), so the epilogue waits for memory once or twice instead of once
-  // per row.
-  constexpr int NR = FM * 16;
-  int rowq[NR];
-#pragma unroll
-  for (int q = 0; q < NR; ++q) rowq[q] = m0 + wm0 + 32 * (q / 16) + acc_row(q % 16, h);
+  // The cell's other inputs for this lane's rows, 8 rows at a time, every
+  // load of a group issued before any value is used (addresses clamped to
+  // row 0 where a row is absent), so the epilogue waits for memory a few
+  // times per group instead of once per row.
+  constexpr int NG = 8;
   auto clamp_row = [&](int row) { return row < M ? row : 0; };
-  float hp[NR], xr[NR], xz[NR], xn[NR];
-  bool keep[NR];
 #pragma unroll
-  for (int q = 0; q < NR; ++q) {
-    hp[q] = xr[q] = xz[q] = xn[q] = 0.f;
-    keep[q] = true;
-  }
-  if (ep.h) {
-    int hr[NR];
-    bool hok[NR];
+  for (int g0 = 0; g0 < FM * 16; g0 += NG) {
+    int rowq[NG];
+    float hp[NG], xr[NG], xz[NG], xn[NG];
+    bool keep[NG];
 #pragma unroll
-    for (int q = 0; q < NR; ++q) hr[q] = ep.hrow ? ep.hrow[clamp_row(rowq[q])] : clamp_row(rowq[q]);
+    for (int q = 0; q < NG; ++q) {
+      rowq[q] = m0 + wm0 + 32 * ((g0 + q) / 16) + acc_row((g0 + q) % 16, h);
+      hp[q] = xr[q] = xz[q] = xn[q] = 0.f;
+      keep[q] = true;
+    }
+    if (ep.h) {
+      int hr[NG];
+      bool hok[NG];
 #pragma unroll
-    for (int q = 0; q < NR; ++q) {
-      hok[q] = !ep.hrow || (hr[q] >= 0 && hr[q] < ep.hrows);
-      hp[q] = ep.h[(int64_t)(hok[q] ? hr[q] : 0) * ep.ldh + j];
+      for (int q = 0; q < NG; ++q) hr[q] = ep.hrow ? ep.hrow[clamp_row(rowq[q])] : clamp_row(rowq[q]);
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        hok[q] = !ep.hrow || (hr[q] >= 0 && hr[q] < ep.hrows);
+        hp[q] = ep.h[(int64_t)(hok[q] ? hr[q] : 0) * ep.ldh + j];
+      }
+#pragma unroll
+      for (int q = 0; q < NG; ++q) hp[q] = hok[q] ? hp[q] : 0.f;
+    }
+    if (ep.xin) {
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        const float* x = ep.xin + (int64_t)clamp_row(rowq[q]) * ep.ldx;
+        xr[q] = x[j];
+        xz[q] = x[H + j];
+        xn[q] = x[2 * H + j];
+      }
+    }
+    if (ep.mask_len) {
+#pragma unroll
+      for (int q = 0; q < NG; ++q) keep[q] = ep.mask_pos < ep.mask_len[clamp_row(rowq[q])];
     }
 #pragma unroll
-    for (int q = 0; q < NR; ++q) hp[q] = hok[q] ? hp[q] : 0.f;
-  }
-  if (ep.xin) {
-#pragma unroll
-    for (int q = 0; q < NR; ++q) {
-      const float* x = ep.xin + (int64_t)clamp_row(rowq[q]) * ep.ldx;
-      xr[q] = x[j];
-      xz[q] = x[H + j];
-      xn[q] = x[2 * H + j];
+    for (int q = 0; q < NG; ++q) {
+      const int i = (g0 + q) / 16, r = (g0 + q) % 16;
+      const float rg = sigmoidf_(ar[i][r] + br + xr[q]);
+      const float zg = sigmoidf_(az[i][r] + bz + xz[q]);
+      const float ng = tanhf(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
+      float hn = zg * hp[q] + (1.f - zg) * ng;
+      if (!keep[q]) hn = 0.f;
+      if (rowq[q] < M) ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
     }
-  }
-  if (ep.mask_len) {
-#pragma unroll
-    for (int q = 0; q < NR; ++q) keep[q] = ep.mask_pos < ep.mask_len[clamp_row(rowq[q])];
-  }
-#pragma unroll
-  for (int q = 0; q < NR; ++q) {
-    const int i = q / 16, r = q % 16;
-    const float rg = sigmoidf_(ar[i][r] + br + xr[q]);
-    const float zg = sigmoidf_(az[i][r] + bz + xz[q]);
-    const float ng = tanhf(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
-    float hn = zg * hp[q] + (1.f - zg) * ng;
-    if (!keep[q]) hn = 0.f;
-    if (rowq[q] < M) ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
   }
 }
 
