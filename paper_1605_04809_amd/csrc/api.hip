@@ -179,10 +179,11 @@ hipError_t upload_table(Allocs& mem, void** d, const float* h, int64_t rows, int
   return upload_w(mem, d, padded, true);
 }
 
-hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int N, int TN, int kc, bool bf16) {
+hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int N, int TN, int kc, bool bf16,
+                      int spare = 0) {
   P->N = N;
   P->bf16 = bf16;
-  P->Npad = round_up(N, TN);
+  P->Npad = round_up(N, TN) + spare;
   std::vector<float> h =
       pack_host(segs, P->Npad, kc, bf16 ? 8 : 4, [N](int64_t np) { return np < N ? (int)np : -1; }, &P->Kpad);
   return upload_w(mem, &P->d, h, bf16);
@@ -297,7 +298,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * 2 * d.H * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.nS = vocab_slices((int)B, m->out.Npad, m->bf16);
+  L.nS = vocab_slices((int)B, m->dims.V, m->bf16);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
@@ -376,7 +377,8 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)) > vocab_max_kpad(bf16))
     return fail(NMT_EINVAL, "E must be at most %d for this weight type",
                 vocab_max_kpad(bf16) - vocab_bias_rows(bf16));
-  if (!vocab_offsets_fit(round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)), round_up(d.V, kVocabTN), bf16))
+  if (!vocab_offsets_fit(round_up(d.E + vocab_bias_rows(bf16), chunk_k(bf16)), round_up(d.V, kVocabTN) + kVocabSpare,
+                         bf16))
     return fail(NMT_EINVAL, "the packed output weights (E x V) must stay under 2 GiB");
   const float* const* wp = (const float* const*)w;
   for (size_t i = 0; i < sizeof(nmt_weights) / sizeof(float*); ++i)
@@ -445,7 +447,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
       }
     }
     Seg sg{w->out_W, E, V, brows.data(), nb};
-    step(pack_plain(m->mem, &m->out, {sg}, V, kVocabTN, kc, bf16));
+    step(pack_plain(m->mem, &m->out, {sg}, V, kVocabTN, kc, bf16, kVocabSpare));
     m->out.Krows = E;
     m->out.nbias = nb;
   }

@@ -27,6 +27,7 @@ constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
 #endif
 constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
+constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 
 // A weight matrix packed for one kernel family: [Kpad/KV][Npad][KV] of fp32
 // (KV = 4) or bf16 (KV = 8), 16 bytes per (vector row, column).
@@ -91,7 +92,7 @@ hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const P
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
-int vocab_slices(int M, int64_t Npad, bool bf16);
+int vocab_slices(int M, int V, bool bf16);
 int vocab_max_kpad(bool bf16);
 bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,

@@ -400,8 +400,10 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   }
   __syncthreads();
 
-  // This slice's 32-column blocks, balanced over the slices, in groups of VFN.
-  const int NB = (int)(Npad / 32);
+  // This slice's 32-column blocks, balanced over the slices, in groups of VFN
+  // (the packed matrix has one more, all zero, past the last one with
+  // columns below V).
+  const int NB = (V + 31) / 32;
   const int cb_begin = (int)((int64_t)NB * slice / nS), cb_end = (int)((int64_t)NB * (slice + 1) / nS);
   const int ngrp = (cb_end - cb_begin + VFN - 1) / VFN;
   const int NKG = KQ / 2;  // k groups per column block (a multiple of VPF)
@@ -590,10 +592,10 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   }
 }
 
-int vocab_slices(int M, int64_t Npad, bool bf16) {
+int vocab_slices(int M, int V, bool bf16) {
   const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
   int nS = 8 * ceil_div(ceil_div(256, nM), 8);  // fill the 256 CUs (one block per CU)
-  const int NB = (int)(Npad / 32);
+  const int NB = (V + 31) / 32;
   while (nS > 8 && nS > NB) nS -= 8;
   return nS;
 }
@@ -636,7 +638,8 @@ hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, int V, float
 hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
                             hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1) return hipErrorInvalidValue;
+  if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1 || W.Npad < ((int64_t)V + 31) / 32 * 32 + 32)
+    return hipErrorInvalidValue;
   if (!vocab_offsets_fit(W.Kpad, W.Npad, W.bf16)) return hipErrorInvalidValue;
   return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, V, part, nS, st) : vocab_lse<PrecF32>(t, M, E, W, V, part, nS, st);
 }
