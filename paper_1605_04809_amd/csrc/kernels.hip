@@ -731,11 +731,16 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
 
 // ------------------------------------------------------------ attention
 
-// tanh x = 1 - 2 / (e^{2x} + 1), with the hardware base-2 exponential and
-// reciprocal: about 1e-7 absolute error, saturating to +-1 for large |x|.
-__device__ __forceinline__ float tanh_fast(float x) {
-  const float ex = __builtin_amdgcn_exp2f(x * (2.f * kLog2e));
-  return 1.f - 2.f * __builtin_amdgcn_rcpf(ex + 1.f);
+// Attention scores.  With tanh x = 1 - 2 / (e^{2x} + 1),
+//   e_i = v . tanh(k_i + q) = sum(v) + sum_a (-2 v_a) / (2^(k_ia c + q_a c) + 1),  c = 2 log2(e),
+// and the softmax over i ignores the constant sum(v), so the kernels score
+//   e'_i = sum_a w_a / (2^(k_ia c + q'_a) + 1)   with w = -2 v and q' = c q:
+// one fma, the hardware exp2, one add, the hardware reciprocal and one fma
+// per term (the reciprocal is about 1 ulp; the result saturates correctly
+// for large |x|).
+constexpr float kTanhScale = 2.f * kLog2e;
+__device__ __forceinline__ float score_term(float k, float qs, float w, float acc) {
+  return fmaf(w, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(fmaf(k, kTanhScale, qs)) + 1.f), acc);
 }
 
 // Fallback for more sentences than the grouping kernel counts: one block
@@ -764,12 +769,12 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
   }
   const int L = len[s];
   const int A4 = A / 4;
-  f32x4 qv[NQ], vv[NQ];
+  f32x4 qv[NQ], vv[NQ];  // scaled query c q and weights -2 v (see score_term)
 #pragma unroll
   for (int k = 0; k < NQ; ++k) {
     const int a4 = lane + 64 * k;
-    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) : zero4();
-    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) : zero4();
+    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) * kTanhScale : zero4();
+    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
   }
   const float* P = pctx + (int64_t)s * Tpad * A;
   for (int i = wave; i < L; i += 4) {
@@ -779,8 +784,8 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
       const int a4 = lane + 64 * k;
       if (a4 < A4) {
         const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
-        acc += vv[k][0] * tanh_fast(p[0] + qv[k][0]) + vv[k][1] * tanh_fast(p[1] + qv[k][1]) +
-               vv[k][2] * tanh_fast(p[2] + qv[k][2]) + vv[k][3] * tanh_fast(p[3] + qv[k][3]);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) acc = score_term(p[x], qv[k][x], vv[k][x], acc);
       }
     }
     acc = wave_sum(acc);
@@ -931,15 +936,16 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
     }
     return;
   }
+  // scaled queries c q in LDS and weights -2 v in registers (see score_term)
   for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
     const int g = idx / A4, a4 = idx - g * A4;
-    qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+    qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) * kTanhScale : zero4();
   }
   f32x4 vv[NQ];
 #pragma unroll
   for (int k = 0; k < NQ; ++k) {
     const int a4 = lane + 64 * k;
-    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) : zero4();
+    vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
   }
   __syncthreads();
   const int L = len[s];
@@ -956,8 +962,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           const f32x4 qq = qs[g * A4 + a4];
-          acc[g] += vv[k][0] * tanh_fast(p[0] + qq[0]) + vv[k][1] * tanh_fast(p[1] + qq[1]) +
-                    vv[k][2] * tanh_fast(p[2] + qq[2]) + vv[k][3] * tanh_fast(p[3] + qq[3]);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) acc[g] = score_term(p[x], qq[x], vv[k][x], acc[g]);
         }
       }
     }
