@@ -829,29 +829,60 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
 // sentence and reads that sentence's keys and annotations once for all of
 // them.  k_group_rows (one block) counts the rows of each sentence in LDS
 // (rows with an invalid sentence id go to an extra bucket, scored as zeros),
-// lists the rows sentence by sentence in perm, and cuts each sentence's rows
-// into tiles (sentence or -1, first index into perm, row count).  The order
-// of rows inside a sentence does not matter: each row's arithmetic is the
-// same in any tile.
+// orders the sentences longest first, lists the rows sentence by sentence
+// in that order in perm, and cuts each sentence's rows into tiles (sentence
+// or -1, first index into perm, row count).  A tile's work grows with its
+// sentence's length, and the blocks are dispatched in tile order, so the
+// longest tiles start first and the short ones fill the slots that free up
+// (a sentence-order list left a second round of a few long tiles).  The
+// order of rows inside a sentence does not matter: each row's arithmetic is
+// the same in any tile.
 __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const int32_t* __restrict__ sent_id,
+                                                     const int32_t* __restrict__ len, int Tpad,
                                                      int32_t* __restrict__ perm, int4* __restrict__ tiles,
                                                      int32_t* __restrict__ n_tiles) {
-  __shared__ int cnt[kGroupMaxS + 1];
+  __shared__ int cnt[kGroupMaxS + 1];    // rows per bucket, then the bucket's write cursor
+  __shared__ int order[kGroupMaxS + 1];  // buckets longest sentence first, the invalid bucket last
+  __shared__ int keyc[kMaxTpad + 2];     // buckets per key, then the key's write cursor
   __shared__ int part[2][1024];
-  const int tid = threadIdx.x, NB = S + 1;
+  const int tid = threadIdx.x, NB = S + 1, NK = Tpad + 1;
   for (int i = tid; i < NB; i += 1024) cnt[i] = 0;
+  for (int k = tid; k < NK; k += 1024) keyc[k] = 0;
   __syncthreads();
   for (int b = tid; b < B; b += 1024) {
     const int s = sent_id[b];
     atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1);
   }
+  // key of bucket i: Tpad - length (0 for the longest); the invalid bucket sorts last
+  auto key = [&](int i) { return i < S ? Tpad - min(max(len[i], 0), Tpad) : Tpad; };
+  for (int i = tid; i < NB; i += 1024) atomicAdd(&keyc[key(i)], 1);
   __syncthreads();
-  // exclusive scans of the row and tile counts; thread tid owns buckets [lo, hi)
+  // exclusive scan of the key counts (NK <= 1025: thread t owns keys [2t, 2t+2))
+  {
+    const int k0 = 2 * tid, k1 = k0 + 1;
+    const int c0 = k0 < NK ? keyc[k0] : 0, c1 = k1 < NK ? keyc[k1] : 0;
+    part[0][tid] = c0 + c1;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int a0 = tid >= o ? part[0][tid - o] : 0;
+      __syncthreads();
+      part[0][tid] += a0;
+      __syncthreads();
+    }
+    const int base = part[0][tid] - c0 - c1;
+    if (k0 < NK) keyc[k0] = base;
+    if (k1 < NK) keyc[k1] = base + c0;
+    __syncthreads();
+  }
+  for (int i = tid; i < NB; i += 1024) order[atomicAdd(&keyc[key(i)], 1)] = i;
+  __syncthreads();
+  // exclusive scans of the row and tile counts in that order; thread tid owns ranks [lo, hi)
   const int per = (NB + 1023) / 1024, lo = tid * per < NB ? tid * per : NB, hi = lo + per < NB ? lo + per : NB;
   int rs = 0, ts = 0;
-  for (int i = lo; i < hi; ++i) {
-    rs += cnt[i];
-    ts += (cnt[i] + G - 1) / G;
+  for (int j = lo; j < hi; ++j) {
+    const int n = cnt[order[j]];
+    rs += n;
+    ts += (n + G - 1) / G;
   }
   part[0][tid] = rs;
   part[1][tid] = ts;
@@ -865,8 +896,8 @@ __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const 
   }
   int roff = part[0][tid] - rs, toff = part[1][tid] - ts;
   if (tid == 1023) *n_tiles = part[1][1023];
-  for (int i = lo; i < hi; ++i) {
-    const int n = cnt[i];
+  for (int j = lo; j < hi; ++j) {
+    const int i = order[j], n = cnt[i];
     for (int k = 0; k * G < n; ++k) tiles[toff + k] = make_int4(i < S ? i : -1, roff + k * G, min(G, n - k * G), 0);
     toff += (n + G - 1) / G;
     cnt[i] = roff;  // becomes the bucket's write cursor
@@ -1027,7 +1058,8 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   }
   // rows per tile: kAttnGroup when their queries and scores fit 64 KB of LDS, else 4
   const int G = ((size_t)kAttnGroup * (A + Tpad) * 4 <= 65536) ? kAttnGroup : 4;
-  hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, grp.perm, grp.tiles, grp.n_tiles);
+  hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
+                     grp.n_tiles);
   if (G == kAttnGroup)
     attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, pctx, ctx, len, grp, S, v, c, alpha, st);
   else
