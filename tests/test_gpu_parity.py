@@ -124,9 +124,8 @@ def test_many_sentences_every_row(gpu, S):
 @pytest.mark.parametrize("V,wtype", [(1, "f32"), (2, "f32"), (33, "f32"), (1, "bf16"), (33, "bf16")])
 def test_minimal_dimensions(gpu, V, wtype):
     """Every dimension far below its tile: E = H = A = 4, one source position,
-    and vocabularies of 1, 2 and 33 words.  A single word has log p = 0; the
-    kernel's base-2 running maximum converted back to natural units costs one
-    fp32 rounding of the logit, so |log p| stays within a few ulp of it."""
+    and vocabularies of 1, 2 and 33 words.  A single word has log p = 0 up to
+    the fp32 rounding of the log-sum-exp arithmetic (a few ulp)."""
     _torch()
     cfg = Config("minimal", V=V, V_src=3, E=4, H=4, A=4, B=5, S=2, len_lo=1, len_hi=1, Tpad=1,
                  sigma_w=0.5, sigma_emb=0.5, seed=17, wtype=wtype)
@@ -138,6 +137,37 @@ def test_minimal_dimensions(gpu, V, wtype):
     compare(gr, o.step(*args), tol_logp=tol_logp, tol=tol)
     if V == 1:
         assert np.all(np.abs(gr["logp"]) <= 1e-6), gr["logp"]
+    g.close()
+
+
+@pytest.mark.parametrize("wtype,V", [("f32", 1000), ("bf16", 1000), ("bf16", 3001)])
+def test_output_bias_is_exact(gpu, wtype, V):
+    """With zero output weights every logit is its bias, so log Z is the
+    log-sum-exp of the biases and log p(w) = b_w - log Z.  The biases are
+    fp32 values far from any bf16 value (spread over 2^-8 .. 2^6): the bf16
+    path must still add each exactly (it keeps the bias as three bf16 rows,
+    hi + mid + lo), so both paths match the oracle to fp32 rounding, where a
+    bias rounded to bf16 would be off by up to |b| 2^-9 (about 0.1 here)."""
+    _torch()
+    cfg = CONFIGS["tiny"].replace(V=V, wtype=wtype, seed=23)
+    wl = make_workload(cfg)
+    rng = np.random.default_rng(29)
+    wl.params["out_W"] = np.zeros_like(wl.params["out_W"])
+    b = (rng.uniform(-1, 1, V) * np.exp2(rng.uniform(-8, 6, V))).astype(np.float32)
+    assert np.all(b.view(np.uint32) & 0xFFFF) or V < 4, "biases must not be bf16 values"
+    wl.params["out_b"] = b
+    g, o = gpu.GpuRun(wl), gpu.OracleRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    gr, orr = g.step(*args, debug=False), o.step(*args, intermediates=False)
+    b64 = b.astype(np.float64)
+    lz = b64.max() + math.log(np.exp(b64 - b64.max()).sum())
+    want = b64[wl.req] - lz
+    # fp32 rounding of values up to |120|: a few ulp, i.e. 2e-5 + 2e-7 |x|
+    tol_p, tol_z = 2e-5 + 2e-7 * np.abs(want), 2e-5 + 2e-7 * abs(lz)
+    e_z, e_p = np.abs(gr["logZ"] - lz), np.abs(gr["logp"] - want)
+    e_o = np.abs(gr["logp"] - orr["logp"])
+    print(f"{wtype} V={V}: max |dlogZ| {e_z.max():.2e} |dlogp| {e_p.max():.2e} vs oracle {e_o.max():.2e}")
+    assert np.all(e_z <= tol_z) and np.all(e_p <= tol_p) and np.all(e_o <= tol_p), (e_z, e_p, e_o)
     g.close()
 
 
