@@ -318,6 +318,16 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 #define NMT_PLAIN_LA 2
 #endif
 
+// MFMAs issued between two staging loads (measured: fp32 1, bf16 2).
+#ifndef NMT_GEMM_MFMA_PER_LOAD_F32
+#define NMT_GEMM_MFMA_PER_LOAD_F32 1
+#endif
+#ifndef NMT_GEMM_MFMA_PER_LOAD_BF16
+#define NMT_GEMM_MFMA_PER_LOAD_BF16 2
+#endif
+template <class P>
+constexpr int kMfmaPerLoad = P::kBF16 ? NMT_GEMM_MFMA_PER_LOAD_BF16 : NMT_GEMM_MFMA_PER_LOAD_F32;
+
 // Main loop over chunks [cb, ce) of one A segment (chunk indices local to
 // the segment; vq0 = packed weight vector row of the segment's chunk 0).
 // Chunk i's global loads are issued LA iterations before it is computed
@@ -365,11 +375,18 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
     constexpr int j = decltype(jc)::value;  // this step's register set
     const int cur = (i & 1) * STG, nxt = STG - cur;
     load(st[j], i + LA);
-    // keep the loads ahead of the compute: scheduled after it, their
-    // registers get reused by the fragment reads, whose writes must then
-    // wait for the loads at the next step
-    __builtin_amdgcn_sched_barrier(0);
     compute(lds + cur, lds + cur + ASZ);
+    // The loads go out one after every kMfmaPerLoad MFMAs of the compute, so
+    // a load that waits for the memory pipeline to take it (a chunk's loads
+    // are about 56 KB per CU in bf16) does not hold up the matrix cores.
+    // Left to the scheduler, the loads sank below the compute and their
+    // registers were reused by the fragment reads, whose writes then waited
+    // for the loads; issued all before the compute, their issue stalled the
+    // wave for about 480 cycles per chunk.
+    static_for<St::NB + St::NA * (St::kTwo ? 2 : 1)>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerLoad<P>, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    });
     if (store_next) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
     __syncthreads();
   };
