@@ -193,12 +193,13 @@ hipError_t pack_plain(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int 
 hipError_t pack_gru(Allocs& mem, Packed* P, const std::vector<Seg>& segs, int H, int kc, bool bf16) {
   P->N = 3 * H;
   P->bf16 = bf16;
-  P->Npad = (int64_t)ceil_div(H, kGruHB) * 3 * kGruHB;
+  const int HB = gru_hb(bf16);
+  P->Npad = (int64_t)ceil_div(H, HB) * 3 * HB;
   std::vector<float> h = pack_host(
       segs, P->Npad, kc, bf16 ? 8 : 4,
-      [H](int64_t np) {
-        const int ub = (int)(np / (3 * kGruHB)), rem = (int)(np % (3 * kGruHB));
-        const int g = rem / kGruHB, j = ub * kGruHB + rem % kGruHB;
+      [H, HB](int64_t np) {
+        const int ub = (int)(np / (3 * HB)), rem = (int)(np % (3 * HB));
+        const int g = rem / HB, j = ub * HB + rem % HB;
         return j < H ? g * H + j : -1;
       },
       &P->Kpad);

@@ -65,16 +65,19 @@ __device__ __forceinline__ f32x4 pack_bf16(const f32x4& x0, const f32x4& x1) {
   return __builtin_bit_cast(f32x4, v);
 }
 
-// Vectors per row per K chunk of the LDS-staged GEMM tiles.
-#ifndef NMT_KQ
-#define NMT_KQ 8
+// Vectors per row per K chunk of the LDS-staged GEMM tiles, per precision.
+#ifndef NMT_KQ_F32
+#define NMT_KQ_F32 8
 #endif
-constexpr int KQ = NMT_KQ;
+#ifndef NMT_KQ_BF16
+#define NMT_KQ_BF16 8
+#endif
 
 struct PrecF32 {
   static constexpr bool kBF16 = false;
-  static constexpr int KV = 4;        // k per 16-byte vector
-  static constexpr int KC = KQ * KV;  // k per chunk
+  static constexpr int KV = 4;           // k per 16-byte vector
+  static constexpr int KQ = NMT_KQ_F32;  // vectors per row per chunk
+  static constexpr int KC = KQ * KV;     // k per chunk
   __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
@@ -91,6 +94,7 @@ struct PrecF32 {
 struct PrecBF16 {
   static constexpr bool kBF16 = true;
   static constexpr int KV = 8;
+  static constexpr int KQ = NMT_KQ_BF16;
   static constexpr int KC = KQ * KV;
   __device__ static __forceinline__ void mma(const f32x4& a, const f32x4& b, f32x16& acc) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
@@ -234,12 +238,21 @@ __device__ __forceinline__ f32x4 with_bias_ones(f32x4 v, int kq, int E, int nb) 
   }
 }
 
-// Rows of an A stage in LDS: TM plus one vector of padding, so that the
-// transposed stores of the staging (consecutive lanes writing consecutive
-// vectors of one row, a stage row apart) fall in different banks.
-template <int TM>
+// An A stage in LDS is [KQ][a_rows] vectors.  The staging stores are
+// transposed (consecutive lanes write consecutive vectors of one row, a
+// stage row apart), which would put them all in the same banks.  fp32 pads
+// each vector's rows by one vector; bf16 keeps row r of vector v at row
+// r ^ a_swz(v), a permutation within each aligned block of 32 rows, so a
+// fragment's 32 rows stay 32 distinct slots (measured: the swizzle is a
+// little faster for the bf16 GRU tile, the padding for the fp32 one, whose
+// fragment reads then need no address arithmetic).
+template <int TM, class P>
 constexpr int a_rows() {
-  return TM + 1;
+  return P::kBF16 ? TM : TM + 1;
+}
+template <class P>
+__device__ __forceinline__ int a_swz(int v) {
+  return P::kBF16 ? (v & (P::KQ - 1) & 31) : 0;
 }
 
 // Global -> register -> LDS staging of one K chunk of the A and B tiles.
@@ -250,6 +263,7 @@ constexpr int a_rows() {
 // SRC16: the A segment is stored in bf16 (only with bf16 weights).
 template <int TM, int TN, int NT, class P, bool SRC16>
 struct Stager {
+  static constexpr int KQ = P::KQ;
   static constexpr int NA = TM * KQ / NT;
   static constexpr int NB = TN * KQ / NT;
   static_assert((TM * KQ) % NT == 0 && (TN * KQ) % NT == 0, "whole vectors per thread");
@@ -291,7 +305,7 @@ struct Stager {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      As[a_vec(i) * a_rows<TM>() + a_row(i)] = a_from_raw<P, SRC16>(ra[i], rx[kTwo ? i : 0]);
+      As[a_vec(i) * a_rows<TM, P>() + (a_row(i) ^ a_swz<P>(a_vec(i)))] = a_from_raw<P, SRC16>(ra[i], rx[kTwo ? i : 0]);
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int idx = tid + i * NT;
@@ -307,6 +321,12 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
   const int lane = threadIdx.x & 63;
   return S[(2 * kg + (lane >> 5)) * TROWS + r0 + (lane & 31)];
 }
+// The same from an A stage of TM rows (padded or swizzled: a_rows, a_swz).
+template <int TM, class P>
+__device__ __forceinline__ f32x4 lds_frag_a(const f32x4* S, int kg, int r0) {
+  const int lane = threadIdx.x & 63, v = 2 * kg + (lane >> 5);
+  return S[v * a_rows<TM, P>() + r0 + ((lane & 31) ^ a_swz<P>(v))];
+}
 
 // Global-load lookahead of the tile GEMMs: chunks whose loads are in
 // flight in registers while a chunk is computed from LDS (the GRU tile; the
@@ -314,9 +334,19 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 #ifndef NMT_GEMM_LA
 #define NMT_GEMM_LA 2
 #endif
+#ifndef NMT_GEMM_LA_BF16
+#define NMT_GEMM_LA_BF16 2
+#endif
 #ifndef NMT_PLAIN_LA
 #define NMT_PLAIN_LA 2
 #endif
+#ifndef NMT_PLAIN_LA_BF16
+#define NMT_PLAIN_LA_BF16 2
+#endif
+template <class P>
+constexpr int kGruLA = P::kBF16 ? NMT_GEMM_LA_BF16 : NMT_GEMM_LA;
+template <class P>
+constexpr int kPlainLA = P::kBF16 ? NMT_PLAIN_LA_BF16 : NMT_PLAIN_LA;
 
 // MFMAs issued between two staging loads (measured: fp32 1, bf16 2).
 #ifndef NMT_GEMM_MFMA_PER_LOAD_F32
@@ -328,14 +358,46 @@ __device__ __forceinline__ f32x4 lds_frag(const f32x4* S, int kg, int r0) {
 template <class P>
 constexpr int kMfmaPerLoad = P::kBF16 ? NMT_GEMM_MFMA_PER_LOAD_BF16 : NMT_GEMM_MFMA_PER_LOAD_F32;
 
+// Work of one k group of a wave's compute: kFrags fragment reads from LDS
+// and kMfma MFMAs.
+template <int FR, int MK>
+struct KgShape {
+  static constexpr int kFrags = FR, kMfma = MK;
+};
+
+// Instruction order of one chunk step with NL staging loads: the first k
+// group's fragment reads, then per k group one MFMA, the next k group's
+// fragment reads (so they land while this group's MFMAs run), and the rest
+// of the group's MFMAs with the step's loads spread among them.
+template <class KS, int NKG, int NL>
+__device__ __forceinline__ void sched_chunk_step() {
+  constexpr int FR = KS::kFrags, MK = KS::kMfma;
+  __builtin_amdgcn_sched_group_barrier(0x100, FR, 0);
+  static_for<NKG>([&](auto kc) {
+    constexpr int kg = decltype(kc)::value;
+    constexpr int nl = (kg + 1) * NL / NKG - kg * NL / NKG;  // loads placed in this k group
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (kg + 1 < NKG) __builtin_amdgcn_sched_group_barrier(0x100, FR, 0);
+    static_for<nl>([&](auto lc) {
+      constexpr int l = decltype(lc)::value;
+      constexpr int before = (l + 1) * (MK - 1) / nl - l * (MK - 1) / nl;  // MFMAs ahead of load l
+      if constexpr (before > 0) __builtin_amdgcn_sched_group_barrier(0x008, before, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    });
+    if constexpr (nl == 0 && MK > 1) __builtin_amdgcn_sched_group_barrier(0x008, MK - 1, 0);
+  });
+}
+
 // Main loop over chunks [cb, ce) of one A segment (chunk indices local to
 // the segment; vq0 = packed weight vector row of the segment's chunk 0).
+// KS (a KgShape, or void) describes the compute's k groups for the
+// instruction order of a step (sched_chunk_step).
 // Chunk i's global loads are issued LA iterations before it is computed
 // (into register set i % LA), it is stored to LDS stage i % 2 at the end of
 // iteration i - 1, and `compute(As, Bs)` runs on it at iteration i.  The
 // loop is unrolled by LA so register sets are picked at compile time.  Ends
 // with a barrier, so a following call may reuse the LDS stages.
-template <int TM, int TN, int NT, class P, bool SRC16, int LA, class Compute>
+template <int TM, int TN, int NT, class P, bool SRC16, int LA, class KS, class Compute>
 __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
                                                int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
                                                int ce) {
@@ -344,7 +406,8 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
   // pointers hides the LDS address space from the compiler, which then emits
   // flat loads that share the global-load counter, so every fragment wait
   // would also wait for the next chunk's prefetch.
-  constexpr int ASZ = a_rows<TM>() * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
+  constexpr int KQ = P::KQ;
+  constexpr int ASZ = a_rows<TM, P>() * KQ, BSZ = TN * KQ, STG = ASZ + BSZ;  // vectors per stage
   using St = Stager<TM, TN, NT, P, SRC16>;
   const int n = ce - cb;
   if (n <= 0) return;
@@ -376,17 +439,23 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
     const int cur = (i & 1) * STG, nxt = STG - cur;
     load(st[j], i + LA);
     compute(lds + cur, lds + cur + ASZ);
-    // The loads go out one after every kMfmaPerLoad MFMAs of the compute, so
-    // a load that waits for the memory pipeline to take it (a chunk's loads
-    // are about 56 KB per CU in bf16) does not hold up the matrix cores.
-    // Left to the scheduler, the loads sank below the compute and their
-    // registers were reused by the fragment reads, whose writes then waited
-    // for the loads; issued all before the compute, their issue stalled the
-    // wave for about 480 cycles per chunk.
-    static_for<St::NB + St::NA * (St::kTwo ? 2 : 1)>([&](auto) {
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerLoad<P>, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    });
+    // The loads go out spread among the compute's MFMAs, so a load that
+    // waits for the memory pipeline to take it (a chunk's loads are about
+    // 56 KB per CU in bf16) does not hold up the matrix cores.  Left to the
+    // scheduler, the loads sank below the compute and their registers were
+    // reused by the fragment reads, whose writes then waited for the loads;
+    // issued all before the compute, their issue stalled the wave for about
+    // 480 cycles per chunk.  With a k-group shape KS, each k group's
+    // fragment reads are also issued during the previous k group's MFMAs
+    // (otherwise each read lands just before the MFMA that waits for it).
+    if constexpr (!std::is_void_v<KS>) {
+      sched_chunk_step<KS, P::KQ / 2, St::NB + St::NA * (St::kTwo ? 2 : 1)>();
+    } else {
+      static_for<St::NB + St::NA * (St::kTwo ? 2 : 1)>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerLoad<P>, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      });
+    }
     if (store_next) st[(j + 1) % LA].store(lds + nxt, lds + nxt + ASZ);
     __syncthreads();
   };
@@ -406,23 +475,23 @@ __device__ __forceinline__ void gemm_segment_t(const ASeg& sg, int M, const f32x
 // gemm_segment_t with the segment's element type fixed at compile time (a
 // runtime choice between the two load paths made the compiler issue both
 // into the same registers, each waiting for the other).
-template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class Compute>
+template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class KS = void, class Compute>
 __device__ __forceinline__ void gemm_segment(const ASeg& sg, int M, const f32x4* __restrict__ Wp, int64_t Npad,
                                              int m0, int n0, f32x4* lds, Compute&& compute, int64_t vq0, int cb,
                                              int ce) {
   if constexpr (P::kBF16) {
     if (sg.bf16) {
-      gemm_segment_t<TM, TN, NT, P, true, LA>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
+      gemm_segment_t<TM, TN, NT, P, true, LA, KS>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
       return;
     }
   }
-  gemm_segment_t<TM, TN, NT, P, false, LA>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
+  gemm_segment_t<TM, TN, NT, P, false, LA, KS>(sg, M, Wp, Npad, m0, n0, lds, compute, vq0, cb, ce);
 }
 
 // All segments of A, restricted to global chunks [c_begin, c_end) (chunk c
 // covers packed weight vector rows KQ*c .. KQ*c+KQ-1, whichever segment it
 // falls in).
-template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class Compute>
+template <int TM, int TN, int NT, class P, int LA = NMT_GEMM_LA, class KS = void, class Compute>
 __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __restrict__ Wp, int64_t Npad, int m0,
                                               int n0, f32x4* lds, Compute&& compute, int c_begin = 0,
                                               int c_end = 1 << 30) {
@@ -431,7 +500,8 @@ __device__ __forceinline__ void gemm_mainloop(const AOperand& A, const f32x4* __
     const ASeg sg = seg_at(A, i);
     const int s1 = s0 + sg.nchunk;
     const int cb = c_begin > s0 ? c_begin : s0, ce = c_end < s1 ? c_end : s1;
-    gemm_segment<TM, TN, NT, P, LA>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * KQ, cb - s0, ce - s0);
+    gemm_segment<TM, TN, NT, P, LA, KS>(sg, A.M, Wp, Npad, m0, n0, lds, compute, (int64_t)s0 * P::KQ, cb - s0,
+                                        ce - s0);
     s0 = s1;
   }
 }

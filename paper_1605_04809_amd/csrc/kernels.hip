@@ -31,7 +31,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
                                                                            int64_t Npad, PlainEpi ep) {
   constexpr int NT = (TM / WM) * (TN / WN) * 64;
   constexpr int FM = WM / 32, FN = WN / 32;
-  __shared__ f32x4 lds[2 * (a_rows<TM>() + TN) * KQ];
+  __shared__ f32x4 lds[2 * (a_rows<TM, P>() + TN) * P::KQ];
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm0 = (wave % (TM / WM)) * WM, wn0 = (wave / (TM / WM)) * WN;
@@ -47,14 +47,18 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
     c_begin = (int)((int64_t)nc * blockIdx.z / ep.ksplit);
     c_end = (int)((int64_t)nc * (blockIdx.z + 1) / ep.ksplit);
   }
-  gemm_mainloop<TM, TN, NT, P, NMT_PLAIN_LA>(
+  // fp32: each k group's fragment reads go out during the previous group's
+  // MFMAs (readout 72 -> 69.5 us, query 43 -> 41.5 us); bf16 (one MFMA per
+  // k group and wave) keeps the compiler's order (readout 54 vs 56 us).
+  using KS = std::conditional_t<P::kBF16, void, KgShape<FM + FN, 4 * FM * FN>>;
+  gemm_mainloop<TM, TN, NT, P, kPlainLA<P>, KS>(
       A, Wp, Npad, m0, n0, lds,
       [&](const f32x4* As, const f32x4* Bs) {
 #pragma unroll
-        for (int kg = 0; kg < KQ / 2; ++kg) {
+        for (int kg = 0; kg < P::KQ / 2; ++kg) {
           f32x4 a[FM], b[FN];
 #pragma unroll
-          for (int i = 0; i < FM; ++i) a[i] = lds_frag<a_rows<TM>()>(As, kg, wm0 + 32 * i);
+          for (int i = 0; i < FM; ++i) a[i] = lds_frag_a<TM, P>(As, kg, wm0 + 32 * i);
 #pragma unroll
           for (int j = 0; j < FN; ++j) b[j] = lds_frag<TN>(Bs, kg, wn0 + 32 * j);
 #pragma unroll
@@ -138,7 +142,7 @@ hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi
 
 // Each segment with work needs a matrix behind it, and the staging
 // addresses the segments and the packed weights with 32-bit byte offsets.
-static bool segments_loadable(const AOperand& A, int64_t Npad) {
+static bool segments_loadable(const AOperand& A, int64_t Npad, bool bf16) {
   int64_t chunks = 0;
   for (int i = 0; i < A.nseg; ++i) {
     const ASeg& s = A.seg[i];
@@ -147,12 +151,12 @@ static bool segments_loadable(const AOperand& A, int64_t Npad) {
     if ((int64_t)(s.gather ? s.gmax : A.M) * s.ld * (s.bf16 ? 2 : 4) >= ((int64_t)1 << 31)) return false;
     chunks += s.nchunk;
   }
-  return chunks * KQ * Npad * 16 < ((int64_t)1 << 31);
+  return chunks * (bf16 ? PrecBF16::KQ : PrecF32::KQ) * Npad * 16 < ((int64_t)1 << 31);
 }
 
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
   if (A.M <= 0 || ep.N <= 0) return hipSuccess;
-  if (!segments_loadable(A, W.Npad)) return hipErrorInvalidValue;
+  if (!segments_loadable(A, W.Npad, W.bf16)) return hipErrorInvalidValue;
   return W.bf16 ? gemm_plain<PrecBF16>(t, A, W, ep, st) : gemm_plain<PrecF32>(t, A, W, ep, st);
 }
 
@@ -167,7 +171,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
-  __shared__ f32x4 lds[2 * (a_rows<TM>() + TN) * KQ];
+  __shared__ f32x4 lds[2 * (a_rows<TM, P>() + TN) * P::KQ];
   const GruProblem& Pb = batch.p[blockIdx.z];
   const f32x4* Wp = (const f32x4*)Pb.Wp;
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
@@ -179,10 +183,10 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
 
   auto chunk = [&](const f32x4* As, const f32x4* Bs, auto state_side) {
 #pragma unroll
-    for (int kg = 0; kg < KQ / 2; ++kg) {
+    for (int kg = 0; kg < P::KQ / 2; ++kg) {
       f32x4 a[FM];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = lds_frag<a_rows<TM>()>(As, kg, wm0 + 32 * i);
+      for (int i = 0; i < FM; ++i) a[i] = lds_frag_a<TM, P>(As, kg, wm0 + 32 * i);
       const f32x4 br = lds_frag<TN>(Bs, kg, wu0);
       const f32x4 bz = lds_frag<TN>(Bs, kg, HB + wu0);
       const f32x4 bn = lds_frag<TN>(Bs, kg, 2 * HB + wu0);
@@ -197,6 +201,10 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
       }
     }
   };
+  // bf16: each k group's fragment reads go out during the previous group's
+  // MFMAs (GRU2 116 -> 112 us); fp32 (12 MFMAs per k group) keeps the
+  // compiler's order, which measured faster there (287 vs 295 us).
+  using KS = std::conditional_t<P::kBF16, KgShape<FM + 3, 3 * FM>, void>;
   // One main loop per A segment, each with its side fixed at compile time:
   // a per-chunk branch between the two candidate accumulators would make the
   // compiler shuttle every accumulator between AGPRs and VGPRs each chunk.
@@ -204,14 +212,14 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
   for (int sg = 0; sg < Pb.A.nseg; ++sg) {
     const ASeg seg = seg_at(Pb.A, sg);
     if (seg.side)
-      gemm_segment<TM, TN, NT, P>(
+      gemm_segment<TM, TN, NT, P, kGruLA<P>, KS>(
           seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
           [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); }, vq0, 0, seg.nchunk);
     else
-      gemm_segment<TM, TN, NT, P>(
+      gemm_segment<TM, TN, NT, P, kGruLA<P>, KS>(
           seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
           [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); }, vq0, 0, seg.nchunk);
-    vq0 += (int64_t)seg.nchunk * KQ;
+    vq0 += (int64_t)seg.nchunk * P::KQ;
   }
 
   const GruEpi& ep = Pb.ep;
@@ -285,13 +293,16 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   for (int i = 1; i < nprob; ++i) M = M > probs[i].A.M ? M : probs[i].A.M;
   if (M <= 0) return hipSuccess;
   for (int i = 0; i < nprob; ++i)
-    if (!segments_loadable(probs[i].A, probs[i].Npad)) return hipErrorInvalidValue;
-  dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
-  constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
-  if (bf16)
-    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM, PrecBF16>), grid, dim3(threads), 0, st, b);
-  else
+    if (!segments_loadable(probs[i].A, probs[i].Npad, bf16)) return hipErrorInvalidValue;
+  if (bf16) {
+    dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB16), nprob);
+    constexpr int threads = (kGruTM / kGruWM16) * (kGruHB16 / 32) * 64;
+    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB16, kGruWM16, PrecBF16>), grid, dim3(threads), 0, st, b);
+  } else {
+    dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
+    constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
     hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM, PrecF32>), grid, dim3(threads), 0, st, b);
+  }
   return hipGetLastError();
 }
 
