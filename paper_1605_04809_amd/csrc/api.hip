@@ -270,8 +270,8 @@ nmt_status hip_fail(hipError_t e, const char* what) {
 #ifndef NMT_SPLITK_BLOCKS
 #define NMT_SPLITK_BLOCKS 1024
 #endif
-int plain_ksplit(int M, int N, int K_total, int kc) {
-  const int tiles = ceil_div(M, kPlainSmallTM) * ceil_div(N, kPlainSmallTN);
+int plain_ksplit(int M, int N, int K_total, int kc, Tile t) {
+  const int tiles = ceil_div(M, tile_m(t)) * ceil_div(N, tile_n(t));
   const int nc = ceil_div(K_total, kc);
   int ks = ceil_div(NMT_SPLITK_BLOCKS, tiles);
   if (ks > nc / 4) ks = nc / 4;
@@ -304,7 +304,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;

@@ -15,8 +15,8 @@ constexpr int kMaxTpad = 1024;     // attention keeps one score per source posit
 inline int chunk_k(bool bf16) { return bf16 ? PrecBF16::KC : PrecF32::KC; }
 
 // Tile shapes (rows x packed columns) of the kernel families.
-constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;
-constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;
+constexpr int kPlainSmallTM = 64, kPlainSmallTN = 64;    // 4 waves of 32 x 32
+constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;  // 4 waves of 64 x 64
 // GRU tile: TM rows x HB hidden units (3*HB packed columns), waves of WM rows
 // x 32 units.  Overridable at compile time for tuning sweeps.
 #ifndef NMT_GRU_TM
@@ -52,6 +52,8 @@ struct Packed {
 };
 
 enum class Tile { Small, Large };
+inline int tile_m(Tile t) { return t == Tile::Small ? kPlainSmallTM : kPlainLargeTM; }
+inline int tile_n(Tile t) { return t == Tile::Small ? kPlainSmallTN : kPlainLargeTN; }
 
 // Epilogue of the plain GEMM: out = act(acc + bias); rows with
 // (m % mask_T) >= mask_len[m / mask_T] are written as zeros.  With

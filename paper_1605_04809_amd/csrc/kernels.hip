@@ -118,24 +118,27 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
   ep.out[(int64_t)row * ep.ldo + n] = v;
 }
 
+template <int TM, int TN, int WM, int WN, class P>
+static void plain_tile(const AOperand& A, const f32x4* Wp, const Packed& W, const PlainEpi& ep, int ksplit,
+                       hipStream_t st) {
+  dim3 grid(ceil_div(A.M, TM), (unsigned)(W.Npad / TN), ksplit);
+  hipLaunchKernelGGL((k_gemm_plain<TM, TN, WM, WN, P>), grid, dim3((TM / WM) * (TN / WN) * 64), 0, st, A, Wp,
+                     W.Npad, ep);
+}
+
 template <class P>
 hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
   const f32x4* Wp = (const f32x4*)W.d;
+  if (W.Npad % tile_n(t)) return hipErrorInvalidValue;
+  if (ep.ksplit > 1 && !ep.part) return hipErrorInvalidValue;
+  const int ks = ep.ksplit > 1 ? ep.ksplit : 1;
+  if (t == Tile::Small)
+    plain_tile<kPlainSmallTM, kPlainSmallTN, 32, 32, P>(A, Wp, W, ep, ks, st);
+  else
+    plain_tile<kPlainLargeTM, kPlainLargeTN, 64, 64, P>(A, Wp, W, ep, ks, st);
   if (ep.ksplit > 1) {
-    if (t != Tile::Small || !ep.part) return hipErrorInvalidValue;
-    dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN), ep.ksplit);
-    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
-                       ep);
     const int64_t n = (int64_t)A.M * ep.N;
     hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
-  } else if (t == Tile::Small) {
-    dim3 grid(ceil_div(A.M, kPlainSmallTM), (unsigned)(W.Npad / kPlainSmallTN));
-    hipLaunchKernelGGL((k_gemm_plain<kPlainSmallTM, kPlainSmallTN, 32, 32, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
-                       ep);
-  } else {
-    dim3 grid(ceil_div(A.M, kPlainLargeTM), (unsigned)(W.Npad / kPlainLargeTN));
-    hipLaunchKernelGGL((k_gemm_plain<kPlainLargeTM, kPlainLargeTN, 64, 64, P>), grid, dim3(256), 0, st, A, Wp, W.Npad,
-                       ep);
   }
   return hipGetLastError();
 }
