@@ -60,7 +60,8 @@ extern "C" {
 #endif
 
 typedef struct nmt_model nmt_model;   /* device copy of all weights (library-owned) */
-typedef struct nmt_source nmt_source; /* ctx, pctx and lengths of S sentences (library-owned) */
+typedef struct nmt_source nmt_source; /* ctx, pctx (and the factors e^{2 pctx} the score kernels
+                                         read) and lengths of S sentences (library-owned) */
 
 typedef enum {
   NMT_OK = 0,

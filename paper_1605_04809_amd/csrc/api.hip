@@ -93,6 +93,7 @@ struct nmt_source {
   int32_t S = 0, Tpad = 0;
   Allocs mem;
   float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
+  float* kfac = nullptr;  // 2^{2 log2(e) pctx}: the keys' factors of the attention scores
   int32_t* len = nullptr;
   std::vector<int32_t> h_len;
 };
@@ -337,6 +338,7 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   const size_t rows = (size_t)S * Tpad;
   hipError_t e = src->mem.alloc((void**)&src->ctx, rows * 2 * d.H * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->pctx, rows * d.A * sizeof(float));
+  if (e == hipSuccess) e = src->mem.alloc((void**)&src->kfac, rows * d.A * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->len, S * sizeof(int32_t));
   if (e == hipSuccess && with_scratch) e = src->mem.alloc((void**)&src->scratch, rows * 6 * d.H * sizeof(float));
   if (e == hipSuccess)
@@ -350,13 +352,16 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   return NMT_OK;
 }
 
-// Attention keys pctx = ctx att_Wc + att_b for the unmasked positions.
+// Attention keys pctx = ctx att_Wc + att_b for the unmasked positions, and
+// their factors 2^{2 log2(e) pctx} that the score kernels use.
 hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
   const nmt_dims& d = m->dims;
   const int C = 2 * d.H;
   AOperand A = make_a(src->S * src->Tpad, {make_seg(src->ctx, C, C, 0, m->kc)});
   PlainEpi ep{src->pctx, d.A, m->att_b, d.A, 0, src->len, src->Tpad};
-  return launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
+  hipError_t e = launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
+  if (e == hipSuccess) e = launch_tanh_factors(src->pctx, src->kfac, (int64_t)src->S * src->Tpad * d.A, st);
+  return e;
 }
 
 }  // namespace
@@ -641,7 +646,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // masked attention and context
   if (e == hipSuccess) {
     const AttnGroups grp{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
-    e = launch_attention(B, Aw, C, src->Tpad, q, src->pctx, src->ctx, src->len, d_sent_id, src->S, m->att_v, c,
+    e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->ctx, src->len, d_sent_id, src->S, m->att_v, c,
                          d_alpha, grp, st);
   }
   mark(NMT_PHASE_ATTENTION + 1);

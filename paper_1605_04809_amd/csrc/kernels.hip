@@ -745,16 +745,39 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
 
 // ------------------------------------------------------------ attention
 
-// Attention scores.  With tanh x = 1 - 2 / (e^{2x} + 1),
-//   e_i = v . tanh(k_i + q) = sum(v) + sum_a (-2 v_a) / (2^(k_ia c + q_a c) + 1),  c = 2 log2(e),
-// and the softmax over i ignores the constant sum(v), so the kernels score
-//   e'_i = sum_a w_a / (2^(k_ia c + q'_a) + 1)   with w = -2 v and q' = c q:
-// one fma, the hardware exp2, one add, the hardware reciprocal and one fma
-// per term (the reciprocal is about 1 ulp; the result saturates correctly
-// for large |x|).
+// Attention scores.  With tanh x = 1 - 2 / (e^{2x} + 1) and
+// e^{2(k+q)} = 2^{ck} 2^{cq} (c = 2 log2 e),
+//   e_i = v . tanh(k_i + q) = sum(v) + sum_a (-2 v_a) / (2^{c k_ia} 2^{c q_a} + 1),
+// and the softmax over i ignores the constant sum(v).  The keys' factors
+// K = 2^{c k} are formed once per source position when the source is
+// encoded, the query's Q = 2^{c q} once per row, so the kernels score
+//   e'_i = sum_a w_a / (K_ia Q_a + 1)   with w = -2 v:
+// one fma, the hardware reciprocal and one fma per term (one
+// transcendental instead of an exp and a reciprocal).  The exponents are
+// clamped to [-126, 126], so K and Q are finite normal numbers; their
+// product over- or underflows exactly where tanh has saturated
+// (1 / (inf + 1) = 0, 1 / (0 + 1) = 1), and for |k|, |q| <= 43 each term is
+// the tanh form up to rounding.
 constexpr float kTanhScale = 2.f * kLog2e;
-__device__ __forceinline__ float score_term(float k, float qs, float w, float acc) {
-  return fmaf(w, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(fmaf(k, kTanhScale, qs)) + 1.f), acc);
+__device__ __forceinline__ float tanh_factor(float x) {
+  return __builtin_amdgcn_exp2f(fminf(fmaxf(x * kTanhScale, -126.f), 126.f));
+}
+__device__ __forceinline__ f32x4 tanh_factor(f32x4 x) {
+  return f32x4{tanh_factor(x[0]), tanh_factor(x[1]), tanh_factor(x[2]), tanh_factor(x[3])};
+}
+__device__ __forceinline__ float score_term(float kf, float qf, float w, float acc) {
+  return fmaf(w, __builtin_amdgcn_rcpf(fmaf(kf, qf, 1.f)), acc);
+}
+
+__global__ void k_tanh_factors(int64_t n, const float* __restrict__ x, float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = tanh_factor(x[i]);
+}
+
+hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_tanh_factors, dim3((unsigned)ceil_div(n, (int64_t)256)), dim3(256), 0, st, n, x, out);
+  return hipGetLastError();
 }
 
 // Fallback for more sentences than the grouping kernel counts: one block
@@ -764,7 +787,7 @@ __device__ __forceinline__ float score_term(float k, float qs, float w, float ac
 // float4 pieces of the context over the unmasked positions.
 template <int NQ>
 __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, const float* __restrict__ q,
-                                                   const float* __restrict__ pctx, const float* __restrict__ ctx,
+                                                   const float* __restrict__ kfac, const float* __restrict__ ctx,
                                                    const int32_t* __restrict__ len,
                                                    const int32_t* __restrict__ sent_id, int S,
                                                    const float* __restrict__ v, float* __restrict__ c,
@@ -783,14 +806,14 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
   }
   const int L = len[s];
   const int A4 = A / 4;
-  f32x4 qv[NQ], vv[NQ];  // scaled query c q and weights -2 v (see score_term)
+  f32x4 qv[NQ], vv[NQ];  // query factors 2^{c q} and weights -2 v (see score_term)
 #pragma unroll
   for (int k = 0; k < NQ; ++k) {
     const int a4 = lane + 64 * k;
-    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) * kTanhScale : zero4();
+    qv[k] = a4 < A4 ? tanh_factor(*(const f32x4*)(q + (int64_t)row * A + 4 * a4)) : zero4();
     vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
   }
-  const float* P = pctx + (int64_t)s * Tpad * A;
+  const float* P = kfac + (int64_t)s * Tpad * A;
   for (int i = wave; i < L; i += 4) {
     float acc = 0.f;
 #pragma unroll
@@ -948,29 +971,15 @@ __device__ __forceinline__ float wave_sums(float (&v)[G]) {
   return r;
 }
 
-// One block (NW waves) per tile of up to G rows of one sentence.  The rows'
-// queries sit in LDS; wave w takes source positions w, w+NW, ..., loads the
-// position's key once and scores it against all G rows at once (rows past
-// the tile's count score zero queries and are dropped), each lane covering
-// float4 pieces of the attention width; then one wave per row normalises the
-// scores; finally every thread accumulates a float4 piece of the context of
-// all rows, reading each annotation once.
 template <int G, int NQ>
-__global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
-    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ pctx, const float* __restrict__ ctx,
-    const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
-    const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
-    float* __restrict__ alpha) {
+__device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int Tpad, const float* __restrict__ q,
+                                               const float* __restrict__ kfac, const float* __restrict__ ctx,
+                                               const int32_t* __restrict__ len, const int32_t* __restrict__ perm,
+                                               const float* __restrict__ v, float* __restrict__ c,
+                                               float* __restrict__ alpha, f32x4* qs, float* e, int* rows, int wave,
+                                               int lane, int A4, int C4) {
   constexpr int NW = kAttnWaves, NT = NW * 64;
-  extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
-  __shared__ int rows[G];
-  if ((int)blockIdx.x >= *n_tiles) return;
-  const int4 tl = tiles[blockIdx.x];
   const int s = tl.x, n = tl.z;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int A4 = A / 4, C4 = C / 4;
-  f32x4* qs = dyn;
-  float* e = (float*)(dyn + G * A4);
   if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? perm[tl.y + threadIdx.x] : 0;
   __syncthreads();
   if (s < 0) {  // rows with an invalid sentence: flagged and NaN-ed by the combine kernel
@@ -981,10 +990,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
     }
     return;
   }
-  // scaled queries c q in LDS and weights -2 v in registers (see score_term)
+  // query factors 2^{c q} in LDS and weights -2 v in registers (see score_term);
+  // rows past the tile's count get factor 0 and are dropped
   for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
     const int g = idx / A4, a4 = idx - g * A4;
-    qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) * kTanhScale : zero4();
+    qs[idx] = g < n ? tanh_factor(*(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4)) : zero4();
   }
   f32x4 vv[NQ];
 #pragma unroll
@@ -994,7 +1004,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
   }
   __syncthreads();
   const int L = len[s];
-  const float* P = pctx + (int64_t)s * Tpad * A;
+  const float* P = kfac + (int64_t)s * Tpad * A;
   for (int i = wave; i < L; i += NW) {
     float acc[G];
 #pragma unroll
@@ -1051,22 +1061,48 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
   }
 }
 
+// One block (NW waves) per tile of up to G rows of one sentence.  The rows'
+// queries sit in LDS; wave w takes source positions w, w+NW, ..., loads the
+// position's key once and scores it against all G rows at once (rows past
+// the tile's count score zero queries and are dropped), each lane covering
+// float4 pieces of the attention width; then one wave per row normalises the
+// scores; finally every thread accumulates a float4 piece of the context of
+// all rows, reading each annotation once.
 template <int G, int NQ>
-static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+__global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
+    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ ctx,
+    const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
+    const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
+    float* __restrict__ alpha) {
+  constexpr int NW = kAttnWaves, NT = NW * 64;
+  extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
+  __shared__ int rows[G];
+  const int nt = *n_tiles;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int A4 = A / 4, C4 = C / 4;
+  f32x4* qs = dyn;
+  float* e = (float*)(dyn + G * A4);
+  if ((int)blockIdx.x >= nt) return;
+  attention_tile<G, NQ>(tiles[blockIdx.x], A, C, Tpad, q, kfac, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
+                        lane, A4, C4);
+}
+
+template <int G, int NQ>
+static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                               const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
                               float* alpha, hipStream_t st) {
-  const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);
+  const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
   const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
-  hipLaunchKernelGGL((k_attention_grouped<G, NQ>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C, Tpad, q, pctx, ctx, len,
+  hipLaunchKernelGGL((k_attention_grouped<G, NQ>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C, Tpad, q, kfac, ctx, len,
                      grp.perm, grp.tiles, grp.n_tiles, v, c, alpha);
 }
 
 template <int NQ>
-static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                          const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
                          float* c, float* alpha, hipStream_t st) {
   if (S > kGroupMaxS || !grp.perm) {
-    hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, pctx, ctx, len, sent_id, S, v,
+    hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, ctx, len, sent_id, S, v,
                        c, alpha);
     return;
   }
@@ -1075,24 +1111,24 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                      grp.n_tiles);
   if (G == kAttnGroup)
-    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, pctx, ctx, len, grp, S, v, c, alpha, st);
+    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, st);
   else
-    attention_grouped<4, NQ>(B, A, C, Tpad, q, pctx, ctx, len, grp, S, v, c, alpha, st);
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, st);
 }
 
-hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* pctx, const float* ctx,
+hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                             const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
                             const AttnGroups& grp, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    attention_nq<1>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<1>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 2)
-    attention_nq<2>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<2>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 4)
-    attention_nq<4>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<4>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else if (nq <= 8)
-    attention_nq<8>(B, A, C, Tpad, q, pctx, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<8>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

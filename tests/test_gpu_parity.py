@@ -105,6 +105,33 @@ def test_high_signal_every_row(gpu, cfg):
     g2.close()
 
 
+@pytest.mark.parametrize("S", [3, 8200], ids=["grouped", "per_row_fallback"])
+def test_large_keys_and_queries_every_row(gpu, S):
+    """Keys and queries far into tanh's saturation (|pctx| up to 38, queries
+    scaled to the same bound), so many terms tanh(k + q) are sums of two
+    large values of opposite sign.  The kernels score each term from the
+    factors 2^{2 log2(e) k} and 2^{2 log2(e) q}, formed separately (exact up
+    to rounding for |k|, |q| <= 43); the oracle takes tanh of the sum."""
+    _torch()
+    cfg = high_signal(CONFIGS["tiny"]).replace(B=200, S=S, len_lo=1, Tpad=10)
+    wl = make_workload(cfg)
+    ctx = random_annotations(cfg, seed=31)
+    p = wl.params
+    L = wl.src_len
+    valid = np.arange(cfg.Tpad)[None, :] < L[:, None]
+    pctx = ctx.astype(np.float64) @ p["att_Wc"].astype(np.float64) + p["att_b"]
+    f = 38.0 / np.abs(pctx[valid]).max()
+    p["att_Wc"] = (p["att_Wc"] * f).astype(np.float32)
+    p["att_b"] = (p["att_b"] * f).astype(np.float32)
+    # queries: |s1 Wq| <= sum_h |Wq[h, a]| since |s1| < 1
+    p["att_Wq"] = (p["att_Wq"] * (38.0 / np.abs(p["att_Wq"]).sum(axis=0).max())).astype(np.float32)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    assert np.abs(o.pctx).max() > 30
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+
+
 @pytest.mark.parametrize("S", [8192, 8200], ids=["grouped_at_limit", "per_row_fallback"])
 def test_many_sentences_every_row(gpu, S):
     """Attention groups rows by sentence with per-sentence counters in LDS for
