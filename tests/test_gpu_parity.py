@@ -296,6 +296,47 @@ def test_paper_sized_step_sampled_rows(gpu, name):
     g.close()
 
 
+@pytest.mark.parametrize("wtype", ["f32", "bf16"])
+def test_large_batch_sampled_rows(gpu, wtype):
+    """16 times the benchmarked batch: B = 32768 rows over 64 sentences at
+    the paper's dimensions (grids, 32-bit offsets, the grouping kernel and
+    the vocabulary slices far past the benchmarked shapes); oracle on
+    sampled rows."""
+    _torch()
+    wl = make_workload(CONFIGS["enru_b2000"].replace(B=32768, S=64, wtype=wtype, seed=41))
+    g = gpu.GpuRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    out = g.step(*args, debug=False)
+    assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
+    rows = sample_rows(wl.cfg.B, 24, seed=42)
+    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows],
+                                 intermediates=False)
+    if wtype == "bf16":
+        compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16, keys=("s_new",))
+    else:
+        compare(out, ref, rows=rows, keys=("s_new",))
+    g.close()
+
+
+def test_longest_sources_every_row(gpu):
+    """Sources at the attention's length limit (Tpad = 1024 positions) next
+    to a one-word source, through the GPU encoder (1024 recurrence steps in
+    each direction) and through injected annotations; every row."""
+    _torch()
+    cfg = CONFIGS["tiny"].replace(B=48, S=3, len_lo=1, len_hi=1024, Tpad=1024, seed=43)
+    wl = make_workload(cfg)
+    wl.src_len[:] = [1024, 1, 517]
+    wl.sent_id[:3] = [0, 1, 2]
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    g, o = gpu.GpuRun(wl), gpu.OracleRun(wl)
+    compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+    ctx = random_annotations(cfg, seed=44)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+
+
 def test_phrase_scoring_stepwise(gpu):
     """Phrase workload: the batch shrinks as phrases end, states are fed back,
     and log-probs are summed per phrase (the per-depth loop of Figure 2)."""
