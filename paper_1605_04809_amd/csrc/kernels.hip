@@ -874,44 +874,85 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
 // (a sentence-order list left a second round of a few long tiles).  The
 // order of rows inside a sentence does not matter: each row's arithmetic is
 // the same in any tile.
+// Exclusive prefix sums over the 1024 threads of a block of two values per
+// thread (wave scans with shuffles, then one scan of the 16 wave totals);
+// returns the block totals.  wsum: 2 x 16 ints of LDS, free on entry and
+// on return.
+__device__ __forceinline__ int2 block_scan2(int& a, int& b, int (*wsum)[16]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = a, y = b;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int px = __shfl_up(x, o, 64), py = __shfl_up(y, o, 64);
+    if (lane >= o) {
+      x += px;
+      y += py;
+    }
+  }
+  if (lane == 63) {
+    wsum[0][wave] = x;
+    wsum[1][wave] = y;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    int u = lane < 16 ? wsum[0][lane] : 0, w = lane < 16 ? wsum[1][lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int pu = __shfl_up(u, o, 64), pw = __shfl_up(w, o, 64);
+      if (lane >= o) {
+        u += pu;
+        w += pw;
+      }
+    }
+    if (lane < 16) {
+      wsum[0][lane] = u;
+      wsum[1][lane] = w;
+    }
+  }
+  __syncthreads();
+  const int2 tot = make_int2(wsum[0][15], wsum[1][15]);
+  a = (wave ? wsum[0][wave - 1] : 0) + x - a;
+  b = (wave ? wsum[1][wave - 1] : 0) + y - b;
+  __syncthreads();
+  return tot;
+}
+
 __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const int32_t* __restrict__ sent_id,
                                                      const int32_t* __restrict__ len, int Tpad,
                                                      int32_t* __restrict__ perm, int4* __restrict__ tiles,
                                                      int32_t* __restrict__ n_tiles) {
   __shared__ int cnt[kGroupMaxS + 1];    // rows per bucket, then the bucket's write cursor
   __shared__ int order[kGroupMaxS + 1];  // buckets longest sentence first, the invalid bucket last
+  __shared__ int keyv[kGroupMaxS + 1];   // sort key of each bucket
   __shared__ int keyc[kMaxTpad + 2];     // buckets per key, then the key's write cursor
-  __shared__ int part[2][1024];
+  __shared__ int wsum[2][16];
   const int tid = threadIdx.x, NB = S + 1, NK = Tpad + 1;
   for (int i = tid; i < NB; i += 1024) cnt[i] = 0;
   for (int k = tid; k < NK; k += 1024) keyc[k] = 0;
   __syncthreads();
+  // rows per bucket, and the key of each bucket: Tpad - length (0 for the
+  // longest sentence); the invalid bucket sorts last
   for (int b = tid; b < B; b += 1024) {
     const int s = sent_id[b];
     atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1);
   }
-  // key of bucket i: Tpad - length (0 for the longest); the invalid bucket sorts last
-  auto key = [&](int i) { return i < S ? Tpad - min(max(len[i], 0), Tpad) : Tpad; };
-  for (int i = tid; i < NB; i += 1024) atomicAdd(&keyc[key(i)], 1);
+  for (int i = tid; i < NB; i += 1024) {
+    const int k = i < S ? Tpad - min(max(len[i], 0), Tpad) : Tpad;
+    keyv[i] = k;
+    atomicAdd(&keyc[k], 1);
+  }
   __syncthreads();
   // exclusive scan of the key counts (NK <= 1025: thread t owns keys [2t, 2t+2))
   {
     const int k0 = 2 * tid, k1 = k0 + 1;
     const int c0 = k0 < NK ? keyc[k0] : 0, c1 = k1 < NK ? keyc[k1] : 0;
-    part[0][tid] = c0 + c1;
-    __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-      const int a0 = tid >= o ? part[0][tid - o] : 0;
-      __syncthreads();
-      part[0][tid] += a0;
-      __syncthreads();
-    }
-    const int base = part[0][tid] - c0 - c1;
+    int base = c0 + c1, unused = 0;
+    block_scan2(base, unused, wsum);
     if (k0 < NK) keyc[k0] = base;
     if (k1 < NK) keyc[k1] = base + c0;
     __syncthreads();
   }
-  for (int i = tid; i < NB; i += 1024) order[atomicAdd(&keyc[key(i)], 1)] = i;
+  for (int i = tid; i < NB; i += 1024) order[atomicAdd(&keyc[keyv[i]], 1)] = i;
   __syncthreads();
   // exclusive scans of the row and tile counts in that order; thread tid owns ranks [lo, hi)
   const int per = (NB + 1023) / 1024, lo = tid * per < NB ? tid * per : NB, hi = lo + per < NB ? lo + per : NB;
@@ -921,18 +962,9 @@ __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const 
     rs += n;
     ts += (n + G - 1) / G;
   }
-  part[0][tid] = rs;
-  part[1][tid] = ts;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int a0 = tid >= o ? part[0][tid - o] : 0, a1 = tid >= o ? part[1][tid - o] : 0;
-    __syncthreads();
-    part[0][tid] += a0;
-    part[1][tid] += a1;
-    __syncthreads();
-  }
-  int roff = part[0][tid] - rs, toff = part[1][tid] - ts;
-  if (tid == 1023) *n_tiles = part[1][1023];
+  int roff = rs, toff = ts;
+  const int2 tot = block_scan2(roff, toff, wsum);
+  if (tid == 0) *n_tiles = tot.y;
   for (int j = lo; j < hi; ++j) {
     const int i = order[j], n = cnt[i];
     for (int k = 0; k * G < n; ++k) tiles[toff + k] = make_int4(i < S ? i : -1, roff + k * G, min(G, n - k * G), 0);
