@@ -18,6 +18,8 @@
 //                  masked MLP attention and context, rows grouped by
 //                  sentence so a block reads each key and annotation once
 //                  for several rows (k_attention: one row per block).
+//   k_tanh_factors the keys' factors 2^{2 log2(e) pctx} the attention
+//                  scores read (formed once per source).
 #include <algorithm>
 
 #include "internal.hpp"
