@@ -138,9 +138,12 @@ struct AttnGroups {
   int32_t* n_tiles;
 };
 // kfac [S x Tpad x A]: the keys' factors 2^{2 log2(e) pctx} (launch_tanh_factors).
+// c_bf16: the context c [B x C] is written in bf16 (nearest even) instead of fp32.
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac,
                             const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
-                            const float* v, float* c, float* alpha, const AttnGroups& grp, hipStream_t st);
+                            const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
+                            hipStream_t st);
+hipError_t launch_bf16_to_f32(const void* x, float* y, int64_t n, hipStream_t st);
 // out[i] = 2^{2 log2(e) x[i]}, exponent clamped to [-126, 126] (the attention's key factors).
 hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_t st);
 hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src,

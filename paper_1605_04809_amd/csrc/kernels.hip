@@ -771,6 +771,18 @@ __device__ __forceinline__ float score_term(float kf, float qf, float w, float a
   return fmaf(w, __builtin_amdgcn_rcpf(fmaf(kf, qf, 1.f)), acc);
 }
 
+// Four context values at element index i of c: fp32, or (c_bf16) bf16
+// rounded to nearest even, the rounding the bf16 GEMMs apply when they
+// stage an fp32 operand.
+__device__ __forceinline__ void store_c4(float* c, int64_t i, const f32x4& v, int c_bf16) {
+  if (c_bf16) {
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    *(bf16x4_t*)((__bf16*)c + i) = bf16x4_t{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+  } else {
+    *(f32x4*)(c + i) = v;
+  }
+}
+
 __global__ void k_tanh_factors(int64_t n, const float* __restrict__ x, float* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) out[i] = tanh_factor(x[i]);
@@ -793,15 +805,14 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
                                                    const int32_t* __restrict__ len,
                                                    const int32_t* __restrict__ sent_id, int S,
                                                    const float* __restrict__ v, float* __restrict__ c,
-                                                   float* __restrict__ alpha) {
+                                                   float* __restrict__ alpha, int c_bf16) {
   __shared__ float e[kMaxTpad];
   __shared__ float red[8];
   const int row = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int s = sent_id[row];
-  float* crow = c + (int64_t)row * C;
   if (s < 0 || s >= S) {  // flagged and NaN-ed by the combine kernel; keep the rest finite
-    for (int k4 = threadIdx.x; k4 < C / 4; k4 += 256) *(f32x4*)(crow + 4 * k4) = zero4();
+    for (int k4 = threadIdx.x; k4 < C / 4; k4 += 256) store_c4(c, (int64_t)row * C + 4 * k4, zero4(), c_bf16);
     if (alpha)
       for (int i = threadIdx.x; i < Tpad; i += 256) alpha[(int64_t)row * Tpad + i] = 0.f;
     return;
@@ -860,7 +871,7 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
       acc[2] += a * x[2];
       acc[3] += a * x[3];
     }
-    *(f32x4*)(crow + 4 * k4) = acc;
+    store_c4(c, (int64_t)row * C + 4 * k4, acc, c_bf16);
   }
 }
 
@@ -1011,14 +1022,14 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
                                                const int32_t* __restrict__ len, const int32_t* __restrict__ perm,
                                                const float* __restrict__ v, float* __restrict__ c,
                                                float* __restrict__ alpha, f32x4* qs, float* e, int* rows, int wave,
-                                               int lane, int A4, int C4) {
+                                               int lane, int A4, int C4, int c_bf16) {
   constexpr int NW = kAttnWaves, NT = NW * 64;
   const int s = tl.x, n = tl.z;
   if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? perm[tl.y + threadIdx.x] : 0;
   __syncthreads();
   if (s < 0) {  // rows with an invalid sentence: flagged and NaN-ed by the combine kernel
     for (int g = 0; g < n; ++g) {
-      for (int k4 = threadIdx.x; k4 < C4; k4 += NT) *(f32x4*)(c + (int64_t)rows[g] * C + 4 * k4) = zero4();
+      for (int k4 = threadIdx.x; k4 < C4; k4 += NT) store_c4(c, (int64_t)rows[g] * C + 4 * k4, zero4(), c_bf16);
       if (alpha)
         for (int i = threadIdx.x; i < Tpad; i += NT) alpha[(int64_t)rows[g] * Tpad + i] = 0.f;
     }
@@ -1091,7 +1102,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (g < n) *(f32x4*)(c + (int64_t)rows[g] * C + 4 * k4) = acc[g];
+      if (g < n) store_c4(c, (int64_t)rows[g] * C + 4 * k4, acc[g], c_bf16);
   }
 }
 
@@ -1107,7 +1118,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
     int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ ctx,
     const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
-    float* __restrict__ alpha) {
+    float* __restrict__ alpha, int c_bf16) {
   constexpr int NW = kAttnWaves, NT = NW * 64;
   extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
   __shared__ int rows[G];
@@ -1118,26 +1129,26 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
   float* e = (float*)(dyn + G * A4);
   if ((int)blockIdx.x >= nt) return;
   attention_tile<G, NQ>(tiles[blockIdx.x], A, C, Tpad, q, kfac, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
-                        lane, A4, C4);
+                        lane, A4, C4, c_bf16);
 }
 
 template <int G, int NQ>
 static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                               const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
-                              float* alpha, hipStream_t st) {
+                              float* alpha, int c_bf16, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
   const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
   hipLaunchKernelGGL((k_attention_grouped<G, NQ>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C, Tpad, q, kfac, ctx, len,
-                     grp.perm, grp.tiles, grp.n_tiles, v, c, alpha);
+                     grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16);
 }
 
 template <int NQ>
 static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                          const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
-                         float* c, float* alpha, hipStream_t st) {
+                         float* c, float* alpha, int c_bf16, hipStream_t st) {
   if (S > kGroupMaxS || !grp.perm) {
     hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, ctx, len, sent_id, S, v,
-                       c, alpha);
+                       c, alpha, c_bf16);
     return;
   }
   // rows per tile: kAttnGroup when their queries and scores fit 64 KB of LDS, else 4
@@ -1145,26 +1156,39 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                      grp.n_tiles);
   if (G == kAttnGroup)
-    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, st);
+    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, c_bf16, st);
   else
-    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, st);
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, c_bf16, st);
 }
 
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
                             const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
-                            const AttnGroups& grp, hipStream_t st) {
+                            const AttnGroups& grp, bool c_bf16, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    attention_nq<1>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<1>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 2)
-    attention_nq<2>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<2>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 4)
-    attention_nq<4>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<4>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 8)
-    attention_nq<8>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, st);
+    attention_nq<8>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// Widens n bf16 values to fp32 (a bf16 context for the debug output).
+__global__ void k_bf16_to_f32(int64_t n, const __bf16* __restrict__ x, float* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = (float)x[i];
+}
+
+hipError_t launch_bf16_to_f32(const void* x, float* y, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_bf16_to_f32, dim3((unsigned)ceil_div(n, (int64_t)256)), dim3(256), 0, st, n, (const __bf16*)x,
+                     y);
   return hipGetLastError();
 }
 
