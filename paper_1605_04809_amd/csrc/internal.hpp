@@ -88,6 +88,7 @@ struct GruEpi {
   const int32_t* mask_len;  // nullable: row m is kept iff mask_pos < mask_len[m]
   int32_t mask_pos;
   int32_t H;
+  __bf16* out16 = nullptr;  // nullable: a bf16 copy of out (nearest even), row stride ldo
 };
 
 struct GruProblem {

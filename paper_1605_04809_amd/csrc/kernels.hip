@@ -284,7 +284,10 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
       const float ng = tanhf(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
       float hn = zg * hp[q] + (1.f - zg) * ng;
       if (!keep[q]) hn = 0.f;
-      if (rowq[q] < M) ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
+      if (rowq[q] < M) {
+        ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
+        if (ep.out16) ep.out16[(int64_t)rowq[q] * ep.ldo + j] = (__bf16)hn;
+      }
     }
   }
 }
