@@ -687,23 +687,29 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // readout t = tanh(s_new Ws + x Wy + c Wc + b)
   if (e == hipSuccess) {
     PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
+    if (m->bf16) {  // the vocabulary and combine kernels stage t in bf16 anyway
+      ep.out16 = (__bf16*)t;
+      ep.ldo = bf16_row(E);
+    }
     e = launch_gemm_plain(Tile::Small,
                           make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}), m->ro,
                           ep, st);
   }
   mark(NMT_PHASE_READOUT + 1);
   // vocabulary projection with an online log-sum-exp per slice, then the combine
-  if (e == hipSuccess) e = launch_vocab_lse(t, B, E, m->out, V, part, L.nS, st);
+  if (e == hipSuccess) e = launch_vocab_lse(t, m->bf16, B, E, m->out, V, part, L.nS, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
-    e = launch_lse_combine(B, part, L.nS, t, E, m->out, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
+    e = launch_lse_combine(B, part, L.nS, t, m->bf16, E, m->out, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
                            m->err, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && d_c)
-    e = c16 ? launch_bf16_to_f32(c, d_c, (int64_t)B * C, st)
+    e = c16 ? launch_bf16_to_f32(c, B, C, C, d_c, st)
             : hipMemcpyAsync(d_c, c, (size_t)B * C * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess && d_t) e = hipMemcpyAsync(d_t, t, (size_t)B * E * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && d_t)
+    e = m->bf16 ? launch_bf16_to_f32(t, B, E, bf16_row(E), d_t, st)
+                : hipMemcpyAsync(d_t, t, (size_t)B * E * 4, hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) return hip_fail(e, "score step");
   return ok();
 }

@@ -224,16 +224,18 @@ template <class P>
 __device__ __forceinline__ f32x4 with_bias_ones(f32x4 v, int kq, int E, int nb) {
   const int k0 = kq * P::KV;
   if (k0 + P::KV <= E || k0 >= E + nb) return v;
+  // slots past E: 1 at the bias slots, 0 after them (whatever the row's
+  // memory held there)
   if constexpr (P::kBF16) {
     bf16x8 b = __builtin_bit_cast(bf16x8, v);
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-      if (k0 + e >= E && k0 + e < E + nb) b[e] = (__bf16)1.f;
+      if (k0 + e >= E) b[e] = (__bf16)(k0 + e < E + nb ? 1.f : 0.f);
     return __builtin_bit_cast(f32x4, b);
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      if (k0 + e >= E && k0 + e < E + nb) v[e] = 1.f;
+      if (k0 + e >= E) v[e] = k0 + e < E + nb ? 1.f : 0.f;
     return v;
   }
 }

@@ -70,6 +70,7 @@ struct PlainEpi {
   int32_t mask_T;
   int32_t ksplit = 1;
   float* part = nullptr;
+  __bf16* out16 = nullptr;  // nullable: the output goes here in bf16 (nearest even) instead of to out
 };
 
 // Epilogue of the GRU gate GEMM (see device.hpp for the cell).
@@ -106,7 +107,11 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
 int vocab_slices(int M, int V, bool bf16);
 int vocab_max_kpad(bool bf16);
 bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
-hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
+// Row stride of a bf16 copy of rows E wide: whole 16-byte vectors.
+inline __host__ __device__ int bf16_row(int E) { return (E + 7) / 8 * 8; }
+// t16: t is stored in bf16 (row stride bf16_row(E)) instead of fp32; the
+// kernels never use the padding slots' contents (with_bias_ones).
+hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
                             hipStream_t st);
 // Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same
 // indices (req_off nullable: one request per row, req[b] -> logp[b]).
@@ -118,7 +123,7 @@ struct Requests {
   const int32_t* state_row;
   int32_t pool_rows;
 };
-hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W, int V,
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int t16, int E, const Packed& W, int V,
                               const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
                               hipStream_t st);
@@ -144,7 +149,7 @@ hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const
                             const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
                             hipStream_t st);
-hipError_t launch_bf16_to_f32(const void* x, float* y, int64_t n, hipStream_t st);
+hipError_t launch_bf16_to_f32(const void* x, int64_t rows, int cols, int64_t ld, float* y, hipStream_t st);
 // out[i] = 2^{2 log2(e) x[i]}, exponent clamped to [-126, 126] (the attention's key factors).
 hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_t st);
 hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src,

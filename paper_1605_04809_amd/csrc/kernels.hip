@@ -102,7 +102,10 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
         float v = acc[i][j][r] + bn;
         if (ep.act == 1) v = tanhf(v);
         if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
-        ep.out[(int64_t)row * ep.ldo + n] = v;
+        if (ep.out16)
+          ep.out16[(int64_t)row * ep.ldo + n] = (__bf16)v;
+        else
+          ep.out[(int64_t)row * ep.ldo + n] = v;
       }
   }
 }
@@ -117,7 +120,10 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
   v += ep.bias ? ep.bias[n] : 0.f;
   if (ep.act == 1) v = tanhf(v);
   if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
-  ep.out[(int64_t)row * ep.ldo + n] = v;
+  if (ep.out16)
+    ep.out16[(int64_t)row * ep.ldo + n] = (__bf16)v;
+  else
+    ep.out[(int64_t)row * ep.ldo + n] = v;
 }
 
 template <int TM, int TN, int WM, int WN, class P>
@@ -393,7 +399,7 @@ struct VocabTune {
 // rotates registers at each loop back-edge.  No other vector-memory load is
 // issued in the loop: its wait would drain the prefetch ring.
 template <class P, int VPF>
-__global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int M, int E,
+__global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int t16, int M, int E,
                                                                       int nb, int Kpad, const f32x4* __restrict__ Wp,
                                                                       int64_t Npad, int V, int nM, int nS,
                                                                       float2* __restrict__ part) {
@@ -415,7 +421,11 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
     const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
     As[kq * VTM + m] = with_bias_ones<P>(
-        load_a_vec<P>(row < M ? (const char*)(t + (int64_t)row * E) : nullptr, 0, E, kq * P::KV), kq, E, nb);
+        load_a_vec<P>(row >= M ? nullptr
+                      : t16    ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
+                               : (const char*)(t + (int64_t)row * E),
+                      t16, E, kq * P::KV),
+        kq, E, nb);
   }
   __syncthreads();
 
@@ -629,7 +639,8 @@ int vocab_max_kpad(bool bf16) {
 }
 
 template <class P>
-hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS, hipStream_t st) {
+hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
+                     hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
   const int nM = ceil_div(M, VocabTune<P>::VTM);
   dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
@@ -638,29 +649,31 @@ hipError_t vocab_lse(const float* t, int M, int E, const Packed& W, int V, float
   // the deepest prefetch that divides the k groups into at least two blocks
   auto fits = [&](int vpf) { return PF >= vpf && nkg % vpf == 0 && nkg >= 2 * vpf; };
   if (fits(16))
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2)>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp,
                        W.Npad, V, nM, nS, part);
   else if (fits(8))
-    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 2)>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp,
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 2)>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp,
                        W.Npad, V, nM, nS, part);
   else if (fits(4))
-    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
+    hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
                        part);
   else if (fits(2))
-    hipLaunchKernelGGL((k_vocab_lse<P, 2>), grid, block, 0, st, t, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
+    hipLaunchKernelGGL((k_vocab_lse<P, 2>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
                        part);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_vocab_lse(const float* t, int M, int E, const Packed& W, int V, float2* part, int nS,
+hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
                             hipStream_t st) {
   if (M <= 0) return hipSuccess;
+  if (t16 && !W.bf16) return hipErrorInvalidValue;
   if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1 || W.Npad < ((int64_t)V + 31) / 32 * 32 + 32)
     return hipErrorInvalidValue;
   if (!vocab_offsets_fit(W.Kpad, W.Npad, W.bf16)) return hipErrorInvalidValue;
-  return W.bf16 ? vocab_lse<PrecBF16>(t, M, E, W, V, part, nS, st) : vocab_lse<PrecF32>(t, M, E, W, V, part, nS, st);
+  return W.bf16 ? vocab_lse<PrecBF16>(t, t16, M, E, W, V, part, nS, st)
+                : vocab_lse<PrecF32>(t, 0, M, E, W, V, part, nS, st);
 }
 
 // ---------------------------------------------------- partials combine
@@ -686,7 +699,7 @@ __device__ __forceinline__ float dot_vec(const f32x4& a, const f32x4& b) {
 // offsets, gets NaN outputs and sets the flag.
 template <class P>
 __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __restrict__ part, int nS,
-                                                     const float* __restrict__ t, int E, int nb, int Kpad,
+                                                     const float* __restrict__ t, int t16, int E, int nb, int Kpad,
                                                      const f32x4* __restrict__ Wp, int64_t Npad, int V,
                                                      Requests rq,
                                                      const int32_t* __restrict__ y_prev,
@@ -721,12 +734,13 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
   }
   sum = wave_sum(sum);
   const float lz = mx + logf(sum);
-  const char* tr = (const char*)(t + (int64_t)row * E);
+  const char* tr = t16 ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
+                       : (const char*)(t + (int64_t)row * E);
   for (int j = j0; j < j1; ++j) {
     const int w = rq.req[j];
     float dot = 0.f;
     for (int kq = lane; kq < Kpad / P::KV; kq += 64)
-      dot += dot_vec<P>(with_bias_ones<P>(load_a_vec<P>(tr, 0, E, kq * P::KV), kq, E, nb),
+      dot += dot_vec<P>(with_bias_ones<P>(load_a_vec<P>(tr, t16, E, kq * P::KV), kq, E, nb),
                         Wp[(int64_t)kq * Npad + w]);
     dot = wave_sum(dot);
     if (lane == 0) logp[j] = dot - lz;
@@ -734,16 +748,16 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
   if (lane == 0 && logZ) logZ[row] = lz;
 }
 
-hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int E, const Packed& W, int V,
+hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int t16, int E, const Packed& W, int V,
                               const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
   if (B <= 0) return hipSuccess;
-  if (W.Krows != E || W.nbias < 1) return hipErrorInvalidValue;
+  if (W.Krows != E || W.nbias < 1 || (t16 && !W.bf16)) return hipErrorInvalidValue;
   if (W.bf16)
-    hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
+    hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, t16, E,
                        W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
   else
-    hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, E,
+    hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, 0, E,
                        W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
   return hipGetLastError();
 }
@@ -1182,16 +1196,19 @@ hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const
   return hipGetLastError();
 }
 
-// Widens n bf16 values to fp32 (a bf16 context for the debug output).
-__global__ void k_bf16_to_f32(int64_t n, const __bf16* __restrict__ x, float* __restrict__ y) {
+// Widens a bf16 matrix [rows x cols] with row stride ld to a dense fp32 one
+// (bf16 intermediates for the debug outputs).
+__global__ void k_bf16_to_f32(int64_t rows, int cols, int64_t ld, const __bf16* __restrict__ x,
+                              float* __restrict__ y) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) y[i] = (float)x[i];
+  if (i < rows * cols) y[i] = (float)x[(i / cols) * ld + i % cols];
 }
 
-hipError_t launch_bf16_to_f32(const void* x, float* y, int64_t n, hipStream_t st) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_bf16_to_f32, dim3((unsigned)ceil_div(n, (int64_t)256)), dim3(256), 0, st, n, (const __bf16*)x,
-                     y);
+hipError_t launch_bf16_to_f32(const void* x, int64_t rows, int cols, int64_t ld, float* y, hipStream_t st) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const int64_t n = rows * cols;
+  hipLaunchKernelGGL(k_bf16_to_f32, dim3((unsigned)ceil_div(n, (int64_t)256)), dim3(256), 0, st, rows, cols, ld,
+                     (const __bf16*)x, y);
   return hipGetLastError();
 }
 
