@@ -415,19 +415,7 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
 
-  // stationary activation tile: As[kq][m] = vector kq of row m0 + m, with
-  // the bias slots set to 1
   const int KQ = Kpad / P::KV;
-  for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
-    const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
-    As[kq * VTM + m] = with_bias_ones<P>(
-        load_a_vec<P>(row >= M ? nullptr
-                      : t16    ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
-                               : (const char*)(t + (int64_t)row * E),
-                      t16, E, kq * P::KV),
-        kq, E, nb);
-  }
-  __syncthreads();
 
   // This slice's 32-column blocks, balanced over the slices, in groups of VFN
   // (the packed matrix has one more, all zero, past the last one with
@@ -471,6 +459,20 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   f32x4 ring[VPF][VFN];
 #pragma unroll
   for (int p = 0; p < VPF; ++p) load(ring[p], sbase + p * kbytes);
+
+  // Stationary activation tile: As[kq][m] = vector kq of row m0 + m, with
+  // the bias slots set to 1.  Staged after the first weight loads went out,
+  // so their latency and the tile's overlap.
+  for (int idx = threadIdx.x; idx < KQ * VTM; idx += VNW * 64) {
+    const int m = idx % VTM, kq = idx / VTM, row = m0 + m;
+    As[kq * VTM + m] = with_bias_ones<P>(
+        load_a_vec<P>(row >= M ? nullptr
+                      : t16    ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
+                               : (const char*)(t + (int64_t)row * E),
+                      t16, E, kq * P::KV),
+        kq, E, nb);
+  }
+  __syncthreads();
   const f32x4* arow = As + h * VTM + l32;  // + 2*kg*VTM per k group
   f32x4 ae[FM], ao[FM];
 #pragma unroll
