@@ -268,13 +268,19 @@ nmt_status hip_fail(hipError_t e, const char* what) {
 
 // K split of a small-tile plain GEMM: enough blocks for about four per CU,
 // at least four K chunks per block.
+// Blocks a split-K launch aims for (measured on the readout: fp32 1024, so
+// 4 splits at B = 2000; bf16 512, which leaves B = 4096 unsplit, 6.5 us
+// faster than 2 splits and their reduction).
 #ifndef NMT_SPLITK_BLOCKS
 #define NMT_SPLITK_BLOCKS 1024
 #endif
-int plain_ksplit(int M, int N, int K_total, int kc, Tile t) {
+#ifndef NMT_SPLITK_BLOCKS_BF16
+#define NMT_SPLITK_BLOCKS_BF16 512
+#endif
+int plain_ksplit(int M, int N, int K_total, int kc, Tile t, bool bf16) {
   const int tiles = ceil_div(M, tile_m(t)) * ceil_div(N, tile_n(t));
   const int nc = ceil_div(K_total, kc);
-  int ks = ceil_div(NMT_SPLITK_BLOCKS, tiles);
+  int ks = ceil_div(bf16 ? NMT_SPLITK_BLOCKS_BF16 : NMT_SPLITK_BLOCKS, tiles);
   if (ks > nc / 4) ks = nc / 4;
   if (ks > 8) ks = 8;
   return ks < 1 ? 1 : ks;
@@ -305,7 +311,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
