@@ -20,6 +20,7 @@ bounded row sample on the host cores.
   python bench.py --forest             # ScoreBatch over a prefix-tree forest (separate line)
   python bench.py --ensemble K         # K models per step and their parameter average (separate line)
   python bench.py --rescore            # stack rescoring of one sentence's synthetic stacks (separate line)
+  python bench.py --library-gemms      # the vendor GEMM library on the step's shapes (context, separate line)
 """
 from __future__ import annotations
 
@@ -127,6 +128,46 @@ def copy_probe(nbytes: int, reps: int = 5):
         y.copy_(x)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes": n * 4, "reps": reps}), flush=True)
+
+
+def library_gemms(args, reps: int = 20):
+    """The vendor GEMM library (torch.matmul: hipBLASLt) on the step's GEMM
+    shapes at the workload's weight precision, plain products without the
+    kernels' fused epilogues (no GRU cell, no tanh, no log-sum-exp; the vocab
+    product writes its B x V logits), plus a large square product as the
+    library's best case.  Context for the kernels' fractions of peak; none of
+    this is on the scoring path."""
+    import torch
+    from paper_1605_04809_amd.workloads import CONFIGS
+    cfg = CONFIGS[args.config]
+    dt = torch.bfloat16 if cfg.wtype == "bf16" else torch.float32
+    torch.backends.cuda.matmul.allow_tf32 = False
+    B, E, H, A, V = cfg.B, cfg.E, cfg.H, cfg.A, cfg.V
+    C = 2 * H
+    shapes = {"query": (B, H, A), "gru1": (B, E + H, 3 * H), "gru2": (B, H + C, 3 * H),
+              "readout": (B, H + E + C, E), "vocab": (B, E, V), "square_8192": (8192, 8192, 8192)}
+    out = {}
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    for name, (M, K, N) in shapes.items():
+        a = torch.tanh(torch.randn(M, K, device="cuda", generator=gen)).to(dt)
+        b = (torch.randn(K, N, device="cuda", generator=gen) * cfg.sigma_w).to(dt)
+        c = torch.empty(M, N, device="cuda", dtype=dt)
+        for _ in range(5):
+            torch.matmul(a, b, out=c)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, b, out=c)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tf = 2.0 * M * K * N / (ms * 1e-3) / 1e12
+        out[name] = {"M": M, "K": K, "N": N, "us": round(ms * 1e3, 2), "tflops": round(tf, 1),
+                     "frac": round(tf / PEAK_TFLOPS[cfg.wtype], 4)}
+        del a, b, c
+    print(json.dumps({"metric": "library GEMM TFLOP/s on the step's shapes", "library": "torch.matmul (hipBLASLt)",
+                      "dtype": cfg.wtype, "reps": reps, "config": {"workload": cfg.name}, "gemms": out}), flush=True)
 
 
 def forest_bench(args):
@@ -372,6 +413,7 @@ def main():
     ap.add_argument("--ensemble", type=int, default=0, help="K models per step (separate line)")
     ap.add_argument("--rescore", action="store_true", help="stack rescoring of one sentence (separate line)")
     ap.add_argument("--stack-size", type=int, default=1000)
+    ap.add_argument("--library-gemms", action="store_true", help="vendor GEMM library on the step's shapes")
     args = ap.parse_args()
     if args.print_kernel_hash:
         print(kernel_source_hash())
@@ -398,6 +440,9 @@ def main():
         return
     if args.rescore:
         rescore_bench(args)
+        return
+    if args.library_gemms:
+        library_gemms(args)
         return
 
     from paper_1605_04809_amd import binding as nb

@@ -25,6 +25,9 @@ constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;  // 4 waves of 64 x 64
 #ifndef NMT_GRU_WM
 #define NMT_GRU_WM 32
 #endif
+#ifndef NMT_GRU_TM_BF16
+#define NMT_GRU_TM_BF16 128
+#endif
 #ifndef NMT_GRU_HB_BF16
 #define NMT_GRU_HB_BF16 64
 #endif
@@ -32,7 +35,7 @@ constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;  // 4 waves of 64 x 64
 #define NMT_GRU_WM_BF16 32
 #endif
 constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
-constexpr int kGruHB16 = NMT_GRU_HB_BF16, kGruWM16 = NMT_GRU_WM_BF16;  // bf16 weights
+constexpr int kGruTM16 = NMT_GRU_TM_BF16, kGruHB16 = NMT_GRU_HB_BF16, kGruWM16 = NMT_GRU_WM_BF16;  // bf16 weights
 inline int gru_hb(bool bf16) { return bf16 ? kGruHB16 : kGruHB; }
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)

@@ -309,9 +309,9 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   for (int i = 0; i < nprob; ++i)
     if (!segments_loadable(probs[i].A, probs[i].Npad, bf16)) return hipErrorInvalidValue;
   if (bf16) {
-    dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB16), nprob);
-    constexpr int threads = (kGruTM / kGruWM16) * (kGruHB16 / 32) * 64;
-    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB16, kGruWM16, PrecBF16>), grid, dim3(threads), 0, st, b);
+    dim3 grid(ceil_div(M, kGruTM16), ceil_div(H, kGruHB16), nprob);
+    constexpr int threads = (kGruTM16 / kGruWM16) * (kGruHB16 / 32) * 64;
+    hipLaunchKernelGGL((k_gemm_gru<kGruTM16, kGruHB16, kGruWM16, PrecBF16>), grid, dim3(threads), 0, st, b);
   } else {
     dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
     constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
