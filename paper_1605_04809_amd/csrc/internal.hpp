@@ -10,6 +10,7 @@
 namespace nmt {
 
 constexpr int kMaxTpad = 1024;     // attention keeps one score per source position in LDS
+constexpr int kNumCUs = 256;       // MI355X compute units (8 XCDs of 32)
 
 // K chunk of the GEMM tiles: 8 sixteen-byte vectors of 4 fp32 or 8 bf16.
 inline int chunk_k(bool bf16) { return bf16 ? PrecBF16::KC : PrecF32::KC; }
@@ -141,6 +142,12 @@ constexpr int kAttnGroup = NMT_ATTN_GROUP;
 #define NMT_ATTN_WAVES 8
 #endif
 constexpr int kAttnWaves = NMT_ATTN_WAVES;
+#ifndef NMT_ATTN_CU
+#define NMT_ATTN_CU 4
+#endif
+#ifndef NMT_ATTN_SNAKE
+#define NMT_ATTN_SNAKE 1
+#endif
 struct AttnGroups {
   int32_t* perm;
   int4* tiles;

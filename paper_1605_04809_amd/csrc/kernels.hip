@@ -625,7 +625,7 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 
 int vocab_slices(int M, int V, bool bf16) {
   const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
-  int nS = 8 * ceil_div(ceil_div(256, nM), 8);  // fill the 256 CUs (one block per CU)
+  int nS = 8 * ceil_div(ceil_div(kNumCUs, nM), 8);  // fill the CUs (one block per CU)
   const int NB = (V + 31) / 32;
   while (nS > 8 && nS > NB) nS -= 8;
   return nS;
@@ -1108,8 +1108,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
     f32x4 acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = zero4();
-    for (int i = 0; i < L; ++i) {
-      const f32x4 x = X[(int64_t)i * C4 + k4];
+    auto add = [&](const f32x4& x, int i) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float a = e[g * Tpad + i];
@@ -1118,7 +1117,20 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
         acc[g][2] += a * x[2];
         acc[g][3] += a * x[3];
       }
+    };
+    // NMT_ATTN_CU annotations are loaded before any is used, so that many
+    // loads are in flight per wave instead of one or two (each round trip to
+    // L2 or beyond is otherwise paid once per position); the sums still run
+    // over the positions in order.
+    int i = 0;
+    for (; i + NMT_ATTN_CU <= L; i += NMT_ATTN_CU) {
+      f32x4 x[NMT_ATTN_CU];
+#pragma unroll
+      for (int u = 0; u < NMT_ATTN_CU; ++u) x[u] = X[(int64_t)(i + u) * C4 + k4];
+#pragma unroll
+      for (int u = 0; u < NMT_ATTN_CU; ++u) add(x[u], i + u);
     }
+    for (; i < L; ++i) add(X[(int64_t)i * C4 + k4], i);
 #pragma unroll
     for (int g = 0; g < G; ++g)
       if (g < n) store_c4(c, (int64_t)rows[g] * C + 4 * k4, acc[g], c_bf16);
@@ -1137,7 +1149,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
     int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ ctx,
     const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
-    float* __restrict__ alpha, int c_bf16) {
+    float* __restrict__ alpha, int c_bf16, int round) {
   constexpr int NW = kAttnWaves, NT = NW * 64;
   extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
   __shared__ int rows[G];
@@ -1146,9 +1158,18 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attention_grouped(
   const int A4 = A / 4, C4 = C / 4;
   f32x4* qs = dyn;
   float* e = (float*)(dyn + G * A4);
-  if ((int)blockIdx.x >= nt) return;
-  attention_tile<G, NQ>(tiles[blockIdx.x], A, C, Tpad, q, kfac, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
-                        lane, A4, C4, c_bf16);
+  int t = blockIdx.x;
+  if (t >= nt) return;
+  // Blocks are handed to the CUs in order, one per CU per round of `round`
+  // blocks, and the tiles come longest first.  Every other round takes its
+  // tiles in reverse, so the CU that got the longest tile of one round gets
+  // the shortest of the next, and the CUs' total lengths even out.
+  if (round > 0) {
+    const int r = t / round, p = t - r * round;
+    if (r & 1) t = r * round + (min(round, nt - r * round) - 1 - p);
+  }
+  attention_tile<G, NQ>(tiles[t], A, C, Tpad, q, kfac, ctx, len, perm, v, c, alpha, qs, e, rows, wave, lane, A4,
+                        C4, c_bf16);
 }
 
 template <int G, int NQ>
@@ -1157,8 +1178,9 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
                               float* alpha, int c_bf16, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
   const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
+  const int round = NMT_ATTN_SNAKE ? kNumCUs : 0;
   hipLaunchKernelGGL((k_attention_grouped<G, NQ>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C, Tpad, q, kfac, ctx, len,
-                     grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16);
+                     grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
 }
 
 template <int NQ>
