@@ -531,7 +531,28 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-__device__ __forceinline__ float sigmoidf_(float x) { return 1.f / (1.f + expf(-x)); }
+// The cells' nonlinearities through the hardware's 2^x and reciprocal
+// (about one ulp each) instead of the libm functions and an IEEE divide
+// (some 80 instructions per GRU unit): sigma(x) = 1 / (1 + 2^{-x log2 e}),
+// tanh(x) = 1 - 2 / (2^{2x log2 e} + 1).  Absolute error a few 1e-7; both
+// saturate exactly (2^x overflows to inf, whose reciprocal is 0).
+#ifndef NMT_FAST_CELL
+#define NMT_FAST_CELL 1
+#endif
+__device__ __forceinline__ float sigmoidf_(float x) {
+#if NMT_FAST_CELL
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-kLog2e * x));
+#else
+  return 1.f / (1.f + expf(-x));
+#endif
+}
+__device__ __forceinline__ float tanhf_(float x) {
+#if NMT_FAST_CELL
+  return fmaf(-2.f, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(2.f * kLog2e * x) + 1.f), 1.f);
+#else
+  return tanhf(x);
+#endif
+}
 
 // Row of accumulator register r for lane half h.
 __device__ __forceinline__ int acc_row(int r, int h) { return 8 * (r >> 2) + 4 * h + (r & 3); }

@@ -100,7 +100,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
         const int row = m0 + wm0 + 32 * i + acc_row(r, h);
         if (row >= A.M) continue;
         float v = acc[i][j][r] + bn;
-        if (ep.act == 1) v = tanhf(v);
+        if (ep.act == 1) v = tanhf_(v);
         if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
         if (ep.out16)
           ep.out16[(int64_t)row * ep.ldo + n] = (__bf16)v;
@@ -118,7 +118,7 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
   float v = 0.f;
   for (int z = 0; z < ksplit; ++z) v += part[(int64_t)z * M * N + i];
   v += ep.bias ? ep.bias[n] : 0.f;
-  if (ep.act == 1) v = tanhf(v);
+  if (ep.act == 1) v = tanhf_(v);
   if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
   if (ep.out16)
     ep.out16[(int64_t)row * ep.ldo + n] = (__bf16)v;
@@ -287,7 +287,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatc
       const int i = (g0 + q) / 16, r = (g0 + q) % 16;
       const float rg = sigmoidf_(ar[i][r] + br + xr[q]);
       const float zg = sigmoidf_(az[i][r] + bz + xz[q]);
-      const float ng = tanhf(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
+      const float ng = tanhf_(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
       float hn = zg * hp[q] + (1.f - zg) * ng;
       if (!keep[q]) hn = 0.f;
       if (rowq[q] < M) {
