@@ -309,7 +309,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   L.nS = vocab_slices((int)B, m->dims.V, m->bf16);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
-  L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay
+  L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay (B = 1000: 28 -> 32 us)
 
   L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16);
   size_t kp = 0;

@@ -38,6 +38,15 @@ constexpr int kPlainLargeTM = 128, kPlainLargeTN = 128;  // 4 waves of 64 x 64
 constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
 constexpr int kGruTM16 = NMT_GRU_TM_BF16, kGruHB16 = NMT_GRU_HB_BF16, kGruWM16 = NMT_GRU_WM_BF16;  // bf16 weights
 inline int gru_hb(bool bf16) { return bf16 ? kGruHB16 : kGruHB; }
+// Rows of the GRU tile for small batches, used when the large tile would
+// give fewer than kGruSmallBlocks blocks.
+#ifndef NMT_GRU_SMALL_TM
+#define NMT_GRU_SMALL_TM 64
+#endif
+#ifndef NMT_GRU_SMALL_BLOCKS
+#define NMT_GRU_SMALL_BLOCKS 256
+#endif
+constexpr int kGruSmallTM = NMT_GRU_SMALL_TM, kGruSmallBlocks = NMT_GRU_SMALL_BLOCKS;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 

@@ -178,7 +178,8 @@ struct GruBatch {
 };
 
 template <int TM, int HB, int WM, class P>
-__global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) void k_gemm_gru(GruBatch batch) {
+__global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_gemm_gru(
+    GruBatch batch) {
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
@@ -308,14 +309,31 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   if (M <= 0) return hipSuccess;
   for (int i = 0; i < nprob; ++i)
     if (!segments_loadable(probs[i].A, probs[i].Npad, bf16)) return hipErrorInvalidValue;
+  // Batches too small to give every CU a block of the large tile (a forest
+  // level of about 1,000 rows, the encoder's recurrence) take blocks of
+  // kGruSmallTM rows instead, twice as many, which run two to a CU.
+  auto run = [&](auto tm, auto hb, auto wm, auto prec) {
+    constexpr int TM = decltype(tm)::value, HB = decltype(hb)::value, WM = decltype(wm)::value;
+    using P = decltype(prec);
+    dim3 grid(ceil_div(M, TM), ceil_div(H, HB), nprob);
+    hipLaunchKernelGGL((k_gemm_gru<TM, HB, WM, P>), grid, dim3((TM / WM) * (HB / 32) * 64), 0, st, b);
+  };
+  const int tm_large = bf16 ? kGruTM16 : kGruTM, hb = gru_hb(bf16);
+  const bool small = (int64_t)ceil_div(M, tm_large) * ceil_div(H, hb) * nprob < kGruSmallBlocks;
   if (bf16) {
-    dim3 grid(ceil_div(M, kGruTM16), ceil_div(H, kGruHB16), nprob);
-    constexpr int threads = (kGruTM16 / kGruWM16) * (kGruHB16 / 32) * 64;
-    hipLaunchKernelGGL((k_gemm_gru<kGruTM16, kGruHB16, kGruWM16, PrecBF16>), grid, dim3(threads), 0, st, b);
+    if (small)
+      run(std::integral_constant<int, kGruSmallTM>{}, std::integral_constant<int, kGruHB16>{},
+          std::integral_constant<int, kGruWM16>{}, PrecBF16{});
+    else
+      run(std::integral_constant<int, kGruTM16>{}, std::integral_constant<int, kGruHB16>{},
+          std::integral_constant<int, kGruWM16>{}, PrecBF16{});
   } else {
-    dim3 grid(ceil_div(M, kGruTM), ceil_div(H, kGruHB), nprob);
-    constexpr int threads = (kGruTM / kGruWM) * (kGruHB / 32) * 64;
-    hipLaunchKernelGGL((k_gemm_gru<kGruTM, kGruHB, kGruWM, PrecF32>), grid, dim3(threads), 0, st, b);
+    if (small)
+      run(std::integral_constant<int, kGruSmallTM>{}, std::integral_constant<int, kGruHB>{},
+          std::integral_constant<int, kGruWM>{}, PrecF32{});
+    else
+      run(std::integral_constant<int, kGruTM>{}, std::integral_constant<int, kGruHB>{},
+          std::integral_constant<int, kGruWM>{}, PrecF32{});
   }
   return hipGetLastError();
 }
