@@ -641,12 +641,30 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   }
 }
 
+// Slices per row tile: the multiple of 8 (one per XCD) whose launch finishes
+// first.  A block holds one CU, so a launch of nM x nS blocks runs in
+// ceil(nM nS / CUs) rounds, each as long as one block: NB / nS column blocks
+// plus a fixed cost (staging the activation tile, the final merge) of about
+// kVocabBlockFixed column blocks.  Batches whose row tiles divide the CUs
+// evenly get one round (2000 rows: 8 slices); the others, more rounds of
+// shorter blocks (1445 rows: 32 slices in three rounds instead of 16 in
+// two, 25 % less time).
+constexpr int kVocabBlockFixed = 4;
+constexpr int kVocabMaxSlices = 256;
 int vocab_slices(int M, int V, bool bf16) {
   const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
-  int nS = 8 * ceil_div(ceil_div(kNumCUs, nM), 8);  // fill the CUs (one block per CU)
   const int NB = (V + 31) / 32;
-  while (nS > 8 && nS > NB) nS -= 8;
-  return nS;
+  int best = 8;
+  double best_cost = 0;
+  for (int nS = 8; nS <= kVocabMaxSlices && (nS == 8 || nS <= NB); nS += 8) {
+    const double rounds = (double)ceil_div((int64_t)nM * nS, kNumCUs);
+    const double cost = rounds * ((double)NB / nS + kVocabBlockFixed);
+    if (nS == 8 || cost < best_cost) {
+      best_cost = cost;
+      best = nS;
+    }
+  }
+  return best;
 }
 
 // The vocabulary kernel addresses the packed weights with 32-bit byte offsets.
