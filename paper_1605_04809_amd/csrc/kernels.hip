@@ -319,7 +319,11 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
     hipLaunchKernelGGL((k_gemm_gru<TM, HB, WM, P>), grid, dim3((TM / WM) * (HB / 32) * 64), 0, st, b);
   };
   const int tm_large = bf16 ? kGruTM16 : kGruTM, hb = gru_hb(bf16);
-  const bool small = (int64_t)ceil_div(M, tm_large) * ceil_div(H, hb) * nprob < kGruSmallBlocks;
+  // fp32 also when the large tile's last round would be at most half full
+  // (B = 2500 and 3000: GRU2 544 -> 434-440 us); bf16 there measured slower.
+  const int64_t nbl = (int64_t)ceil_div(M, tm_large) * ceil_div(H, hb) * nprob;
+  const int64_t last = nbl % kNumCUs;
+  const bool small = nbl < kGruSmallBlocks || (!bf16 && last != 0 && last <= kNumCUs / 2);
   if (bf16) {
     if (small)
       run(std::integral_constant<int, kGruSmallTM>{}, std::integral_constant<int, kGruHB16>{},
