@@ -296,6 +296,26 @@ def test_paper_sized_step_sampled_rows(gpu, name):
     g.close()
 
 
+@pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "bf16")])
+def test_launch_shape_boundaries_sampled_rows(gpu, B, wtype):
+    """Batches between the tile choices at the paper's dimensions: B = 2600
+    takes the 64-row GRU tile with more than a round of 128-row blocks
+    (fp32), B = 1445 takes 32 vocabulary slices over 23 row tiles, B = 667
+    (bf16) 64-row GRU blocks and many slices; oracle on sampled rows."""
+    _torch()
+    wl = make_workload(CONFIGS["enru_b2000"].replace(B=B, wtype=wtype, seed=43))
+    g = gpu.GpuRun(wl)
+    out = g.step(wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
+    rows = sample_rows(B, 24, seed=44)
+    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
+    if wtype == "bf16":
+        compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16)
+    else:
+        compare(out, ref, rows=rows)
+    g.close()
+
+
 @pytest.mark.parametrize("wtype", ["f32", "bf16"])
 def test_large_batch_sampled_rows(gpu, wtype):
     """16 times the benchmarked batch: B = 32768 rows over 64 sentences at
