@@ -301,7 +301,7 @@ def test_launch_shape_boundaries_sampled_rows(gpu, B, wtype):
     """Batches between the tile choices at the paper's dimensions: B = 2600
     takes the 64-row GRU tile with more than a round of 128-row blocks
     (fp32), B = 1445 takes 32 vocabulary slices over 23 row tiles, B = 667
-    (bf16) 64-row GRU blocks and many slices; oracle on sampled rows."""
+    (bf16) 64-row GRU blocks and 40 slices; oracle on sampled rows."""
     _torch()
     wl = make_workload(CONFIGS["enru_b2000"].replace(B=B, wtype=wtype, seed=43))
     g = gpu.GpuRun(wl)
