@@ -94,6 +94,8 @@ struct nmt_source {
   Allocs mem;
   float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
   float* kfac = nullptr;  // 2^{2 log2(e) pctx}: the keys' factors of the attention scores
+  float* gru_part = nullptr;  // encoder: the recurrent GRU's split-K sums [2][enc_ks][S][4H]
+  int enc_ks = 1;
   int32_t* len = nullptr;
   std::vector<int32_t> h_len;
 };
@@ -331,6 +333,17 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   return L;
 }
 
+// K splits of the encoder's recurrent GRU: its S rows give few tiles
+// (S <= 64: 16 column tiles x 2 directions), so each step's K chunks are
+// split until the blocks cover the CUs, at least two chunks per split.
+int encoder_ksplit(const nmt_model* m, int S) {
+  const int base = ceil_div(S, kGruSmallTM) * ceil_div(m->dims.H, gru_hb(m->bf16)) * 2;
+  const int nc = ceil_div(m->dims.H, m->kc);
+  int ks = kNumCUs / base;
+  if (ks > nc / 2) ks = nc / 2;
+  return ks < 1 ? 1 : ks;
+}
+
 nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_len, bool with_scratch,
                       hipStream_t st, nmt_source** out) {
   const nmt_dims& d = m->dims;
@@ -350,6 +363,11 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->kfac, rows * d.A * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->len, S * sizeof(int32_t));
   if (e == hipSuccess && with_scratch) e = src->mem.alloc((void**)&src->scratch, rows * 6 * d.H * sizeof(float));
+  if (e == hipSuccess && with_scratch) {
+    src->enc_ks = encoder_ksplit(m, S);
+    if (src->enc_ks > 1)
+      e = src->mem.alloc((void**)&src->gru_part, (size_t)2 * src->enc_ks * S * 4 * d.H * sizeof(float));
+  }
   if (e == hipSuccess)
     e = hipMemcpyAsync(src->len, src->h_len.data(), S * sizeof(int32_t), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) {
@@ -534,7 +552,9 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
       g.ep = GruEpi{hprev, ldc, nullptr, 0, Xp + (int64_t)pos * 6 * H + dir * 3 * H, ldx, m->enc_bias.brz, m->enc_bias.bni,
                     m->enc_bias.bns, src->ctx + (int64_t)pos * C + dir * H, ldc, src->len, pos, H};
     }
-    e = launch_gemm_gru(p, 2, H, m->bf16, st);
+    const bool split = src->enc_ks > 1 && p[0].A.nseg > 0 && p[1].A.nseg > 0;
+    e = split ? launch_gemm_gru_split(p, 2, H, m->bf16, src->enc_ks, src->gru_part, S, st)
+              : launch_gemm_gru(p, 2, H, m->bf16, st);
   }
   if (e == hipSuccess) e = source_keys(m, src, st);
   if (e == hipSuccess && d_s0_out) {

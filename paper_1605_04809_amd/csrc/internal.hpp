@@ -115,6 +115,11 @@ struct GruProblem {
 // Launchers (all asynchronous on `st`).
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st);
+// The same with the K chunks split over ksplit blocks per tile: raw sums go
+// to part [nprob][ksplit][part_M][4][H] (part_M >= every problem's rows), a
+// second kernel adds them in split order and applies the cell.
+hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool bf16, int ksplit, float* part,
+                                 int part_M, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
 int vocab_slices(int M, int V, bool bf16);

@@ -175,16 +175,36 @@ hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const P
 
 struct GruBatch {
   GruProblem p[2];
+  int32_t ksplit;  // SPLIT kernels: K splits per problem (blockIdx.z = problem * ksplit + split)
+  float* part;     // SPLIT kernels: raw sums [problem][split][M][4][H] (r, z, input and state candidate)
+  int32_t part_M;  // rows of each problem's part block
 };
 
-template <int TM, int HB, int WM, class P>
+// The cell of Section 5.1's GRUs from the gate pre-activations (without
+// biases) and the previous state.
+__device__ __forceinline__ float gru_cell(float sr, float sz, float sni, float sns, float br, float bz, float bni,
+                                          float bns, float xr, float xz, float xn, float hp) {
+  const float rg = sigmoidf_(sr + br + xr);
+  const float zg = sigmoidf_(sz + bz + xz);
+  const float ng = tanhf_(sni + bni + xn + rg * (sns + bns));
+  return zg * hp + (1.f - zg) * ng;
+}
+
+// SPLIT: the block sums only its split's share of the K chunks (of all A
+// segments together) and writes the raw sums to batch.part; k_gru_cell adds
+// the splits in order and applies the cell.  For launches with few row
+// tiles (the encoder's recurrence over S rows), which would otherwise leave
+// most CUs idle.
+template <int TM, int HB, int WM, class P, bool SPLIT = false>
 __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_gemm_gru(
     GruBatch batch) {
   constexpr int TN = 3 * HB;
   constexpr int NT = (TM / WM) * (HB / 32) * 64;
   constexpr int FM = WM / 32;
   __shared__ f32x4 lds[2 * (a_rows<TM, P>() + TN) * P::KQ];
-  const GruProblem& Pb = batch.p[blockIdx.z];
+  const int prob = SPLIT ? (int)blockIdx.z / batch.ksplit : (int)blockIdx.z;
+  const int split = SPLIT ? (int)blockIdx.z % batch.ksplit : 0;
+  const GruProblem& Pb = batch.p[prob];
   const f32x4* Wp = (const f32x4*)Pb.Wp;
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -220,18 +240,29 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
   // One main loop per A segment, each with its side fixed at compile time:
   // a per-chunk branch between the two candidate accumulators would make the
   // compiler shuttle every accumulator between AGPRs and VGPRs each chunk.
+  // this block's global chunk range (all of them without a split)
+  int c_begin = 0, c_end = 1 << 30;
+  if constexpr (SPLIT) {
+    const int nc = total_chunks(Pb.A);
+    c_begin = (int)((int64_t)nc * split / batch.ksplit);
+    c_end = (int)((int64_t)nc * (split + 1) / batch.ksplit);
+  }
   int64_t vq0 = 0;
+  int s0 = 0;
   for (int sg = 0; sg < Pb.A.nseg; ++sg) {
     const ASeg seg = seg_at(Pb.A, sg);
+    const int cb = c_begin > s0 ? c_begin - s0 : 0;
+    const int ce = c_end - s0 < seg.nchunk ? c_end - s0 : seg.nchunk;
     if (seg.side)
       gemm_segment<TM, TN, NT, P, kGruLA<P>, KS>(
           seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
-          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); }, vq0, 0, seg.nchunk);
+          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::true_type{}); }, vq0, cb, ce);
     else
       gemm_segment<TM, TN, NT, P, kGruLA<P>, KS>(
           seg, Pb.A.M, Wp, Pb.Npad, m0, n0, lds,
-          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); }, vq0, 0, seg.nchunk);
+          [&](const f32x4* As, const f32x4* Bs) { chunk(As, Bs, std::false_type{}); }, vq0, cb, ce);
     vq0 += (int64_t)seg.nchunk * P::KQ;
+    s0 += seg.nchunk;
   }
 
   const GruEpi& ep = Pb.ep;
@@ -239,6 +270,22 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
   const int H = ep.H, M = Pb.A.M;
   const int j = blockIdx.y * HB + wu0 + l32;
   if (j >= H) return;
+  if constexpr (SPLIT) {
+    float* part = batch.part + ((int64_t)prob * batch.ksplit + split) * batch.part_M * 4 * H;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm0 + 32 * i + acc_row(r, h);
+        if (row >= M) continue;
+        float* o = part + (int64_t)row * 4 * H + j;
+        o[0] = ar[i][r];
+        o[H] = az[i][r];
+        o[2 * H] = ani[i][r];
+        o[3 * H] = ans[i][r];
+      }
+    return;
+  }
   const float br = ep.brz[j], bz = ep.brz[H + j], bni = ep.bni[j], bns = ep.bns[j];
   // The cell's other inputs for this lane's rows, 8 rows at a time, every
   // load of a group issued before any value is used (addresses clamped to
@@ -286,10 +333,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
       const int i = (g0 + q) / 16, r = (g0 + q) % 16;
-      const float rg = sigmoidf_(ar[i][r] + br + xr[q]);
-      const float zg = sigmoidf_(az[i][r] + bz + xz[q]);
-      const float ng = tanhf_(ani[i][r] + bni + xn[q] + rg * (ans[i][r] + bns));
-      float hn = zg * hp[q] + (1.f - zg) * ng;
+      float hn = gru_cell(ar[i][r], az[i][r], ani[i][r], ans[i][r], br, bz, bni, bns, xr[q], xz[q], xn[q], hp[q]);
       if (!keep[q]) hn = 0.f;
       if (rowq[q] < M) {
         ep.out[(int64_t)rowq[q] * ep.ldo + j] = hn;
@@ -339,6 +383,73 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
       run(std::integral_constant<int, kGruTM>{}, std::integral_constant<int, kGruHB>{},
           std::integral_constant<int, kGruWM>{}, PrecF32{});
   }
+  return hipGetLastError();
+}
+
+// Adds the K splits of a SPLIT launch in split order and applies the cell,
+// with the same inputs and outputs as the fused epilogue.  One thread per
+// (row, hidden unit) of problem blockIdx.y.
+__global__ void k_gru_cell(GruBatch batch, int H) {
+  const GruProblem& Pb = batch.p[blockIdx.y];
+  const GruEpi& ep = Pb.ep;
+  const int M = Pb.A.M;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)M * H) return;
+  const int row = (int)(i / H), j = (int)(i % H);
+  const int64_t stride = (int64_t)batch.part_M * 4 * H;
+  const float* p = batch.part + (int64_t)blockIdx.y * batch.ksplit * stride + (int64_t)row * 4 * H + j;
+  float sr = 0.f, sz = 0.f, sni = 0.f, sns = 0.f;
+  for (int z = 0; z < batch.ksplit; ++z, p += stride) {
+    sr += p[0];
+    sz += p[H];
+    sni += p[2 * H];
+    sns += p[3 * H];
+  }
+  float hp = 0.f, xr = 0.f, xz = 0.f, xn = 0.f;
+  if (ep.h) {
+    const int hr = ep.hrow ? ep.hrow[row] : row;
+    if (!ep.hrow || (hr >= 0 && hr < ep.hrows)) hp = ep.h[(int64_t)hr * ep.ldh + j];
+  }
+  if (ep.xin) {
+    const float* x = ep.xin + (int64_t)row * ep.ldx;
+    xr = x[j];
+    xz = x[H + j];
+    xn = x[2 * H + j];
+  }
+  float hn = gru_cell(sr, sz, sni, sns, ep.brz[j], ep.brz[H + j], ep.bni[j], ep.bns[j], xr, xz, xn, hp);
+  if (ep.mask_len && ep.mask_pos >= ep.mask_len[row]) hn = 0.f;
+  ep.out[(int64_t)row * ep.ldo + j] = hn;
+  if (ep.out16) ep.out16[(int64_t)row * ep.ldo + j] = (__bf16)hn;
+}
+
+hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool bf16, int ksplit, float* part,
+                                 int part_M, hipStream_t st) {
+  if (nprob < 1 || nprob > 2 || ksplit < 1 || !part) return hipErrorInvalidValue;
+  GruBatch b;
+  b.p[0] = probs[0];
+  b.p[1] = nprob > 1 ? probs[1] : probs[0];
+  b.ksplit = ksplit;
+  b.part = part;
+  b.part_M = part_M;
+  int M = 0;
+  for (int i = 0; i < nprob; ++i) {
+    if (probs[i].A.M > part_M) return hipErrorInvalidValue;
+    if (!segments_loadable(probs[i].A, probs[i].Npad, bf16)) return hipErrorInvalidValue;
+    M = M > probs[i].A.M ? M : probs[i].A.M;
+  }
+  if (M <= 0) return hipSuccess;
+  constexpr int TM = kGruSmallTM;
+  if (bf16)
+    hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB16, kGruWM16, PrecBF16, true>),
+                       dim3(ceil_div(M, TM), ceil_div(H, kGruHB16), nprob * ksplit),
+                       dim3((TM / kGruWM16) * (kGruHB16 / 32) * 64), 0, st, b);
+  else
+    hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB, kGruWM, PrecF32, true>),
+                       dim3(ceil_div(M, TM), ceil_div(H, kGruHB), nprob * ksplit),
+                       dim3((TM / kGruWM) * (kGruHB / 32) * 64), 0, st, b);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gru_cell, dim3(ceil_div((int64_t)M * H, (int64_t)256), nprob), dim3(256), 0, st, b, H);
   return hipGetLastError();
 }
 
