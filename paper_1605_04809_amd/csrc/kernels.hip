@@ -9,7 +9,10 @@
 //                  encoder input projections, initial state.
 //   k_gemm_gru     MFMA GEMM whose tile holds matching r, z and candidate
 //                  columns of the same hidden units, with the GRU cell fused
-//                  into the epilogue (both decoder GRUs, encoder recurrence).
+//                  into the epilogue (both decoder GRUs, encoder recurrence);
+//                  128- or 64-row tiles by batch size.  Its SPLIT form sums
+//                  a share of K and k_gru_cell adds the shares and applies
+//                  the cell (the encoder's few-row recurrence).
 //   k_vocab_lse    MFMA vocabulary projection streaming the output weights,
 //                  fused with an online log-sum-exp; logits never reach HBM.
 //   k_lse_combine  merges the per-slice partials, scores the requested word
