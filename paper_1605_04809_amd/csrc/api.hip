@@ -616,7 +616,20 @@ void nmt_source_destroy(nmt_source* src) {
 
 size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B) {
   if (!m || B <= 0) return 0;
-  return ws_layout(m, B).total;
+  // Some smaller batches need more bytes than B itself: the vocabulary
+  // kernel may take more slices for them (more partials per row), the
+  // readout more K splits.  Both choices are fixed within a run of batch
+  // sizes that fill the same number of row tiles (tiles of 64 or 128 rows,
+  // multiples of 32), where the largest size needs the most.  So the
+  // maximum over B and every multiple of 32 below it bounds every smaller
+  // call, and a workspace sized for B serves any batch up to B (a forest's
+  // levels, a shrinking batch).
+  size_t mx = ws_layout(m, B).total;
+  for (int32_t b = 32; b < B; b += 32) {
+    const size_t t = ws_layout(m, b).total;
+    if (t > mx) mx = t;
+  }
+  return mx;
 }
 
 }  // extern "C"

@@ -768,6 +768,9 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
 // shorter blocks (1445 rows: 32 slices in three rounds instead of 16 in
 // two, 25 % less time).
 constexpr int kVocabBlockFixed = 4;
+// nmt_score_workspace_bytes takes its maximum over multiples of 32 rows.
+static_assert(VocabTune<PrecF32>::VTM % 32 == 0 && VocabTune<PrecBF16>::VTM % 32 == 0 && kPlainSmallTM % 32 == 0,
+              "row tiles in whole multiples of 32");
 constexpr int kVocabMaxSlices = 256;
 int vocab_slices(int M, int V, bool bf16) {
   const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);

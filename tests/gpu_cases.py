@@ -33,14 +33,14 @@ class GpuRun:
             self.src = nb.nmt_source_from_annotations(self.model, cuda(ctx_f32), wl.src_len)
         torch.cuda.synchronize()
 
-    def step(self, s_prev, y_prev, sent_id, req, debug=True, alias=False):
+    def step(self, s_prev, y_prev, sent_id, req, debug=True, alias=False, workspace=None):
         import torch
         c = self.wl.cfg
         B = len(y_prev)
         sp = cuda(np.asarray(s_prev, np.float32))
         out = dict(logp=torch.empty(B, device="cuda"), logZ=torch.empty(B, device="cuda"))
         s_new = sp if alias else torch.empty((B, c.H), device="cuda")
-        kw = {}
+        kw = {} if workspace is None else dict(workspace=workspace)
         if debug:
             kw = dict(alpha=torch.empty((B, c.Tpad), device="cuda"), c=torch.empty((B, c.C), device="cuda"),
                       s1=torch.empty((B, c.H), device="cuda"), t=torch.empty((B, c.E), device="cuda"))
@@ -50,7 +50,8 @@ class GpuRun:
         res = {k: v.cpu().numpy() for k, v in out.items()}
         res["s_new"] = s_new.cpu().numpy()
         for k, v in kw.items():
-            res[k] = v.cpu().numpy()
+            if k != "workspace":
+                res[k] = v.cpu().numpy()
         return res
 
     def close(self):

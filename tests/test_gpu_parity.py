@@ -317,6 +317,23 @@ def test_launch_shape_boundaries_sampled_rows(gpu, B, wtype):
 
 
 @pytest.mark.parametrize("wtype", ["f32", "bf16"])
+def test_workspace_bytes_never_shrink_with_the_batch(gpu, wtype):
+    """A workspace sized for B rows serves every smaller batch (a forest's
+    levels, a shrinking phrase batch), although some smaller batches take
+    more vocabulary slices than B; and such a call runs."""
+    torch = _torch()
+    from paper_1605_04809_amd import binding as nb
+    wl = make_workload(CONFIGS["enru_b2000"].replace(B=65, S=2, len_lo=3, len_hi=5, Tpad=5, wtype=wtype, seed=45))
+    g = gpu.GpuRun(wl)
+    sizes = [nb.nmt_score_workspace_bytes(g.model, b) for b in range(1, 700)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:])), "workspace bytes shrink somewhere below 700 rows"
+    ws = torch.empty(nb.nmt_score_workspace_bytes(g.model, 65), dtype=torch.uint8, device="cuda")
+    out = g.step(wl.s_prev[:64], wl.y_prev[:64], wl.sent_id[:64], wl.req[:64], workspace=ws)
+    assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
+    g.close()
+
+
+@pytest.mark.parametrize("wtype", ["f32", "bf16"])
 def test_large_batch_sampled_rows(gpu, wtype):
     """16 times the benchmarked batch: B = 32768 rows over 64 sentences at
     the paper's dimensions (grids, 32-bit offsets, the grouping kernel and
