@@ -348,7 +348,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
 
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st) {
   if (nprob < 1 || nprob > 2) return hipErrorInvalidValue;
-  GruBatch b;
+  GruBatch b{};
   b.p[0] = probs[0];
   b.p[1] = nprob > 1 ? probs[1] : probs[0];
   int M = probs[0].A.M;
@@ -428,7 +428,7 @@ __global__ void k_gru_cell(GruBatch batch, int H) {
 hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool bf16, int ksplit, float* part,
                                  int part_M, hipStream_t st) {
   if (nprob < 1 || nprob > 2 || ksplit < 1 || !part) return hipErrorInvalidValue;
-  GruBatch b;
+  GruBatch b{};
   b.p[0] = probs[0];
   b.p[1] = nprob > 1 ? probs[1] : probs[0];
   b.ksplit = ksplit;
