@@ -156,6 +156,7 @@ constexpr int kAttnGroup = NMT_ATTN_GROUP;
 #define NMT_ATTN_WAVES 8
 #endif
 constexpr int kAttnWaves = NMT_ATTN_WAVES;
+constexpr int kAttnWideTiles = 640;  // grouped-attention launches of at most this many blocks use 2 * kAttnWaves waves
 #ifndef NMT_ATTN_CU
 #define NMT_ATTN_CU 4
 #endif
