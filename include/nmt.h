@@ -172,6 +172,30 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
                                  size_t ws_bytes, void* stream, float* d_alpha, float* d_c,
                                  float* d_s1, float* d_t);
 
+/* Size of the library's own scratch for nmt_score_batch_noalloc: 64 MiB per
+ * device.  At the paper's dimensions (E = 500, H = A = 1024, V = 100k) that
+ * holds the step of up to about 2,500 rows with fp32 weights and 2,700 with
+ * bf16 weights. */
+#define NMT_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* nmt_score_batch for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, results and errors as nmt_score_batch, without the
+ * workspace: the step's scratch is a device array of
+ * NMT_NOALLOC_SCRATCH_BYTES inside the library, one per device, set up by
+ * nmt_model_create and held until the process ends.  The call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine).
+ * Every call on a device shares that device's array, whatever the model or
+ * stream: calls that overlap in time on one device race and must be
+ * serialised by the caller (one stream, or events).  The array keeps the
+ * last call's contents; the step overwrites every byte it reads, so nothing
+ * needs clearing.  Errors: those of nmt_score_batch, and NMT_EWORKSPACE
+ * (nothing enqueued) when B rows need more than NMT_NOALLOC_SCRATCH_BYTES of
+ * scratch; a B whose nmt_score_workspace_bytes is at most that always fits. */
+nmt_status nmt_score_batch_noalloc(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                                   const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
+                                   float* d_logp, float* d_s_new, float* d_logZ, void* stream);
+
 /* One level of the ScoreBatch procedure (Section 5.1, Figure 2): a batched
  * step whose rows take their input states from a device state pool by index
  * and may request several next words each.

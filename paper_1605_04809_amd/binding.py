@@ -32,7 +32,7 @@ WEIGHT_FIELDS = (
 # Every function the header declares (checked against include/nmt.h by the tests).
 EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_from_annotations",
            "nmt_source_info", "nmt_source_destroy", "nmt_score_workspace_bytes", "nmt_score_batch",
-           "nmt_score_batch_debug", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
+           "nmt_score_batch_debug", "nmt_score_batch_noalloc", "nmt_stream_status", "nmt_last_error", "nmt_profile_begin",
            "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
            "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
@@ -87,6 +87,7 @@ def load_library(path: str = LIB_PATH):
     score = [_VP, _VP, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]
     lib.nmt_score_batch.argtypes = score
     lib.nmt_score_batch_debug.argtypes = score + [_VP, _VP, _VP, _VP]
+    lib.nmt_score_batch_noalloc.argtypes = [_VP, _VP, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
     lib.nmt_stream_status.argtypes = [_VP, _VP]
     lib.nmt_profile_begin.argtypes = [_VP, _I32]
     lib.nmt_profile_end.argtypes = [_VP, _VP, P(Timing)]
@@ -115,7 +116,7 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
-              "nmt_score_batch", "nmt_score_batch_debug", "nmt_stream_status", "nmt_profile_begin",
+              "nmt_score_batch", "nmt_score_batch_debug", "nmt_score_batch_noalloc", "nmt_stream_status", "nmt_profile_begin",
               "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
               "nmt_forest_level", "nmt_forest_pair_paths", "nmt_score_forest", "nmt_model_average",
               "nmt_score_ensemble", "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info"):
@@ -293,6 +294,19 @@ def nmt_score_batch(model: Model, src: Source, s_prev, y_prev, sent_id, req, log
         _check(lib.nmt_score_batch_debug(*args, _ptr(alpha), _ptr(c), _ptr(s1), _ptr(t)))
     else:
         _check(lib.nmt_score_batch(*args))
+
+
+# The scratch size of nmt_score_batch_noalloc (NMT_NOALLOC_SCRATCH_BYTES in nmt.h).
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def nmt_score_batch_noalloc(model: Model, src: Source, s_prev, y_prev, sent_id, req, logp, s_new, logZ=None,
+                            stream=None):
+    """nmt_score_batch on the library's own per-device scratch: allocates nothing."""
+    B = int(y_prev.shape[0])
+    _check(load_library().nmt_score_batch_noalloc(model.handle, src.handle, B, _ptr(s_prev), _ptr(y_prev),
+                                                  _ptr(sent_id), _ptr(req), _ptr(logp), _ptr(s_new), _ptr(logZ),
+                                                  _stream(stream)))
 
 
 def _handles(objs):

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -83,6 +84,7 @@ struct nmt_model {
   float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr;
   GruBias enc_bias, g1_bias, g2_bias;
   int* err = nullptr;  // sticky device error flag
+  void* noalloc_ws = nullptr;  // this device's copy of the allocation-free step's scratch array
   // event timing of the step's phases (nmt_profile.h); not thread-safe
   std::vector<hipEvent_t> prof_events;  // (NMT_NUM_PHASES + 1) per timed step
   int prof_max = 0, prof_used = 0;
@@ -391,6 +393,32 @@ hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
   return e;
 }
 
+// Scratch of nmt_score_batch_noalloc: a file-scope device array, so that
+// step allocates nothing.  Every GPU the library runs on holds its own copy
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// never the device memory: the device address of each GPU's copy is looked
+// up once per device (noalloc_scratch, called from nmt_model_create with the
+// model's device current) and only that address reaches the kernels.
+static __device__ __align__(256) char scratch[NMT_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+hipError_t noalloc_scratch(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || ((uintptr_t)p & 255)) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -486,6 +514,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   }
   step(m->mem.alloc((void**)&m->err, sizeof(int)));
   if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
+  if (e == hipSuccess) step(noalloc_scratch(m->device, &m->noalloc_ws));
   if (e == hipSuccess) step(hipDeviceSynchronize());
   if (e != hipSuccess) {
     m->mem.release();
@@ -780,6 +809,21 @@ nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const
                            float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes, void* stream) {
   return nmt_score_batch_debug(m, src, B, d_s_prev, d_y_prev, d_sent_id, d_req, d_logp, d_s_new, d_logZ, d_workspace,
                                ws_bytes, stream, nullptr, nullptr, nullptr, nullptr);
+}
+
+nmt_status nmt_score_batch_noalloc(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
+                                   const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
+                                   float* d_logp, float* d_s_new, float* d_logZ, void* stream) {
+  if (!m || !src) return fail(NMT_EINVAL, "NULL model or source");
+  if (B < 0) return fail(NMT_EINVAL, "B must be >= 0 (got %d)", B);
+  if (B == 0) return ok();
+  if (!m->noalloc_ws) return fail(NMT_EDEVICE, "the allocation-free scratch of device %d is not set up", m->device);
+  const size_t need = ws_layout(m, B).total;
+  if (need > (size_t)NMT_NOALLOC_SCRATCH_BYTES)
+    return fail(NMT_EWORKSPACE, "%d rows need %zu bytes of scratch; the allocation-free step holds %zu (use "
+                "nmt_score_batch with a workspace, or fewer rows)", B, need, (size_t)NMT_NOALLOC_SCRATCH_BYTES);
+  return nmt_score_batch(m, src, B, d_s_prev, d_y_prev, d_sent_id, d_req, d_logp, d_s_new, d_logZ, m->noalloc_ws,
+                         (size_t)NMT_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 nmt_status nmt_score_forest_step(nmt_model* m, const nmt_source* src, int32_t B, const float* d_state_pool,

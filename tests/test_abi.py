@@ -74,3 +74,14 @@ def _fresh_load(path):
         nb.load_library(path)
     finally:
         nb._lib = saved
+
+
+def test_noalloc_scratch_size_and_host_errors():
+    """The binding's copy of the allocation-free scratch size matches the
+    header, and the entry point rejects host arguments without a device."""
+    hdr = open(os.path.join(INCLUDE, "nmt.h")).read()
+    m = re.search(r"#define\s+NMT_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == nb.NOALLOC_SCRATCH_BYTES
+    lib = nb.load_library()
+    assert lib.nmt_score_batch_noalloc(None, None, 4, *([None] * 7), None) == nb.NMT_EINVAL
+    assert "NULL" in nb.last_error()
