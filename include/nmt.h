@@ -137,7 +137,11 @@ nmt_status nmt_source_info(const nmt_source* src, int32_t* S, int32_t* Tpad, con
 /* Free a source (waits for the device first).  NULL is a no-op. */
 void nmt_source_destroy(nmt_source* src);
 
-/* Bytes of device workspace nmt_score_batch needs for B rows. */
+/* Bytes of device workspace that serve nmt_score_batch (and
+ * nmt_score_forest_step) for any batch of at most B rows: some smaller
+ * batches need more than B itself (they split the vocabulary into more
+ * slices), so this is the largest need over all sizes up to B.  0 for a NULL
+ * model or B <= 0. */
 size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B);
 
 /* One batched decoder step: the forward step (H_i, P_i) <- NMT(H_{i-1}, E_i)
@@ -347,8 +351,9 @@ void nmt_rescorer_destroy(nmt_rescorer* r);
 nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h_coef, void* stream,
                              nmt_model** out);
 
-/* Workspace bytes nmt_score_ensemble needs for these K models and B rows
- * (the largest single-model step workspace; 0 for invalid arguments). */
+/* Workspace bytes that serve nmt_score_ensemble for these K models and any
+ * batch of at most B rows (the largest nmt_score_workspace_bytes over the
+ * models; 0 for invalid arguments). */
 size_t nmt_ensemble_workspace_bytes(int32_t K, nmt_model* const* models, int32_t B);
 
 /* One batched step of the same B rows under K models (1 <= K <= 32), each

@@ -96,6 +96,7 @@ struct nmt_source {
   Allocs mem;
   float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
   float* kfac = nullptr;  // 2^{2 log2(e) pctx}: the keys' factors of the attention scores
+  int32_t* kbig = nullptr;  // [S] 1 where a sentence has keys too large for their factors
   float* gru_part = nullptr;  // encoder: the recurrent GRU's split-K sums [2][enc_ks][S][4H]
   int enc_ks = 1;
   int32_t* len = nullptr;
@@ -364,6 +365,7 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->pctx, rows * d.A * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->kfac, rows * d.A * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->len, S * sizeof(int32_t));
+  if (e == hipSuccess) e = src->mem.alloc((void**)&src->kbig, S * sizeof(int32_t));
   if (e == hipSuccess && with_scratch) e = src->mem.alloc((void**)&src->scratch, rows * 6 * d.H * sizeof(float));
   if (e == hipSuccess && with_scratch) {
     src->enc_ks = encoder_ksplit(m, S);
@@ -389,7 +391,7 @@ hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
   AOperand A = make_a(src->S * src->Tpad, {make_seg(src->ctx, C, C, 0, m->kc)});
   PlainEpi ep{src->pctx, d.A, m->att_b, d.A, 0, src->len, src->Tpad};
   hipError_t e = launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
-  if (e == hipSuccess) e = launch_tanh_factors(src->pctx, src->kfac, (int64_t)src->S * src->Tpad * d.A, st);
+  if (e == hipSuccess) e = launch_key_factors(src->S, src->Tpad, d.A, src->pctx, src->kfac, src->kbig, st);
   return e;
 }
 
@@ -737,8 +739,8 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // masked attention and context
   if (e == hipSuccess) {
     const AttnGroups grp{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
-    e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->ctx, src->len, d_sent_id, src->S, m->att_v, c,
-                         d_alpha, grp, c16, st);
+    e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
+                         src->S, m->att_v, c, d_alpha, grp, c16, st);
   }
   mark(NMT_PHASE_ATTENTION + 1);
   // second GRU: s_new = GRU(c, s1)
@@ -941,12 +943,25 @@ nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h
   return ok();
 }
 
+// Bytes an ensemble step of B rows actually uses: the models run one after
+// another on the same workspace, so the largest single step.
+static size_t ensemble_need(int32_t K, nmt_model* const* models, int32_t B) {
+  size_t mx = 0;
+  for (int k = 0; k < K; ++k) {
+    const size_t b = ws_layout(models[k], B).total;
+    mx = b > mx ? b : mx;
+  }
+  return mx;
+}
+
+// The largest nmt_score_workspace_bytes over the models, so that (as for one
+// model) a workspace sized for B serves every smaller batch.
 size_t nmt_ensemble_workspace_bytes(int32_t K, nmt_model* const* models, int32_t B) {
   if (!models || K < 1 || K > kMaxModels || B <= 0) return 0;
   size_t mx = 0;
   for (int k = 0; k < K; ++k) {
     if (!models[k]) return 0;
-    const size_t b = ws_layout(models[k], B).total;
+    const size_t b = nmt_score_workspace_bytes(models[k], B);
     mx = b > mx ? b : mx;
   }
   return mx;
@@ -975,7 +990,7 @@ nmt_status nmt_score_ensemble(int32_t K, nmt_model* const* models, const nmt_sou
     if (!std::isfinite(tab.w[k])) return fail(NMT_EINVAL, "weight %d is not finite", k);
   }
   // validate everything before the first launch: a failed call enqueues nothing
-  const size_t need = nmt_ensemble_workspace_bytes(K, models, B);
+  const size_t need = ensemble_need(K, models, B);
   if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < need) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
   for (int k = 0; k < K; ++k)

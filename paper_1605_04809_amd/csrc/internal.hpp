@@ -168,15 +168,20 @@ struct AttnGroups {
   int4* tiles;
   int32_t* n_tiles;
 };
-// kfac [S x Tpad x A]: the keys' factors 2^{2 log2(e) pctx} (launch_tanh_factors).
+// kfac [S x Tpad x A]: the keys' factors 2^{2 log2(e) pctx}, kbig [S] the
+// sentences whose keys are too large for them (launch_key_factors); pctx the
+// keys themselves, which tiles with such keys and large queries score from.
 // c_bf16: the context c [B x C] is written in bf16 (nearest even) instead of fp32.
-hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac,
-                            const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
+hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+                            const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
                             hipStream_t st);
 hipError_t launch_bf16_to_f32(const void* x, int64_t rows, int cols, int64_t ld, float* y, hipStream_t st);
-// out[i] = 2^{2 log2(e) x[i]}, exponent clamped to [-126, 126] (the attention's key factors).
-hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_t st);
+// Per sentence of the keys pctx [S x Tpad x A] (A a multiple of 4):
+// kfac = 2^{2 log2(e) pctx}, exponent clamped to [-126, 126], and big[s] = 1
+// when some exponent of sentence s exceeds the range where the clamped
+// factors still score exactly (0 otherwise).
+hipError_t launch_key_factors(int S, int Tpad, int A, const float* pctx, float* kfac, int32_t* big, hipStream_t st);
 hipError_t launch_check_src_ids(int S, int Tpad, const int32_t* ids, const int32_t* len, int V_src,
                                 int* err, hipStream_t st);
 hipError_t launch_masked_copy(int S, int Tpad, int C, const float* src, const int32_t* len, float* dst,

@@ -21,9 +21,11 @@
 //                  masked MLP attention and context, rows grouped by
 //                  sentence so a block reads each key and annotation once
 //                  for several rows (k_attention: one row per block).
-//   k_tanh_factors the keys' factors 2^{2 log2(e) pctx} the attention
-//                  scores read (formed once per source).
+//   k_key_factors  the keys' factors 2^{2 log2(e) pctx} the attention
+//                  scores read, and each sentence's flag for keys too
+//                  large for them (formed once per source).
 #include <algorithm>
+#include <type_traits>
 
 #include "internal.hpp"
 
@@ -931,20 +933,46 @@ hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t,
 // encoded, the query's Q = 2^{c q} once per row, so the kernels score
 //   e'_i = sum_a w_a / (K_ia Q_a + 1)   with w = -2 v:
 // one fma, the hardware reciprocal and one fma per term (one
-// transcendental instead of an exp and a reciprocal).  The exponents are
-// clamped to [-126, 126], so K and Q are finite normal numbers; their
-// product over- or underflows exactly where tanh has saturated
-// (1 / (inf + 1) = 0, 1 / (0 + 1) = 1), and for |k|, |q| <= 43 each term is
-// the tanh form up to rounding.
+// transcendental instead of an exp and a reciprocal).
+//
+// A factor is a finite fp32 number only while |c x| < 128, so the factor
+// exponents are clamped to [-126, 126].  The product K Q is then the exact
+// 2^{c(k+q)} (up to rounding; it over- or underflows only where tanh has
+// saturated) as long as neither exponent was clamped.  It stays exact to
+// within 2^-26 of a term when one exponent is clamped and the other is at
+// most kFactorSafe in magnitude: then |c(k+q)| > 26 in both the true and
+// the clamped product, where the term is 0 or w to that precision.  Only
+// when a clamped exponent meets an opposite one above kFactorSafe can the
+// clamp change a term (k = 50, q = -49.5 would score tanh 0 instead of
+// tanh 0.5).  So each source sentence carries a flag, set when the
+// magnitude of any of its key exponents exceeds kFactorSafe, and each
+// attention tile tests its queries the same way; a tile with both scores
+// every term as w / (2^{c(k+q)} + 1) from the keys themselves (an exp2 and
+// a reciprocal per term), which is exact for any k and q.
 constexpr float kTanhScale = 2.f * kLog2e;
+constexpr float kFactorSafe = 100.f;
 __device__ __forceinline__ float tanh_factor(float x) {
   return __builtin_amdgcn_exp2f(fminf(fmaxf(x * kTanhScale, -126.f), 126.f));
 }
 __device__ __forceinline__ f32x4 tanh_factor(f32x4 x) {
   return f32x4{tanh_factor(x[0]), tanh_factor(x[1]), tanh_factor(x[2]), tanh_factor(x[3])};
 }
+// True when some factor exponent of x is beyond kFactorSafe.
+__device__ __forceinline__ bool factor_big(f32x4 x) {
+  const float m = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
+  return m * kTanhScale > kFactorSafe;
+}
 __device__ __forceinline__ float score_term(float kf, float qf, float w, float acc) {
   return fmaf(w, __builtin_amdgcn_rcpf(fmaf(kf, qf, 1.f)), acc);
+}
+// The same term from the key k and the query q themselves: exact for any
+// magnitudes (2^{c(k+q)} is inf or 0 exactly where tanh has saturated).
+__device__ __forceinline__ float score_term_exact(float k, float q, float w, float acc) {
+  return fmaf(w, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f((k + q) * kTanhScale) + 1.f), acc);
+}
+template <bool EXACT>
+__device__ __forceinline__ float score_term_t(float k, float q, float w, float acc) {
+  return EXACT ? score_term_exact(k, q, w, acc) : score_term(k, q, w, acc);
 }
 
 // Four context values at element index i of c: fp32, or (c_bf16) bf16
@@ -959,14 +987,26 @@ __device__ __forceinline__ void store_c4(float* c, int64_t i, const f32x4& v, in
   }
 }
 
-__global__ void k_tanh_factors(int64_t n, const float* __restrict__ x, float* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) out[i] = tanh_factor(x[i]);
+// The keys' factors of one sentence per block, and the sentence's flag: 1
+// when some key exponent exceeds kFactorSafe in magnitude (the positions
+// past the length hold zero keys).
+__global__ __launch_bounds__(1024) void k_key_factors(int64_t per_sentence4, const f32x4* __restrict__ x,
+                                                      f32x4* __restrict__ out, int32_t* __restrict__ big) {
+  const int64_t base = (int64_t)blockIdx.x * per_sentence4;
+  bool b = false;
+  for (int64_t i = threadIdx.x; i < per_sentence4; i += 1024) {
+    const f32x4 v = x[base + i];
+    b |= factor_big(v);
+    out[base + i] = tanh_factor(v);
+  }
+  b = __syncthreads_or(b);
+  if (threadIdx.x == 0) big[blockIdx.x] = b ? 1 : 0;
 }
 
-hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_t st) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_tanh_factors, dim3((unsigned)ceil_div(n, (int64_t)256)), dim3(256), 0, st, n, x, out);
+hipError_t launch_key_factors(int S, int Tpad, int A, const float* pctx, float* kfac, int32_t* big, hipStream_t st) {
+  if (S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_key_factors, dim3(S), dim3(1024), 0, st, (int64_t)Tpad * A / 4, (const f32x4*)pctx,
+                     (f32x4*)kfac, big);
   return hipGetLastError();
 }
 
@@ -977,7 +1017,8 @@ hipError_t launch_tanh_factors(const float* x, float* out, int64_t n, hipStream_
 // float4 pieces of the context over the unmasked positions.
 template <int NQ>
 __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, const float* __restrict__ q,
-                                                   const float* __restrict__ kfac, const float* __restrict__ ctx,
+                                                   const float* __restrict__ kfac, const float* __restrict__ pctx,
+                                                   const int32_t* __restrict__ kbig, const float* __restrict__ ctx,
                                                    const int32_t* __restrict__ len,
                                                    const int32_t* __restrict__ sent_id, int S,
                                                    const float* __restrict__ v, float* __restrict__ c,
@@ -995,27 +1036,40 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
   }
   const int L = len[s];
   const int A4 = A / 4;
-  f32x4 qv[NQ], vv[NQ];  // query factors 2^{c q} and weights -2 v (see score_term)
+  f32x4 qv[NQ], vv[NQ];  // the query and weights -2 v (see score_term)
+  bool big = false;
 #pragma unroll
   for (int k = 0; k < NQ; ++k) {
     const int a4 = lane + 64 * k;
-    qv[k] = a4 < A4 ? tanh_factor(*(const f32x4*)(q + (int64_t)row * A + 4 * a4)) : zero4();
+    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) : zero4();
     vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
+    big |= factor_big(qv[k]);
   }
-  const float* P = kfac + (int64_t)s * Tpad * A;
-  for (int i = wave; i < L; i += 4) {
-    float acc = 0.f;
+  // Every wave holds the row's whole query, so the test is uniform over the block.
+  const bool exact = __any(big) && kbig[s];
+  auto score = [&](auto exact_tag, const float* P) {
+    constexpr bool EX = decltype(exact_tag)::value;
+    for (int i = wave; i < L; i += 4) {
+      float acc = 0.f;
 #pragma unroll
-    for (int k = 0; k < NQ; ++k) {
-      const int a4 = lane + 64 * k;
-      if (a4 < A4) {
-        const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
+      for (int k = 0; k < NQ; ++k) {
+        const int a4 = lane + 64 * k;
+        if (a4 < A4) {
+          const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
 #pragma unroll
-        for (int x = 0; x < 4; ++x) acc = score_term(p[x], qv[k][x], vv[k][x], acc);
+          for (int x = 0; x < 4; ++x) acc = score_term_t<EX>(p[x], qv[k][x], vv[k][x], acc);
+        }
       }
+      acc = wave_sum(acc);
+      if (lane == 0) e[i] = acc;
     }
-    acc = wave_sum(acc);
-    if (lane == 0) e[i] = acc;
+  };
+  if (exact) {
+    score(std::true_type{}, pctx + (int64_t)s * Tpad * A);
+  } else {
+#pragma unroll
+    for (int k = 0; k < NQ; ++k) qv[k] = tanh_factor(qv[k]);  // padding lanes: factor 1, weight 0
+    score(std::false_type{}, kfac + (int64_t)s * Tpad * A);
   }
   __syncthreads();
   float mx = -INFINITY;
@@ -1194,7 +1248,8 @@ __device__ __forceinline__ float wave_sums(float (&v)[G]) {
 
 template <int G, int NQ, int NW>
 __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int Tpad, const float* __restrict__ q,
-                                               const float* __restrict__ kfac, const float* __restrict__ ctx,
+                                               const float* __restrict__ kfac, const float* __restrict__ pctx,
+                                               const int32_t* __restrict__ kbig, const float* __restrict__ ctx,
                                                const int32_t* __restrict__ len, const int32_t* __restrict__ perm,
                                                const float* __restrict__ v, float* __restrict__ c,
                                                float* __restrict__ alpha, f32x4* qs, float* e, int* rows, int wave,
@@ -1213,9 +1268,12 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
   }
   // query factors 2^{c q} in LDS and weights -2 v in registers (see score_term);
   // rows past the tile's count get factor 0 and are dropped
+  bool big = false;
   for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
     const int g = idx / A4, a4 = idx - g * A4;
-    qs[idx] = g < n ? tanh_factor(*(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4)) : zero4();
+    const f32x4 qv = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+    big |= factor_big(qv);
+    qs[idx] = g < n ? tanh_factor(qv) : zero4();
   }
   f32x4 vv[NQ];
 #pragma unroll
@@ -1223,28 +1281,40 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
     const int a4 = lane + 64 * k;
     vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
   }
-  __syncthreads();
+  const bool exact = __syncthreads_or(big) && kbig[s];
   const int L = len[s];
-  const float* P = kfac + (int64_t)s * Tpad * A;
-  for (int i = wave; i < L; i += NW) {
-    float acc[G];
+  auto score = [&](auto exact_tag, const float* P) {
+    constexpr bool EX = decltype(exact_tag)::value;
+    for (int i = wave; i < L; i += NW) {
+      float acc[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+      for (int g = 0; g < G; ++g) acc[g] = 0.f;
 #pragma unroll
-    for (int k = 0; k < NQ; ++k) {
-      const int a4 = lane + 64 * k;
-      if (a4 < A4) {
-        const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
+      for (int k = 0; k < NQ; ++k) {
+        const int a4 = lane + 64 * k;
+        if (a4 < A4) {
+          const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const f32x4 qq = qs[g * A4 + a4];
+          for (int g = 0; g < G; ++g) {
+            const f32x4 qq = qs[g * A4 + a4];
 #pragma unroll
-          for (int x = 0; x < 4; ++x) acc[g] = score_term(p[x], qq[x], vv[k][x], acc[g]);
+            for (int x = 0; x < 4; ++x) acc[g] = score_term_t<EX>(p[x], qq[x], vv[k][x], acc[g]);
+          }
         }
       }
+      const float r = wave_sums<G>(acc);
+      if ((lane & (64 / G - 1)) == 0) e[(lane / (64 / G)) * Tpad + i] = r;
     }
-    const float r = wave_sums<G>(acc);
-    if ((lane & (64 / G - 1)) == 0) e[(lane / (64 / G)) * Tpad + i] = r;
+  };
+  if (exact) {  // the queries themselves replace their factors (see kFactorSafe)
+    for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
+      const int g = idx / A4, a4 = idx - g * A4;
+      qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+    }
+    __syncthreads();
+    score(std::true_type{}, pctx + (int64_t)s * Tpad * A);
+  } else {
+    score(std::false_type{}, kfac + (int64_t)s * Tpad * A);
   }
   __syncthreads();
   for (int g = wave; g < n; g += NW) {
@@ -1303,8 +1373,9 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
 // all rows, reading each annotation once.
 template <int G, int NQ, int NW>
 __global__ __launch_bounds__(NW * 64) void k_attention_grouped(
-    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ ctx,
-    const int32_t* __restrict__ len, const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
+    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ pctx,
+    const int32_t* __restrict__ kbig, const float* __restrict__ ctx, const int32_t* __restrict__ len,
+    const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
     float* __restrict__ alpha, int c_bf16, int round) {
   extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
@@ -1324,13 +1395,13 @@ __global__ __launch_bounds__(NW * 64) void k_attention_grouped(
     const int r = t / round, p = t - r * round;
     if (r & 1) t = r * round + (min(round, nt - r * round) - 1 - p);
   }
-  attention_tile<G, NQ, NW>(tiles[t], A, C, Tpad, q, kfac, ctx, len, perm, v, c, alpha, qs, e, rows, wave, lane, A4,
-                            C4, c_bf16);
+  attention_tile<G, NQ, NW>(tiles[t], A, C, Tpad, q, kfac, pctx, kbig, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
+                            lane, A4, C4, c_bf16);
 }
 
 template <int G, int NQ>
-static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
-                              const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
+static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+                              const int32_t* kbig, const float* ctx, const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
                               float* alpha, int c_bf16, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
   const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
@@ -1342,19 +1413,19 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
   // faster (70.6 against 75.1 us).
   if (grid <= kAttnWideTiles)
     hipLaunchKernelGGL((k_attention_grouped<G, NQ, 2 * kAttnWaves>), dim3(grid), dim3(2 * kAttnWaves * 64), lds, st, A,
-                       C, Tpad, q, kfac, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
+                       C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
   else
     hipLaunchKernelGGL((k_attention_grouped<G, NQ, kAttnWaves>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C,
-                       Tpad, q, kfac, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
+                       Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
 }
 
 template <int NQ>
-static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
-                         const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
+static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+                         const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
                          float* c, float* alpha, int c_bf16, hipStream_t st) {
   if (S > kGroupMaxS || !grp.perm) {
-    hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, ctx, len, sent_id, S, v,
-                       c, alpha, c_bf16);
+    hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len,
+                       sent_id, S, v, c, alpha, c_bf16);
     return;
   }
   // rows per tile: kAttnGroup when their queries and scores fit 64 KB of LDS, else 4
@@ -1362,24 +1433,24 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                      grp.n_tiles);
   if (G == kAttnGroup)
-    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, c_bf16, st);
+    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, st);
   else
-    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, ctx, len, grp, S, v, c, alpha, c_bf16, st);
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, st);
 }
 
-hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* ctx,
-                            const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
+hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+                            const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
                             const AttnGroups& grp, bool c_bf16, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    attention_nq<1>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<1>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 2)
-    attention_nq<2>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<2>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 4)
-    attention_nq<4>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<4>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else if (nq <= 8)
-    attention_nq<8>(B, A, C, Tpad, q, kfac, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<8>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -190,6 +190,35 @@ def high_signal(cfg: Config, seed: int = 100) -> Config:
     return cfg.replace(sigma_w=0.5, sigma_emb=0.5, seed=seed)
 
 
+def unit_gain(cfg: Config, v_spread: float = 1.5, key_scale: float = 1.0, query_scale: float = 1.0) -> Workload:
+    """The workload of ``cfg`` with every layer passing signal at unit scale,
+    so that a mistake anywhere in the step moves its outputs (at sigma = 0.01
+    attention is nearly uniform and hides attention bugs).
+
+    Weight matrices are N(0, 1/fan-in) (fan-in: rows of the x.W matrix),
+    embeddings N(0, 1), biases N(0, 0.1^2).  For N(0, 1) annotations the keys
+    are then about N(0, key_scale^2) and the queries about query_scale times
+    the first GRU's state scale (|s1| < 1); the attention vector is scaled so
+    that a row's scores vary by about ``v_spread`` over source positions
+    (tanh(k + q) varies by about 0.3 in variance per term).  bf16 workloads
+    are rounded to bf16 again after scaling.
+    """
+    wl = make_workload(cfg.replace(sigma_w=1.0, sigma_emb=1.0))
+    p = wl.params
+    for name, a in p.items():
+        if name in EMBEDDINGS:
+            continue
+        a *= np.float32(1.0 / np.sqrt(a.shape[0]) if a.ndim == 2 else 0.1)
+    p["att_Wc"] *= np.float32(key_scale)
+    p["att_b"] *= np.float32(key_scale)
+    p["att_Wq"] *= np.float32(query_scale)
+    p["att_v"] *= np.float32(10.0 * v_spread / np.sqrt(0.3 * cfg.A))
+    if cfg.wtype == "bf16":
+        for name in p:
+            p[name] = round_to_bf16(p[name])
+    return wl
+
+
 def random_annotations(cfg: Config, seed: int, scale: float = 1.0) -> np.ndarray:
     """Source annotations [S, Tpad, 2H] drawn N(0, scale) for injected-context tests."""
     rng = np.random.default_rng(seed)

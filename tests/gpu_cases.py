@@ -40,10 +40,12 @@ class GpuRun:
         sp = cuda(np.asarray(s_prev, np.float32))
         out = dict(logp=torch.empty(B, device="cuda"), logZ=torch.empty(B, device="cuda"))
         s_new = sp if alias else torch.empty((B, c.H), device="cuda")
-        kw = {} if workspace is None else dict(workspace=workspace)
+        kw = {}
         if debug:
-            kw = dict(alpha=torch.empty((B, c.Tpad), device="cuda"), c=torch.empty((B, c.C), device="cuda"),
+            kw.update(alpha=torch.empty((B, c.Tpad), device="cuda"), c=torch.empty((B, c.C), device="cuda"),
                       s1=torch.empty((B, c.H), device="cuda"), t=torch.empty((B, c.E), device="cuda"))
+        if workspace is not None:
+            kw["workspace"] = workspace
         nb.nmt_score_batch(self.model, self.src, sp, cuda(y_prev), cuda(sent_id), cuda(req), out["logp"], s_new,
                            out["logZ"], **kw)
         torch.cuda.synchronize()

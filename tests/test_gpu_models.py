@@ -184,3 +184,32 @@ def test_ensemble_and_average_argument_errors(env):
         nb.nmt_model_average([r1.model, r1.model], coef=[1.0, float("nan")])
     r1.close()
     r2.close()
+
+
+def test_ensemble_workspace_sized_for_more_rows_serves_fewer(env):
+    """As for one model, a workspace from nmt_ensemble_workspace_bytes(B)
+    serves every smaller ensemble call, although 64 rows need more bytes than
+    65 at the paper's vocabulary (more vocabulary slices)."""
+    torch, nb, gc = env
+    cfg = CONFIGS["enru_b2000"].replace(B=65, S=2, len_lo=3, len_hi=5, Tpad=5, seed=81)
+    w1, w2 = _members(cfg, (81, 82))
+    models = [nb.Model.from_workload(w) for w in (w1, w2)]
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    srcs = [nb.nmt_encode(m, cu(w1.src_ids), w1.src_len) for m in models]
+    assert nb.nmt_ensemble_workspace_bytes(models, 64) <= nb.nmt_ensemble_workspace_bytes(models, 65)
+    ws = torch.empty(nb.nmt_ensemble_workspace_bytes(models, 65), dtype=torch.uint8, device="cuda")
+    n = 64
+    sp = [cu(w1.s_prev[:n]) for _ in models]
+    sn = [torch.empty_like(x) for x in sp]
+    logp = torch.empty((2, n), device="cuda")
+    nb.nmt_score_ensemble(models, srcs, sp, cu(w1.y_prev[:n]), cu(w1.sent_id[:n]), cu(w1.req[:n]), logp, sn,
+                          workspace=ws)
+    torch.cuda.synchronize()
+    for k, m in enumerate(models):
+        alone = torch.empty(n, device="cuda")
+        nb.nmt_score_batch(m, srcs[k], sp[k], cu(w1.y_prev[:n]), cu(w1.sent_id[:n]), cu(w1.req[:n]), alone,
+                           torch.empty_like(sp[k]))
+        torch.cuda.synchronize()
+        assert np.array_equal(logp[k].cpu().numpy(), alone.cpu().numpy())
+    for x in srcs + models:
+        x.close()

@@ -2,15 +2,19 @@
 
 The batched step is the forward step of Section 5.1 of the paper; inputs are
 the seeded synthetic workloads of ``paper_1605_04809_amd.workloads``.  Every
-case compares element by element with the oracle on the same inputs:
-small shapes on every row, full-size shapes on sampled rows (rows are
-independent, so the oracle can score any subset).
+case compares element by element with the oracle on the same inputs, on
+every row of the batch (the paper-sized workloads included); only the
+32,768-row stress case samples rows (rows are independent, so the oracle can
+score any subset).
 
 Tolerances (fp32 path): |d log p| <= 1e-4 is the stated bar.  Intermediates
 (states, context, readout, attention weights) are bounded by fp32 rounding of
 dot products of length K <= 3572 with fp32 accumulation: roughly
 K * 2^-24 * sum|terms|, which is below 1e-5 for the sigma = 0.01 workloads and
 below 1e-4 for the high-signal variants (sigma = 0.5, unit-scale context).
+bf16 weights: |d log p| <= 2e-2 (stated bar); intermediates of the
+paper-sized workloads within bars derived from the path's bf16 rounding of
+its MFMA operands (tests/bf16_bars.py).
 """
 import math
 
@@ -18,7 +22,8 @@ import numpy as np
 import pytest
 
 from paper_1605_04809_amd.workloads import CONFIGS, Config, make_workload, high_signal, random_annotations
-from paper_1605_04809_amd.workloads import phrase_schedule
+from paper_1605_04809_amd.workloads import phrase_schedule, unit_gain
+from tests.parity_cases import ATT, ATT_CASES, CLAMP_SCALES, PAPER_SIGNAL, attention_grid
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +63,19 @@ def compare(g, o, rows=None, tol_logp=TOL_LOGP, tol=TOL_INTER, keys=("s_new", "s
 
 
 # ------------------------------------------------------------------ tiny
+
+
+def compare_bf16(g, o, wl, ctx, rows=None):
+    """bf16 weights: log p and log Z within the stated 2e-2, every
+    intermediate within the bar derived from the path's bf16 rounding of
+    MFMA operands (tests/bf16_bars.py), computed from the oracle's values."""
+    from tests.bf16_bars import bf16_bars
+    bars = bf16_bars(wl.cfg, wl, o, ctx, rows)
+    print("bf16 bars:", {k: f"{v:.2e}" for k, v in bars.items()}, flush=True)
+    errs = compare(g, o, rows=rows, tol_logp=TOL_LOGP_BF16, tol=float("inf"))
+    for k, bar in bars.items():
+        assert errs[k] <= bar, (k, errs[k], bar)
+    return errs
 
 
 def test_tiny_every_row_and_encoder(gpu):
@@ -129,6 +147,66 @@ def test_large_keys_and_queries_every_row(gpu, S):
     assert np.abs(o.pctx).max() > 30
     args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
     compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+
+
+@pytest.mark.parametrize("case", list(ATT_CASES))
+def test_attention_at_paper_width_every_row(gpu, case):
+    """The attention width of every paper-sized workload (A = 1024, so each
+    lane covers four float4 pieces of the query) with inputs where attention
+    matters: unit-gain weights and N(0, 1) annotations, so each row's scores
+    spread over its positions (zeroing att_v moves alpha by about 0.4, see
+    test_parity_inputs).  Three launch shapes: blocks of 16 waves (at most
+    640 tiles), of 8 waves (more tiles, as bf16_b4096 runs) and one row per
+    block (more than 8192 sentences).  Every row, every output."""
+    _torch()
+    cfg = ATT.replace(**ATT_CASES[case])
+    grid, waves = attention_grid(cfg.B, cfg.S, cfg.A)
+    print(f"{case}: B={cfg.B} S={cfg.S} Tpad={cfg.Tpad}: grid {grid}, {waves}", flush=True)
+    wl = unit_gain(cfg)
+    ctx = random_annotations(cfg, seed=72)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    errs = compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    assert errs["alpha"] <= TOL_INTER, errs
+    g.close()
+
+
+@pytest.mark.parametrize("wtype", ["f32", "bf16"])
+def test_attention_signal_at_paper_dimensions_every_row(gpu, wtype):
+    """Section 3's sizes (E = 500, H = A = 1024, V = 100,000) with unit-gain
+    weights and N(0, 1) annotations: the step of the paper-sized workloads
+    where attention, the GRUs and the readout all carry signal."""
+    _torch()
+    cfg = PAPER_SIGNAL.replace(wtype=wtype)
+    wl = unit_gain(cfg)
+    ctx = random_annotations(cfg, seed=74)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    if wtype == "f32":
+        compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    else:
+        compare(g.step(*args), o.step(*args), tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16_SIGNAL)
+    g.close()
+
+
+@pytest.mark.parametrize("case", ["grouped_16_waves", "per_row"])
+def test_keys_beyond_the_factor_range_every_row(gpu, case):
+    """Keys up to about |pctx| = 66 against queries of either sign up to about
+    75, so many terms tanh(k + q) pair a key whose factor 2^{2 log2(e) k}
+    leaves fp32's range with a query of the opposite sign: scored from
+    clamped factors such terms would be wrong (alpha off by 0.03, see
+    test_parity_inputs); the kernels score those tiles from the keys
+    themselves.  Grouped and per-row attention, every row."""
+    _torch()
+    cfg = ATT.replace(**ATT_CASES[case])
+    wl = unit_gain(cfg, **CLAMP_SCALES)
+    ctx = random_annotations(cfg, seed=72)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    assert np.abs(o.pctx).max() > 50
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    errs = compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    assert errs["alpha"] <= TOL_INTER, errs
     g.close()
 
 
@@ -281,55 +359,82 @@ def sample_rows(B, n, seed):
 
 
 @pytest.mark.parametrize("name", ["ruen_b1000", "enru_b2000"])
-def test_paper_sized_step_sampled_rows(gpu, name):
-    """Full batch on the GPU (the benchmarked launch shape); oracle on sampled rows."""
+def test_paper_sized_step_every_row(gpu, name):
+    """The whole batch in the benchmarked launch shape, every row and every
+    output against the oracle."""
     _torch()
     wl = make_workload(CONFIGS[name])
     g = gpu.GpuRun(wl)
     args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
     out = g.step(*args)
     assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
-    rows = sample_rows(wl.cfg.B, 40, seed=5)
-    o = gpu.OracleRun(wl)
-    ref = o.step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
-    compare(out, ref, rows=rows)
+    compare(out, gpu.OracleRun(wl).step(*args))
     g.close()
 
 
 @pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "bf16")])
-def test_launch_shape_boundaries_sampled_rows(gpu, B, wtype):
+def test_launch_shape_boundaries_every_row(gpu, B, wtype):
     """Batches between the tile choices at the paper's dimensions: B = 2600
     takes the 64-row GRU tile with more than a round of 128-row blocks
     (fp32), B = 1445 takes 32 vocabulary slices over 23 row tiles, B = 667
-    (bf16) 64-row GRU blocks and 40 slices; oracle on sampled rows."""
+    (bf16) 64-row GRU blocks and 40 slices; every row."""
     _torch()
     wl = make_workload(CONFIGS["enru_b2000"].replace(B=B, wtype=wtype, seed=43))
     g = gpu.GpuRun(wl)
-    out = g.step(wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    out = g.step(*args)
     assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
-    rows = sample_rows(B, 24, seed=44)
-    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
+    o = gpu.OracleRun(wl)
+    ref = o.step(*args)
     if wtype == "bf16":
-        compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16)
+        compare_bf16(out, ref, wl, o.ctx)
     else:
-        compare(out, ref, rows=rows)
+        compare(out, ref)
     g.close()
 
 
-@pytest.mark.parametrize("wtype", ["f32", "bf16"])
-def test_workspace_bytes_never_shrink_with_the_batch(gpu, wtype):
+def _bytes_needed(nb, g, B):
+    """The exact workspace a step of B rows needs, read from the library's
+    refusal of a 256-byte workspace (nothing is enqueued)."""
+    import re
+    import torch
+    c = g.wl.cfg
+    z = torch.zeros(B, dtype=torch.int32, device="cuda")
+    st = torch.zeros((B, c.H), device="cuda")
+    with pytest.raises(nb.NmtError) as ei:
+        nb.nmt_score_batch(g.model, g.src, st, z, z, z, torch.empty(B, device="cuda"), st,
+                           workspace=torch.empty(256, dtype=torch.uint8, device="cuda"))
+    assert ei.value.status == nb.NMT_EWORKSPACE
+    return int(re.search(r"(\d+) needed", str(ei.value)).group(1))
+
+
+@pytest.mark.parametrize("wtype,big,small", [("f32", 65, 64), ("bf16", 129, 128)])
+def test_workspace_bytes_never_shrink_with_the_batch(gpu, wtype, big, small):
     """A workspace sized for B rows serves every smaller batch (a forest's
-    levels, a shrinking phrase batch), although some smaller batches take
-    more vocabulary slices than B; and such a call runs."""
+    levels, a shrinking phrase batch), although some smaller batches need
+    more bytes than B itself: a batch that fills whole row tiles of the
+    vocabulary kernel (64 rows fp32, 128 bf16) takes more slices than one
+    row more; such a call runs."""
     torch = _torch()
     from paper_1605_04809_amd import binding as nb
-    wl = make_workload(CONFIGS["enru_b2000"].replace(B=65, S=2, len_lo=3, len_hi=5, Tpad=5, wtype=wtype, seed=45))
+    wl = make_workload(CONFIGS["enru_b2000"].replace(B=big, S=2, len_lo=3, len_hi=5, Tpad=5, wtype=wtype, seed=45))
     g = gpu.GpuRun(wl)
     sizes = [nb.nmt_score_workspace_bytes(g.model, b) for b in range(1, 700)]
     assert all(a <= b for a, b in zip(sizes, sizes[1:])), "workspace bytes shrink somewhere below 700 rows"
-    ws = torch.empty(nb.nmt_score_workspace_bytes(g.model, 65), dtype=torch.uint8, device="cuda")
-    out = g.step(wl.s_prev[:64], wl.y_prev[:64], wl.sent_id[:64], wl.req[:64], workspace=ws)
+    need_big, need_small = _bytes_needed(nb, g, big), _bytes_needed(nb, g, small)
+    print(f"{wtype}: a step of {big} rows needs {need_big} bytes, of {small} rows {need_small}", flush=True)
+    assert need_small > need_big, "pick a pair where the smaller batch needs more"
+    ws = torch.empty(nb.nmt_score_workspace_bytes(g.model, big), dtype=torch.uint8, device="cuda")
+    assert ws.numel() >= need_small
+    n = small
+    out = g.step(wl.s_prev[:n], wl.y_prev[:n], wl.sent_id[:n], wl.req[:n], workspace=ws)
     assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
+    o = gpu.OracleRun(wl)
+    ref = o.step(wl.s_prev[:n], wl.y_prev[:n], wl.sent_id[:n], wl.req[:n])
+    if wtype == "f32":
+        compare(out, ref)
+    else:
+        compare_bf16(out, ref, wl, o.ctx, rows=np.arange(n))
     g.close()
 
 
@@ -346,10 +451,12 @@ def test_large_batch_sampled_rows(gpu, wtype):
     out = g.step(*args, debug=False)
     assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
     rows = sample_rows(wl.cfg.B, 24, seed=42)
-    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows],
-                                 intermediates=False)
+    o = gpu.OracleRun(wl)
+    ref = o.step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
     if wtype == "bf16":
-        compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16, keys=("s_new",))
+        from tests.bf16_bars import bf16_bars
+        bar = bf16_bars(wl.cfg, wl, ref, o.ctx, rows)["s_new"]
+        compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=bar, keys=("s_new",))
     else:
         compare(out, ref, rows=rows, keys=("s_new",))
     g.close()
@@ -397,8 +504,8 @@ def test_phrase_scoring_stepwise(gpu):
         y = torch.cat([req, y[n:]])
     gpu_total = np.empty(c.B)
     gpu_total[order] = total.cpu().numpy()
-    # oracle, stepwise with fp64 states, on sampled hypotheses
-    rows = sample_rows(c.B, 24, seed=9)
+    # oracle, stepwise with fp64 states, on every hypothesis
+    rows = np.arange(c.B)
     o = gpu.OracleRun(wl)
     st = wl.s_prev[rows].astype(np.float64)
     yy = wl.y_prev[rows].copy()
@@ -427,6 +534,7 @@ def cuda_i32(a):
 
 TOL_LOGP_BF16 = 2e-2      # stated bar: bf16 weights, fp32 accumulation
 TOL_INTER_BF16 = 1e-2     # states and intermediates (bf16 rounding of MFMA inputs)
+TOL_INTER_BF16_SIGNAL = 2e-2  # unit-scale activations: bf16 rounding of operands of size ~1
 
 
 @pytest.mark.parametrize("cfg", [CONFIGS["tiny"].replace(wtype="bf16", B=96),
@@ -443,14 +551,13 @@ def test_bf16_every_row(gpu, cfg):
     g.close()
 
 
-def test_bf16_paper_sized_step_sampled_rows(gpu):
+def test_bf16_paper_sized_step_every_row(gpu):
     _torch()
     wl = make_workload(CONFIGS["bf16_b4096"])
     g = gpu.GpuRun(wl)
     args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
     out = g.step(*args)
     assert np.all(np.isfinite(out["logp"])) and np.all(out["logp"] <= 0)
-    rows = sample_rows(wl.cfg.B, 40, seed=6)
-    ref = gpu.OracleRun(wl).step(wl.s_prev[rows], wl.y_prev[rows], wl.sent_id[rows], wl.req[rows])
-    compare(out, ref, rows=rows, tol_logp=TOL_LOGP_BF16, tol=TOL_INTER_BF16)
+    o = gpu.OracleRun(wl)
+    compare_bf16(out, o.step(*args), wl, o.ctx)
     g.close()

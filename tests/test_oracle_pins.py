@@ -179,6 +179,67 @@ def test_initial_state_closed_form():
                                rtol=0, atol=1e-15)
 
 
+def test_keys_from_annotations_closed_forms_and_encoder_agreement():
+    """Keys from given annotations: zero key weights give the bias; a single
+    non-zero annotation entry gives that entry times its weight row plus the
+    bias (one rounding); padding contents are ignored; and fed the encoder's
+    own annotations (rounded to fp32, the entry point's input type) it gives
+    the encoder's keys up to that rounding."""
+    p, m = make_model(31)
+    H, A, C = DIMS["H"], DIMS["A"], 2 * DIMS["H"]
+    S, T = 3, 6
+    src_len = np.array([6, 2, 1], np.int32)
+    rng = np.random.default_rng(32)
+    ann = rng.standard_normal((S, T, C)).astype(np.float32)
+    # zero key weights: pctx = att_b below the length, 0 past it; ctx is the input widened, 0 past the length
+    p0 = dict(p)
+    p0["att_Wc"] = np.zeros_like(p["att_Wc"])
+    ctx, pctx = oracle.keys_from_annotations(oracle.Model(p0, **DIMS), ann, src_len)
+    for s in range(S):
+        L = src_len[s]
+        np.testing.assert_array_equal(pctx[s, :L], np.broadcast_to(p["att_b"].astype(np.float64), (L, A)))
+        np.testing.assert_array_equal(ctx[s, :L], ann[s, :L].astype(np.float64))
+        assert np.all(pctx[s, L:] == 0) and np.all(ctx[s, L:] == 0)
+    # one non-zero entry x at (s, i, k): pctx[s, i] = b + x * Wc[k] exactly, other positions b
+    one = np.zeros_like(ann)
+    one[0, 3, 4] = np.float32(1.75)
+    _, pctx = oracle.keys_from_annotations(m, one, src_len)
+    want = p["att_b"].astype(np.float64) + 1.75 * p["att_Wc"][4].astype(np.float64)
+    np.testing.assert_array_equal(pctx[0, 3], want)
+    np.testing.assert_array_equal(pctx[0, 2], p["att_b"].astype(np.float64))
+    # padding contents are ignored
+    junk = ann.copy()
+    for s in range(S):
+        junk[s, src_len[s]:] = 1e6
+    np.testing.assert_array_equal(oracle.keys_from_annotations(m, junk, src_len)[1],
+                                  oracle.keys_from_annotations(m, ann, src_len)[1])
+    # the encoder's annotations give the encoder's keys, within the fp32 rounding of the annotations
+    ids = rng.integers(0, DIMS["V_src"], (S, T)).astype(np.int32)
+    ectx, epctx, _ = oracle.encode(m, ids, src_len)
+    c32 = ectx.astype(np.float32)
+    _, kpctx = oracle.keys_from_annotations(m, c32, src_len)
+    bound = (np.abs(ectx - c32.astype(np.float64)) @ np.abs(p["att_Wc"].astype(np.float64))) + 1e-15
+    assert np.all(np.abs(kpctx - epctx) <= bound)
+    assert np.abs(kpctx - epctx).max() > 0  # the rounding is visible, so the bound is doing the work
+
+
+def test_fp64_states_equal_the_fp32_path_on_fp32_values():
+    """The step with fp64 input states (used for stepwise phrase scoring)
+    equals the step with fp32 states when the states are fp32 values: the
+    two entry points differ only in how the state is widened."""
+    p, m = make_model(33)
+    src_ids, src_len, s_prev, y_prev, sent_id, req = step_inputs(34)
+    ctx, pctx, _ = oracle.encode(m, src_ids, src_len)
+    a = oracle.score_batch(m, ctx, pctx, src_len, s_prev, y_prev, sent_id, req)
+    b = oracle.score_batch(m, ctx, pctx, src_len, s_prev.astype(np.float64), y_prev, sent_id, req)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+    # and an fp64 state that is not an fp32 value is used as such (not rounded to fp32)
+    s64 = s_prev.astype(np.float64) + 1e-12
+    c = oracle.score_batch(m, ctx, pctx, src_len, s64, y_prev, sent_id, req)
+    assert np.abs(c["s_new"] - a["s_new"]).max() > 0
+
+
 # ------------------------------------------------------------ whole step
 
 
