@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "scored hypothesis-words/sec at V=100k, H=1024, B=2000; MFMA util %"
 UNIT = "scored hypothesis-words/s"
-PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # MI355X dense MFMA
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
 KERNEL_HEADERS = ("paper_1605_04809_amd/csrc/device.hpp", "paper_1605_04809_amd/csrc/internal.hpp")
 KERNEL_FILE = "paper_1605_04809_amd/csrc/kernels.hip"
@@ -399,12 +399,173 @@ def rescore_bench(args):
     print(json.dumps(out), flush=True)
 
 
+EXTRA_WORKLOADS = ("tiny", "ruen_b1000", "phrase_h500", "bf16_b4096")
+
+
+def _events_pass(torch, stream, fn, k):
+    """k calls of fn with an event before each and after the last, on the
+    launch stream: per-call times (ms) and the whole pass (ms)."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(k):
+        fn()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(k)]
+    return per, ev[0].elapsed_time(ev[k])
+
+
+def _plain_pass(torch, stream, fn, k):
+    """k calls of fn bracketed by synchronisation and two events (ms total)."""
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(k):
+        fn()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1)
+
+
+def phrase_forest(wl):
+    """The phrase workload as ScoreBatch input (Section 5.1, Figure 2): each
+    hypothesis (its last word, sentence and state) with its one target phrase;
+    the forest's level d holds the hypotheses whose phrase has at least d
+    tokens, so the batch shrinks as phrases end."""
+    phrases = [list(map(int, wl.phrase_tok[b, :wl.phrase_len[b]])) for b in range(len(wl.y_prev))]
+    return wl.y_prev, wl.sent_id, np.arange(len(phrases), dtype=np.int32), phrases
+
+
+def bench_workload(name, args, cpu_seconds, headline=False):
+    """Time one workload: W warm-up steps, a pass of K steps with an event
+    around each of the library's kernels (the roofline's kernel duration), a
+    plain pass of K steps between two events (throughput), and a pass with an
+    event between steps (median step time).  A step of the phrase workload is
+    its whole ScoreBatch: one batched step per tree depth, the batch shrinking
+    as phrases end, and the per-phrase sums (nmt_score_forest)."""
+    import torch
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS, make_workload
+
+    cfg = CONFIGS[name]
+    wl = make_workload(cfg)
+    model = nb.Model.from_workload(wl)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    src_ids = cu(wl.src_ids)
+    src = nb.nmt_encode(model, src_ids, wl.src_len)
+    stream = torch.cuda.current_stream()
+
+    # Source initialisation (off the scoring loop), timed on its own: host
+    # wall clock around encode + synchronise, the source's allocation included.
+    torch.cuda.synchronize()
+    enc_ms = []
+    for _ in range(3):
+        t_enc = time.perf_counter()
+        extra = nb.nmt_encode(model, src_ids, wl.src_len, stream=stream)
+        torch.cuda.synchronize()
+        enc_ms.append((time.perf_counter() - t_enc) * 1e3)
+        extra.close()
+
+    if cfg.phrase_max:
+        hyp_word, hyp_sent, pair_hyp, phrases = phrase_forest(wl)
+        forest = nb.Forest(hyp_word, hyp_sent, pair_hyp, phrases)
+        sh = forest.shape()
+        levels = [forest.level(d) for d in range(1, sh["depth"] + 1)]
+        rows_per_level = [int(lv["y_prev"].size) for lv in levels]
+        hs = cu(wl.s_prev)
+        out_logp = torch.empty(len(phrases), device="cuda")
+        ws = torch.empty(nb.nmt_forest_workspace_bytes(model, forest), dtype=torch.uint8, device="cuda")
+        calls_per_step = sh["depth"]
+        scored = sh["n_req"]                      # requested tokens over all levels
+        row_sent = np.concatenate([lv["sent_id"] for lv in levels])
+
+        def step():
+            nb.nmt_score_forest(model, src, forest, hs, out_logp, workspace=ws, stream=stream)
+        check = out_logp
+    else:
+        B = cfg.B
+        s_prev, y_prev, sent_id, req = cu(wl.s_prev), cu(wl.y_prev), cu(wl.sent_id), cu(wl.req)
+        logp = torch.empty(B, device="cuda")
+        logZ = torch.empty(B, device="cuda")
+        s_new = torch.empty((B, cfg.H), device="cuda")
+        ws = torch.empty(nb.nmt_score_workspace_bytes(model, B), dtype=torch.uint8, device="cuda")
+        calls_per_step = 1
+        scored = B
+        row_sent = wl.sent_id
+        rows_per_level = [B]
+
+        def step():
+            nb.nmt_score_batch(model, src, s_prev, y_prev, sent_id, req, logp, s_new, logZ, workspace=ws,
+                               stream=stream)
+        check = logp
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if nb.nmt_stream_status(model) != nb.NMT_OK:
+        raise SystemExit(f"{name}: device reported an id error during warm-up")
+
+    K = args.steps
+    nb.nmt_profile_begin(model, K * calls_per_step)
+    ms_total_prof = _plain_pass(torch, stream, step, K)
+    phases = nb.nmt_profile_end(model, stream)
+    assert phases["steps"] == K * calls_per_step
+    ms_total = _plain_pass(torch, stream, step, K)
+    per_step, _ = _events_pass(torch, stream, step, K)
+    if not bool(torch.isfinite(check).all()):
+        raise SystemExit(f"{name}: non-finite log-probabilities")
+
+    ms_step = ms_total / K
+    total_flops, vocab_flops = step_flops(cfg, wl.src_len, row_sent)
+    peak = PEAK_TFLOPS[cfg.wtype]
+    vocab_ms = phases["vocab"] / K
+    achieved = vocab_flops / (vocab_ms * 1e-3) / 1e12
+    res = {
+        "value": scored / (ms_step * 1e-3),
+        "unit": UNIT,
+        "ms_per_step": ms_step,
+        "ms_per_step_median": float(np.median(per_step)),
+        "ms_per_step_p10_p90": [float(np.percentile(per_step, 10)), float(np.percentile(per_step, 90))],
+        "dtype": cfg.wtype,
+        "config": {"workload": cfg.name, "V": cfg.V, "E": cfg.E, "H": cfg.H, "A": cfg.A,
+                   "S": cfg.S, "src_len": f"U{{{cfg.len_lo}..{cfg.len_hi}}}", "Tpad": cfg.Tpad,
+                   "weights": cfg.wtype, "rows_per_step": rows_per_level},
+        "roofline": {"bound": "mfma", "kernel": "k_vocab_lse", "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": read_traffic(cfg.name), "algorithmic_flops_per_step": vocab_flops,
+                     "launches_per_step": calls_per_step, "avg_launch_ms": vocab_ms / calls_per_step},
+        "step_tflops": total_flops / (ms_step * 1e-3) / 1e12,
+        "mfma_util_step_pct": 100.0 * total_flops / (ms_step * 1e-3) / 1e12 / peak,
+        "phase_ms": {k: v / K for k, v in phases.items() if k != "steps"},
+        "ms_per_step_with_phase_events": ms_total_prof / K,
+        "encode": {"ms": float(np.median(enc_ms)), "sentences": cfg.S,
+                   "ms_per_sentence": float(np.median(enc_ms)) / cfg.S},
+    }
+    if cfg.phrase_max:
+        res["config"].update(hypotheses=cfg.B, phrase_tokens="U{1..%d}" % cfg.phrase_max, scored_tokens=scored)
+        res["timing"] = ("one step = nmt_score_forest over the 500 phrases: one batched step per depth, the "
+                         "batch shrinking as phrases end, states kept on the device, per-phrase sums; the "
+                         "forest's index arrays (%d bytes, built on the host) are uploaded inside each call"
+                         % (4 * (4 * sh["n_rows"] + sh["depth"] + sh["n_req"] + sh["depth"] * len(phrases))))
+    else:
+        res["config"]["B"] = cfg.B
+    if cpu_seconds > 0:
+        res["cpu_baseline"] = cpu_baseline(wl, min_seconds=cpu_seconds, max_seconds=max(30.0, 3 * cpu_seconds))
+    if cfg.phrase_max:
+        forest.close()
+    src.close()
+    model.close()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="enru_b2000")
+    ap.add_argument("--only", action="store_true", help="time only --config (no other workloads in the line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--print-kernel-hash", action="store_true")
@@ -445,112 +606,45 @@ def main():
         library_gemms(args)
         return
 
-    from paper_1605_04809_amd import binding as nb
-    from paper_1605_04809_amd.workloads import CONFIGS, make_workload
-
-    cfg = CONFIGS[args.config]
-    if cfg.phrase_max:
-        raise SystemExit("the phrase workload is a parity case, not a bench line")
-    wl = make_workload(cfg)
-    B = cfg.B
-    model = nb.Model.from_workload(wl)
-    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-    src_ids = cu(wl.src_ids)
-    src = nb.nmt_encode(model, src_ids, wl.src_len)
-    s_prev, y_prev, sent_id, req = cu(wl.s_prev), cu(wl.y_prev), cu(wl.sent_id), cu(wl.req)
-    logp = torch.empty(B, device="cuda")
-    logZ = torch.empty(B, device="cuda")
-    s_new = torch.empty((B, cfg.H), device="cuda")
-    ws = torch.empty(nb.nmt_score_workspace_bytes(model, B), dtype=torch.uint8, device="cuda")
-    stream = torch.cuda.current_stream()
-
-    # Source initialisation (off the scoring loop), timed on its own: host
-    # wall clock around encode + synchronise, the source's allocation included.
-    torch.cuda.synchronize()
-    enc_ms = []
-    for _ in range(3):
-        t_enc = time.perf_counter()
-        extra = nb.nmt_encode(model, src_ids, wl.src_len, stream=stream)
-        torch.cuda.synchronize()
-        enc_ms.append((time.perf_counter() - t_enc) * 1e3)
-        extra.close()
-    encode_ms = float(np.median(enc_ms))
-
-    def step():
-        nb.nmt_score_batch(model, src, s_prev, y_prev, sent_id, req, logp, s_new, logZ, workspace=ws,
-                           stream=stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if nb.nmt_stream_status(model) != nb.NMT_OK:
-        raise SystemExit("device reported an id error during warm-up")
-
-    def timed(profile: bool):
-        """K steps between events on the launch stream; with `profile`, the
-        library also records events around each of its kernels."""
-        if profile:
-            nb.nmt_profile_begin(model, args.steps)
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0.record(stream)
-        for _ in range(args.steps):
-            step()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        ph = nb.nmt_profile_end(model, stream) if profile else None
-        return t0.elapsed_time(t1), ph
-
-    # A pass of K steps with an event around each kernel gives the per-kernel
-    # durations; the throughput then comes from K plain steps (those events
-    # cost about 1 % of an fp32 step and 3 % of a bf16 one).  The plain pass
-    # goes second: right after a few warm-up steps the clock is still settling.
-    ms_total_prof, phases = timed(True)
-    ms_total, _ = timed(False)
-    assert phases["steps"] == args.steps
-    if not bool(torch.isfinite(logp).all()):
-        raise SystemExit("non-finite log-probabilities")
-
-    ms_step = ms_total / args.steps
-    total_flops, vocab_flops = step_flops(cfg, wl.src_len, wl.sent_id)
-    peak = PEAK_TFLOPS[cfg.wtype]
-    vocab_ms = phases["vocab"] / args.steps
-    achieved = vocab_flops / (vocab_ms * 1e-3) / 1e12
-    traffic = read_traffic(cfg.name)
+    cpu = 0.0 if args.no_cpu_baseline else 10.0
+    head = bench_workload(args.config, args, cpu, headline=True)
     out = {
         "metric": METRIC,
-        "value": B / (ms_step * 1e-3),
+        "value": head["value"],
         "unit": UNIT,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": cfg.wtype,
+        "dtype": head["dtype"],
         "data": "synthetic: seeded N(0, 0.01) random-init weights of the paper's shape, no trained model",
-        "config": {"workload": cfg.name, "V": cfg.V, "E": cfg.E, "H": cfg.H, "A": cfg.A, "B": B,
-                   "S": cfg.S, "src_len": f"U{{{cfg.len_lo}..{cfg.len_hi}}}", "Tpad": cfg.Tpad,
-                   "weights": cfg.wtype},
-        "roofline": {"bound": "mfma", "kernel": "k_vocab_lse", "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic, "algorithmic_flops_per_launch": vocab_flops,
-                     "avg_launch_ms": vocab_ms},
-        "mfma_util_vocab_pct": 100.0 * achieved / peak,
-        "step_tflops": total_flops / (ms_step * 1e-3) / 1e12,
-        "mfma_util_step_pct": 100.0 * total_flops / (ms_step * 1e-3) / 1e12 / peak,
-        "phase_ms": {k: v / args.steps for k, v in phases.items() if k != "steps"},
-        "ms_per_step_with_phase_events": ms_total_prof / args.steps,
-        "encode": {"ms": encode_ms, "sentences": cfg.S, "ms_per_sentence": encode_ms / cfg.S,
-                   "note": "nmt_encode of the step's S sentences (Tpad steps of the bidirectional GRU, keys, "
-                           "initial states), outside the timed step; median of 3, host clock"},
+        "config": head["config"],
+        "roofline": head["roofline"],
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl)
-    src.close()
-    model.close()
+    out["roofline"]["algorithmic_flops_per_launch"] = out["roofline"].pop("algorithmic_flops_per_step") / \
+        out["roofline"]["launches_per_step"]
+    if "cpu_baseline" in head:
+        out["cpu_baseline"] = head["cpu_baseline"]
+    for k in ("ms_per_step_median", "ms_per_step_p10_p90", "step_tflops", "mfma_util_step_pct", "phase_ms",
+              "ms_per_step_with_phase_events", "encode"):
+        out[k] = head[k]
+    out["mfma_util_vocab_pct"] = 100.0 * out["roofline"]["frac"]
+    if not args.only:
+        # The other workloads, each timed the same way in this process (their
+        # CPU baselines on shorter samples, so the run stays within minutes).
+        out["workloads"] = {}
+        for name in EXTRA_WORKLOADS:
+            if name == args.config:
+                continue
+            r = bench_workload(name, args, 0.0 if args.no_cpu_baseline else 4.0)
+            r["roofline"]["algorithmic_flops_per_launch"] = r["roofline"].pop("algorithmic_flops_per_step") / \
+                r["roofline"]["launches_per_step"]
+            out["workloads"][name] = r
+            print(f"# {name}: {r['ms_per_step']:.4f} ms per step, {r['value']:.4g} {UNIT}", file=sys.stderr,
+                  flush=True)
     print(json.dumps(out), flush=True)
 
 
