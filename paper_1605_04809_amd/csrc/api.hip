@@ -75,6 +75,7 @@ struct GruBias {
 struct nmt_model {
   nmt_dims dims{};
   int device = 0;
+  int cus = 0;        // the device's compute units (launch shapes that fill the chip)
   bool bf16 = false;  // weights and embeddings stored as bf16
   int kc = 32;        // K chunk of the GEMM tiles
   int64_t emb_ld = 0; // row stride of the embedding tables (elements)
@@ -271,31 +272,29 @@ nmt_status hip_fail(hipError_t e, const char* what) {
   return fail(NMT_EDEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
-// K split of a small-tile plain GEMM: enough blocks for about four per CU,
-// at least four K chunks per block.
-// Blocks a split-K launch aims for (measured on the readout: fp32 1024, so
-// 4 splits at B = 2000; bf16 512, which leaves B = 4096 unsplit, 6.5 us
-// faster than 2 splits and their reduction).
-#ifndef NMT_SPLITK_BLOCKS
-#define NMT_SPLITK_BLOCKS 1024
-#endif
-#ifndef NMT_SPLITK_BLOCKS_BF16
-#define NMT_SPLITK_BLOCKS_BF16 512
-#endif
-int plain_ksplit(int M, int N, int K_total, int kc, Tile t, bool bf16) {
+// K split of a small-tile plain GEMM: at least four K chunks per block, and
+// enough blocks for about four per CU with fp32 weights, two with bf16
+// (measured on the readout at 256 CUs: fp32 1024 blocks, so 4 splits at
+// B = 2000; bf16 512, which leaves B = 4096 unsplit, 6.5 us faster than 2
+// splits and their reduction).
+int plain_ksplit(int M, int N, int K_total, int kc, Tile t, bool bf16, int cus) {
   const int tiles = ceil_div(M, tile_m(t)) * ceil_div(N, tile_n(t));
   const int nc = ceil_div(K_total, kc);
-  int ks = ceil_div(bf16 ? NMT_SPLITK_BLOCKS_BF16 : NMT_SPLITK_BLOCKS, tiles);
+  int ks = ceil_div((bf16 ? 2 : 4) * cus, tiles);
   if (ks > nc / 4) ks = nc / 4;
   if (ks > 8) ks = 8;
   return ks < 1 ? 1 : ks;
 }
 
-// Workspace layout of one step (offsets in bytes, 256-aligned).
+// Workspace layout of one step (offsets in bytes, 256-aligned).  s1 (and
+// its bf16 copy) and the context live across the two GRUs; everything from
+// q on is dead while a GRU runs, so a GRU's split-K partial sums (gpart)
+// reuse that region, extended if they need more.
 struct WsLayout {
-  size_t s1, q, c, t, part, kpart, perm, tiles, ntiles, s1h, total;
-  int nS;           // vocabulary slices
-  int ks_q, ks_ro;  // K splits of the query and readout GEMMs
+  size_t s1, s1h, c, q, t, part, kpart, perm, tiles, ntiles, gpart, total;
+  int nS;             // vocabulary slices
+  int ks_q, ks_ro;    // K splits of the query and readout GEMMs
+  int ks_g1, ks_g2;   // K splits of the two GRUs (1: fused cell, no partials)
 };
 
 WsLayout ws_layout(const nmt_model* m, int64_t B) {
@@ -305,18 +304,21 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   size_t off = 0;
   L.s1 = off;
   off += al((size_t)B * d.H * 4);
-  L.q = off;
-  off += al((size_t)B * d.A * 4);
+  // bf16 weights: a bf16 copy of s1 for the GEMMs that read it
+  L.s1h = off;
+  off += m->bf16 ? al((size_t)B * d.H * 2) : 0;
   L.c = off;
   off += al((size_t)B * 2 * d.H * 4);
+  L.q = off;
+  off += al((size_t)B * d.A * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.nS = vocab_slices((int)B, m->dims.V, m->bf16);
+  L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
   L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay (B = 1000: 28 -> 32 us)
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16, m->cus);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
@@ -329,9 +331,17 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * 16);
   L.ntiles = off;
   off += al(4);
-  // bf16 weights: a bf16 copy of s1 for the GEMMs that read it
-  L.s1h = off;
-  off += m->bf16 ? al((size_t)B * d.H * 2) : 0;
+  // the GRUs' K splits: GRU1 reads [x | s_prev], GRU2 [s1 | c]
+  const int kc = m->kc;
+  const int kx = m->bf16 ? (int)m->emb_ld : d.E;
+  L.ks_g1 = gru_ksplit((int)B, d.H, ceil_div(kx, kc) + ceil_div(d.H, kc), m->bf16, m->cus);
+  L.ks_g2 = gru_ksplit((int)B, d.H, ceil_div(d.H, kc) + ceil_div(2 * d.H, kc), m->bf16, m->cus);
+  const int ks_g = L.ks_g1 > L.ks_g2 ? L.ks_g1 : L.ks_g2;
+  L.gpart = L.q;
+  if (ks_g > 1) {
+    const size_t end = L.gpart + al((size_t)ks_g * B * 4 * d.H * 4);
+    off = end > off ? end : off;
+  }
   L.total = off;
   return L;
 }
@@ -342,7 +352,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
 int encoder_ksplit(const nmt_model* m, int S) {
   const int base = ceil_div(S, kGruSmallTM) * ceil_div(m->dims.H, gru_hb(m->bf16)) * 2;
   const int nc = ceil_div(m->dims.H, m->kc);
-  int ks = kNumCUs / base;
+  int ks = m->cus / base;
   if (ks > nc / 2) ks = nc / 2;
   return ks < 1 ? 1 : ks;
 }
@@ -452,6 +462,11 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (hipGetDevice(&m->device) != hipSuccess) {
     delete m;
     return fail(NMT_EDEVICE, "hipGetDevice failed");
+  }
+  if (hipDeviceGetAttribute(&m->cus, hipDeviceAttributeMultiprocessorCount, m->device) != hipSuccess ||
+      m->cus < 1) {
+    delete m;
+    return fail(NMT_EDEVICE, "cannot read the compute-unit count of device %d", m->device);
   }
   const int E = d.E, H = d.H, A = d.A, C = 2 * d.H, V = d.V;
   hipError_t e = hipSuccess;
@@ -585,7 +600,7 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
     }
     const bool split = src->enc_ks > 1 && p[0].A.nseg > 0 && p[1].A.nseg > 0;
     e = split ? launch_gemm_gru_split(p, 2, H, m->bf16, src->enc_ks, src->gru_part, S, st)
-              : launch_gemm_gru(p, 2, H, m->bf16, st);
+              : launch_gemm_gru(p, 2, H, m->bf16, m->cus, st);
   }
   if (e == hipSuccess) e = source_keys(m, src, st);
   if (e == hipSuccess && d_s0_out) {
@@ -728,7 +743,12 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   g1.ep = GruEpi{pool, H, state_row, pool_rows, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns,
                  s1, H, nullptr, 0, H};
   g1.ep.out16 = s1h;
-  if (e == hipSuccess) e = launch_gemm_gru(&g1, 1, H, m->bf16, st);
+  float* gpart = (float*)(ws + L.gpart);
+  auto run_gru = [&](const GruProblem& g, int ks) {
+    return ks > 1 ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, st)
+                  : launch_gemm_gru(&g, 1, H, m->bf16, m->cus, st);
+  };
+  if (e == hipSuccess) e = run_gru(g1, L.ks_g1);
   mark(NMT_PHASE_GRU1 + 1);
   // attention query q = s1 att_Wq
   if (e == hipSuccess) {
@@ -740,7 +760,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   if (e == hipSuccess) {
     const AttnGroups grp{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
     e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
-                         src->S, m->att_v, c, d_alpha, grp, c16, st);
+                         src->S, m->att_v, c, d_alpha, grp, c16, m->cus, st);
   }
   mark(NMT_PHASE_ATTENTION + 1);
   // second GRU: s_new = GRU(c, s1)
@@ -751,7 +771,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     g2.Npad = m->g2.Npad;
     g2.ep = GruEpi{s1, H, nullptr, 0, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H,
                    nullptr, 0, H};
-    e = launch_gemm_gru(&g2, 1, H, m->bf16, st);
+    e = run_gru(g2, L.ks_g2);
   }
   mark(NMT_PHASE_GRU2 + 1);
   // readout t = tanh(s_new Ws + x Wy + c Wc + b)

@@ -10,7 +10,9 @@
 namespace nmt {
 
 constexpr int kMaxTpad = 1024;     // attention keeps one score per source position in LDS
-constexpr int kNumCUs = 256;       // MI355X compute units (8 XCDs of 32)
+// Launch shapes that depend on how many blocks fill the chip take the
+// device's compute-unit count (read once per model; 256 on MI355X, in 8
+// XCDs of 32) as an argument named `cus`.
 
 // K chunk of the GEMM tiles: 8 sixteen-byte vectors of 4 fp32 or 8 bf16.
 inline int chunk_k(bool bf16) { return bf16 ? PrecBF16::KC : PrecF32::KC; }
@@ -39,14 +41,11 @@ constexpr int kGruTM = NMT_GRU_TM, kGruHB = 64, kGruWM = NMT_GRU_WM;
 constexpr int kGruTM16 = NMT_GRU_TM_BF16, kGruHB16 = NMT_GRU_HB_BF16, kGruWM16 = NMT_GRU_WM_BF16;  // bf16 weights
 inline int gru_hb(bool bf16) { return bf16 ? kGruHB16 : kGruHB; }
 // Rows of the GRU tile for small batches, used when the large tile would
-// give fewer than kGruSmallBlocks blocks.
+// give fewer blocks than there are compute units.
 #ifndef NMT_GRU_SMALL_TM
 #define NMT_GRU_SMALL_TM 64
 #endif
-#ifndef NMT_GRU_SMALL_BLOCKS
-#define NMT_GRU_SMALL_BLOCKS 256
-#endif
-constexpr int kGruSmallTM = NMT_GRU_SMALL_TM, kGruSmallBlocks = NMT_GRU_SMALL_BLOCKS;
+constexpr int kGruSmallTM = NMT_GRU_SMALL_TM;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 
@@ -114,7 +113,12 @@ struct GruProblem {
 
 // Launchers (all asynchronous on `st`).
 hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
-hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st);
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, int cus, hipStream_t st);
+// K splits for a GRU launch of M rows whose A operand has `nchunks` K chunks:
+// 1 when the launch fills the chip as it is, else enough splits of the
+// small-row tile for about two blocks per compute unit (each split at least
+// four chunks, at most 8 splits).  Its launch needs part [ksplit][M][4][H].
+int gru_ksplit(int M, int H, int nchunks, bool bf16, int cus);
 // The same with the K chunks split over ksplit blocks per tile: raw sums go
 // to part [nprob][ksplit][part_M][4][H] (part_M >= every problem's rows), a
 // second kernel adds them in split order and applies the cell.
@@ -122,7 +126,7 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
                                  int part_M, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
-int vocab_slices(int M, int V, bool bf16);
+int vocab_slices(int M, int V, bool bf16, int cus);
 int vocab_max_kpad(bool bf16);
 bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
 // Row stride of a bf16 copy of rows E wide: whole 16-byte vectors.
@@ -175,7 +179,7 @@ struct AttnGroups {
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
-                            hipStream_t st);
+                            int cus, hipStream_t st);
 hipError_t launch_bf16_to_f32(const void* x, int64_t rows, int cols, int64_t ld, float* y, hipStream_t st);
 // Per sentence of the keys pctx [S x Tpad x A] (A a multiple of 4):
 // kfac = 2^{2 log2(e) pctx}, exponent clamped to [-126, 126], and big[s] = 1

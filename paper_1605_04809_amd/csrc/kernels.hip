@@ -348,7 +348,7 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
   }
 }
 
-hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, hipStream_t st) {
+hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, int cus, hipStream_t st) {
   if (nprob < 1 || nprob > 2) return hipErrorInvalidValue;
   GruBatch b{};
   b.p[0] = probs[0];
@@ -371,8 +371,8 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   // fp32 also when the large tile's last round would be at most half full
   // (B = 2500 and 3000: GRU2 544 -> 434-440 us); bf16 there measured slower.
   const int64_t nbl = (int64_t)ceil_div(M, tm_large) * ceil_div(H, hb) * nprob;
-  const int64_t last = nbl % kNumCUs;
-  const bool small = nbl < kGruSmallBlocks || (!bf16 && last != 0 && last <= kNumCUs / 2);
+  const int64_t last = nbl % cus;
+  const bool small = nbl < cus || (!bf16 && last != 0 && last <= cus / 2);
   if (bf16) {
     if (small)
       run(std::integral_constant<int, kGruSmallTM>{}, std::integral_constant<int, kGruHB16>{},
@@ -389,6 +389,13 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
           std::integral_constant<int, kGruWM>{}, PrecF32{});
   }
   return hipGetLastError();
+}
+
+int gru_ksplit(int M, int H, int nchunks, bool bf16, int cus) {
+  const int64_t blocks = (int64_t)ceil_div(M, kGruSmallTM) * ceil_div(H, gru_hb(bf16));
+  int ks = (int)std::min<int64_t>(8, (2 * (int64_t)cus) / std::max<int64_t>(blocks, 1));
+  ks = std::min(ks, nchunks / 4);
+  return ks < 2 ? 1 : ks;
 }
 
 // Adds the K splits of a SPLIT launch in split order and applies the cell,
@@ -774,13 +781,13 @@ constexpr int kVocabBlockFixed = 4;
 static_assert(VocabTune<PrecF32>::VTM % 32 == 0 && VocabTune<PrecBF16>::VTM % 32 == 0 && kPlainSmallTM % 32 == 0,
               "row tiles in whole multiples of 32");
 constexpr int kVocabMaxSlices = 256;
-int vocab_slices(int M, int V, bool bf16) {
+int vocab_slices(int M, int V, bool bf16, int cus) {
   const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
   const int NB = (V + 31) / 32;
   int best = 8;
   double best_cost = 0;
   for (int nS = 8; nS <= kVocabMaxSlices && (nS == 8 || nS <= NB); nS += 8) {
-    const double rounds = (double)ceil_div((int64_t)nM * nS, kNumCUs);
+    const double rounds = (double)ceil_div((int64_t)nM * nS, cus);
     const double cost = rounds * ((double)NB / nS + kVocabBlockFixed);
     if (nS == 8 || cost < best_cost) {
       best_cost = cost;
@@ -1402,10 +1409,10 @@ __global__ __launch_bounds__(NW * 64) void k_attention_grouped(
 template <int G, int NQ>
 static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                               const int32_t* kbig, const float* ctx, const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
-                              float* alpha, int c_bf16, hipStream_t st) {
+                              float* alpha, int c_bf16, int cus, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
   const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
-  const int round = NMT_ATTN_SNAKE ? kNumCUs : 0;
+  const int round = NMT_ATTN_SNAKE ? cus : 0;
   // Few tiles (about two per CU or fewer, e.g. 2,000 rows in 20 sentences)
   // leave the CUs short of waves to hide memory latency with: twice the
   // waves per tile then take half the positions each (fp32 enru_b2000
@@ -1422,7 +1429,7 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
 template <int NQ>
 static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                          const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
-                         float* c, float* alpha, int c_bf16, hipStream_t st) {
+                         float* c, float* alpha, int c_bf16, int cus, hipStream_t st) {
   if (S > kGroupMaxS || !grp.perm) {
     hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len,
                        sent_id, S, v, c, alpha, c_bf16);
@@ -1433,24 +1440,24 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                      grp.n_tiles);
   if (G == kAttnGroup)
-    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, st);
+    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
   else
-    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, st);
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
 }
 
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
-                            const AttnGroups& grp, bool c_bf16, hipStream_t st) {
+                            const AttnGroups& grp, bool c_bf16, int cus, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    attention_nq<1>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<1>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
   else if (nq <= 2)
-    attention_nq<2>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<2>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
   else if (nq <= 4)
-    attention_nq<4>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<4>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
   else if (nq <= 8)
-    attention_nq<8>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, st);
+    attention_nq<8>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

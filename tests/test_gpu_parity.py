@@ -408,13 +408,13 @@ def _bytes_needed(nb, g, B):
     return int(re.search(r"(\d+) needed", str(ei.value)).group(1))
 
 
-@pytest.mark.parametrize("wtype,big,small", [("f32", 65, 64), ("bf16", 129, 128)])
+@pytest.mark.parametrize("wtype,big,small", [("f32", 257, 256), ("bf16", 257, 256)])
 def test_workspace_bytes_never_shrink_with_the_batch(gpu, wtype, big, small):
     """A workspace sized for B rows serves every smaller batch (a forest's
     levels, a shrinking phrase batch), although some smaller batches need
-    more bytes than B itself: a batch that fills whole row tiles of the
-    vocabulary kernel (64 rows fp32, 128 bf16) takes more slices than one
-    row more; such a call runs."""
+    more bytes than B itself: 256 rows fill whole row tiles, so the GRUs
+    split their K eight ways (and the vocabulary kernel takes more slices)
+    where 257 rows take six splits; such a call runs."""
     torch = _torch()
     from paper_1605_04809_amd import binding as nb
     wl = make_workload(CONFIGS["enru_b2000"].replace(B=big, S=2, len_lo=3, len_hi=5, Tpad=5, wtype=wtype, seed=45))
