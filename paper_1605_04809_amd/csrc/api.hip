@@ -291,7 +291,7 @@ int plain_ksplit(int M, int N, int K_total, int kc, Tile t, bool bf16, int cus) 
 // q on is dead while a GRU runs, so a GRU's split-K partial sums (gpart)
 // reuse that region, extended if they need more.
 struct WsLayout {
-  size_t s1, s1h, c, q, t, part, kpart, perm, tiles, ntiles, gpart, total;
+  size_t s1, s1h, c, q, t, part, kpart, perm, tiles, ntiles, zreq, gpart, total;
   int nS;             // vocabulary slices
   int ks_q, ks_ro;    // K splits of the query and readout GEMMs
   int ks_g1, ks_g2;   // K splits of the two GRUs (1: fused cell, no partials)
@@ -316,7 +316,11 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
-  L.ks_q = 1;  // measured: splitting the query GEMM's K (32 chunks) does not pay (B = 1000: 28 -> 32 us)
+  // The query GEMM splits its K only where its tiles leave at least half the
+  // CUs idle (the shrinking batches of a forest or phrase loop); at B = 1000
+  // (256 tiles) a split measured slower (28 -> 32 us).
+  const int tiles_q = ceil_div(B, kPlainSmallTM) * ceil_div(d.A, kPlainSmallTN);
+  L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->bf16, m->cus) : 1;
 
   L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16, m->cus);
   size_t kp = 0;
@@ -331,6 +335,8 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * 16);
   L.ntiles = off;
   off += al(4);
+  L.zreq = off;  // the requested words' logits
+  off += al((size_t)B * 4);
   // the GRUs' K splits: GRU1 reads [x | s_prev], GRU2 [s1 | c]
   const int kc = m->kc;
   const int kx = m->bf16 ? (int)m->emb_ld : d.E;
@@ -787,11 +793,14 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   }
   mark(NMT_PHASE_READOUT + 1);
   // vocabulary projection with an online log-sum-exp per slice, then the combine
-  if (e == hipSuccess) e = launch_vocab_lse(t, m->bf16, B, E, m->out, V, part, L.nS, st);
+  // rows with one request: the vocabulary kernel also picks out its logit
+  float* zreq = rq.req ? (float*)(ws + L.zreq) : nullptr;
+  if (e == hipSuccess)
+    e = launch_vocab_lse(t, m->bf16, B, E, m->out, V, part, L.nS, rq.req, rq.req_off, rq.nreq, zreq, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
     e = launch_lse_combine(B, part, L.nS, t, m->bf16, E, m->out, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,
-                           m->err, st);
+                           m->err, zreq, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && d_c)

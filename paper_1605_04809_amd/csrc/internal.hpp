@@ -133,10 +133,17 @@ bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
 inline __host__ __device__ int bf16_row(int E) { return (E + 7) / 8 * 8; }
 // t16: t is stored in bf16 (row stride bf16_row(E)) instead of fp32; the
 // kernels never use the padding slots' contents (with_bias_ones).
+// req1 (nullable): the requested words, one per row (req_off NULL) or CSR
+// (req_off [M+1] over nreq words); the logit of each row that requests
+// exactly one word goes to zreq [M] (rows whose word is outside [0, V), or
+// whose span is malformed, get nothing written).
 hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
-                            hipStream_t st);
+                            const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st);
 // Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same
-// indices (req_off nullable: one request per row, req[b] -> logp[b]).
+// indices (req_off nullable: one request per row, req[b] -> logp[b]).  The
+// combine takes the logits of rows with one request from zreq (the
+// vocabulary kernel's, nullable) and scores the other rows' words with dot
+// products of their own.
 // state_row (nullable) is checked against pool_rows like the other ids.
 struct Requests {
   const int32_t* req_off;
@@ -148,14 +155,11 @@ struct Requests {
 hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int t16, int E, const Packed& W, int V,
                               const Requests& rq, const int32_t* y_prev,
                               const int32_t* sent_id, int S, float* logp, float* logZ, int* err,
-                              hipStream_t st);
+                              const float* zreq, hipStream_t st);
 // Attention groups rows by sentence through workspace arrays: perm [B]
 // int32, tiles [B] int4, n_tiles [1] int32 (perm NULL: one block per row).
 constexpr int kGroupMaxS = 8192;  // sentences the grouping kernel can count in LDS
-#ifndef NMT_ATTN_GROUP
-#define NMT_ATTN_GROUP 4
-#endif
-constexpr int kAttnGroup = NMT_ATTN_GROUP;
+constexpr int kAttnGroup = 4;  // rows per attention tile (fewer when the tiles would not cover the CUs)
 #ifndef NMT_ATTN_WAVES
 #define NMT_ATTN_WAVES 8
 #endif

@@ -547,7 +547,10 @@ template <class P, int VPF>
 __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int t16, int M, int E,
                                                                       int nb, int Kpad, const f32x4* __restrict__ Wp,
                                                                       int64_t Npad, int V, int nM, int nS,
-                                                                      float2* __restrict__ part) {
+                                                                      float2* __restrict__ part,
+                                                                      const int32_t* __restrict__ req1,
+                                                                      const int32_t* __restrict__ req_off, int nreq,
+                                                                      float* __restrict__ zreq) {
   constexpr int VTM = VocabTune<P>::VTM, VNW = VocabTune<P>::VNW, VFN = VocabTune<P>::VFN;
   constexpr int FM = VTM / 32;
   __shared__ f32x4 As[VQMAX];
@@ -578,6 +581,25 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
   for (int i = 0; i < FM; ++i) {
     run_m[i] = -INFINITY;
     run_s[i] = 0.f;
+  }
+  // Rows that request exactly one word (req1[row], or with CSR offsets the
+  // one word of a well-formed span of length 1): the lane that holds its
+  // logit writes it to zreq[row] at the fold, so the combine needs no dot
+  // product of its own for them.  Loaded here: no vector-memory load may be
+  // issued in the loop (its wait would drain the prefetch ring).
+  int rq[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = m0 + 32 * i + l32;
+    rq[i] = -1;
+    if (req1 && row < M) {
+      if (!req_off) {
+        rq[i] = req1[row];
+      } else {
+        const int j0 = req_off[row], j1 = req_off[row + 1];
+        if (0 <= j0 && j1 == j0 + 1 && j1 <= nreq) rq[i] = req1[j0];
+      }
+    }
   }
 
   // Weight fragments are read through a buffer resource over the packed
@@ -712,6 +734,25 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
           for (int i = 0; i < FM; ++i) acc[i][f][r] = ok ? acc[i][f][r] : -INFINITY;
         }
     }
+    // A requested column in this group: column 32 (cb0 + f) + acc_row(r, h)
+    // sits in register r of block f of lane half h.  Only the group's blocks
+    // below cb_end are this slice's (the rest belong to the next slice and
+    // were masked above), so every column has exactly one writer; columns
+    // past V are never requested by a valid id.  Rarely taken.
+    const unsigned own = 32u * (unsigned)min(VFN, cb_end - cb0);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int d = rq[i] - 32 * cb0;
+      if ((unsigned)d < own && ((d >> 2) & 1) == h) {
+        const int ff = d >> 5, rr = ((d & 31) >> 3) * 4 + (d & 3);
+        float z = 0.f;
+#pragma unroll
+        for (int f = 0; f < VFN; ++f)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) z = (f == ff && r == rr) ? acc[i][f][r] : z;
+        zreq[m0 + 32 * i + l32] = z;
+      }
+    }
     // fold the group into each row slot's running log-sum-exp
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -808,7 +849,7 @@ int vocab_max_kpad(bool bf16) {
 
 template <class P>
 hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
-                     hipStream_t st) {
+                     const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
   const int nM = ceil_div(M, VocabTune<P>::VTM);
   dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
@@ -818,30 +859,31 @@ hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int
   auto fits = [&](int vpf) { return PF >= vpf && nkg % vpf == 0 && nkg >= 2 * vpf; };
   if (fits(16))
     hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2)>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp,
-                       W.Npad, V, nM, nS, part);
+                       W.Npad, V, nM, nS, part, req1, req_off, nreq, zreq);
   else if (fits(8))
     hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 8 ? 8 : 2)>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp,
-                       W.Npad, V, nM, nS, part);
+                       W.Npad, V, nM, nS, part, req1, req_off, nreq, zreq);
   else if (fits(4))
     hipLaunchKernelGGL((k_vocab_lse<P, 4>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
-                       part);
+                       part, req1, req_off, nreq, zreq);
   else if (fits(2))
     hipLaunchKernelGGL((k_vocab_lse<P, 2>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM, nS,
-                       part);
+                       part, req1, req_off, nreq, zreq);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
-                            hipStream_t st) {
+                            const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (t16 && !W.bf16) return hipErrorInvalidValue;
   if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1 || W.Npad < ((int64_t)V + 31) / 32 * 32 + 32)
     return hipErrorInvalidValue;
   if (!vocab_offsets_fit(W.Kpad, W.Npad, W.bf16)) return hipErrorInvalidValue;
-  return W.bf16 ? vocab_lse<PrecBF16>(t, t16, M, E, W, V, part, nS, st)
-                : vocab_lse<PrecF32>(t, 0, M, E, W, V, part, nS, st);
+  if (req1 && !zreq) return hipErrorInvalidValue;
+  return W.bf16 ? vocab_lse<PrecBF16>(t, t16, M, E, W, V, part, nS, req1, req_off, nreq, zreq, st)
+                : vocab_lse<PrecF32>(t, 0, M, E, W, V, part, nS, req1, req_off, nreq, zreq, st);
 }
 
 // ---------------------------------------------------- partials combine
@@ -872,7 +914,7 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
                                                      Requests rq,
                                                      const int32_t* __restrict__ y_prev,
                                                      const int32_t* __restrict__ sent_id, int S, float* logp,
-                                                     float* logZ, int* err) {
+                                                     float* logZ, int* err, const float* __restrict__ zreq) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= B) return;
   const int j0 = rq.req_off ? rq.req_off[row] : row, j1 = rq.req_off ? rq.req_off[row + 1] : row + 1;
@@ -902,6 +944,11 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
   }
   sum = wave_sum(sum);
   const float lz = mx + logf(sum);
+  if (lane == 0 && logZ) logZ[row] = lz;
+  if (zreq && j1 == j0 + 1) {  // one request: its logit taken by the vocabulary kernel
+    if (lane == 0) logp[j0] = zreq[row] - lz;
+    return;
+  }
   const char* tr = t16 ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
                        : (const char*)(t + (int64_t)row * E);
   for (int j = j0; j < j1; ++j) {
@@ -913,20 +960,19 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
     dot = wave_sum(dot);
     if (lane == 0) logp[j] = dot - lz;
   }
-  if (lane == 0 && logZ) logZ[row] = lz;
 }
 
 hipError_t launch_lse_combine(int B, const float2* part, int nS, const float* t, int t16, int E, const Packed& W, int V,
                               const Requests& rq, const int32_t* y_prev,
-                              const int32_t* sent_id, int S, float* logp, float* logZ, int* err, hipStream_t st) {
+                              const int32_t* sent_id, int S, float* logp, float* logZ, int* err, const float* zreq, hipStream_t st) {
   if (B <= 0) return hipSuccess;
   if (W.Krows != E || W.nbias < 1 || (t16 && !W.bf16)) return hipErrorInvalidValue;
   if (W.bf16)
     hipLaunchKernelGGL(k_lse_combine<PrecBF16>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, t16, E,
-                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
+                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err, zreq);
   else
     hipLaunchKernelGGL(k_lse_combine<PrecF32>, dim3(ceil_div(B, 4)), dim3(256), 0, st, B, part, nS, t, 0, E,
-                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err);
+                       W.nbias, (int)W.Kpad, (const f32x4*)W.d, W.Npad, V, rq, y_prev, sent_id, S, logp, logZ, err, zreq);
   return hipGetLastError();
 }
 
@@ -1229,7 +1275,7 @@ __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const 
   }
 }
 
-// Sums G values (G a power of two, 2 <= G <= 64) over the 64 lanes of a
+// Sums G values (G a power of two, 1 <= G <= 64) over the 64 lanes of a
 // wave: each butterfly step halves the values a lane keeps, so the G sums
 // cost about log2(64) + G shuffles instead of G * log2(64).  On return the
 // sum of value g sits in every lane whose bits 5, 4, ... (the top log2(G)
@@ -1260,7 +1306,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
                                                const int32_t* __restrict__ len, const int32_t* __restrict__ perm,
                                                const float* __restrict__ v, float* __restrict__ c,
                                                float* __restrict__ alpha, f32x4* qs, float* e, int* rows, int wave,
-                                               int lane, int A4, int C4, int c_bf16) {
+                                               int lane, int A4, int C4, int c_bf16, int npg) {
   constexpr int NT = NW * 64;
   const int s = tl.x, n = tl.z;
   if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? perm[tl.y + threadIdx.x] : 0;
@@ -1337,8 +1383,16 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
       for (int i = lane; i < Tpad; i += 64) alpha[(int64_t)rows[g] * Tpad + i] = i < L ? eg[i] : 0.f;
   }
   __syncthreads();
+  // Context.  With more threads than float4 columns (npg > 1), the threads
+  // of position group pg take the column k4 = tid % C4 over the pg-th of npg
+  // contiguous ranges of positions, and group 0 adds the other groups'
+  // partial sums (left in LDS over the queries, dead by now) in group order:
+  // each thread then waits for a fraction of the annotations' round trips.
   const f32x4* X = (const f32x4*)(ctx + (int64_t)s * Tpad * C);
-  for (int k4 = threadIdx.x; k4 < C4; k4 += NT) {
+  const int pg = npg > 1 ? (int)threadIdx.x / C4 : 0;
+  const int i_lo = npg > 1 ? L * pg / npg : 0, i_hi = npg > 1 ? L * (pg + 1) / npg : L;
+  const int k_first = npg > 1 ? (int)threadIdx.x - pg * C4 : (int)threadIdx.x;
+  for (int k4 = k_first; k4 < C4 && pg < npg; k4 += (npg > 1 ? C4 : NT)) {
     f32x4 acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = zero4();
@@ -1356,19 +1410,37 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
     // loads are in flight per wave instead of one or two (each round trip to
     // L2 or beyond is otherwise paid once per position); the sums still run
     // over the positions in order.
-    int i = 0;
-    for (; i + NMT_ATTN_CU <= L; i += NMT_ATTN_CU) {
-      f32x4 x[NMT_ATTN_CU];
+    // Tiles of fewer rows hold fewer accumulators and keep twice the loads
+    // in flight.
+    constexpr int CU = G >= 4 ? NMT_ATTN_CU : 2 * NMT_ATTN_CU;
+    int i = i_lo;
+    for (; i + CU <= i_hi; i += CU) {
+      f32x4 x[CU];
 #pragma unroll
-      for (int u = 0; u < NMT_ATTN_CU; ++u) x[u] = X[(int64_t)(i + u) * C4 + k4];
+      for (int u = 0; u < CU; ++u) x[u] = X[(int64_t)(i + u) * C4 + k4];
 #pragma unroll
-      for (int u = 0; u < NMT_ATTN_CU; ++u) add(x[u], i + u);
+      for (int u = 0; u < CU; ++u) add(x[u], i + u);
     }
-    for (; i < L; ++i) add(X[(int64_t)i * C4 + k4], i);
+    for (; i < i_hi; ++i) add(X[(int64_t)i * C4 + k4], i);
+    if (npg > 1) {
+      if (pg > 0) {
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-      if (g < n) store_c4(c, (int64_t)rows[g] * C + 4 * k4, acc[g], c_bf16);
+        for (int g = 0; g < G; ++g) qs[((pg - 1) * G + g) * C4 + k4] = acc[g];
+      }
+      __syncthreads();
+      if (pg == 0) {
+        for (int q = 1; q < npg; ++q)
+#pragma unroll
+          for (int g = 0; g < G; ++g) acc[g] += qs[((q - 1) * G + g) * C4 + k4];
+      }
+    }
+    if (pg == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (g < n) store_c4(c, (int64_t)rows[g] * C + 4 * k4, acc[g], c_bf16);
+    }
   }
+  if (npg > 1 && (int)threadIdx.x >= npg * C4) __syncthreads();  // threads without a column still meet the barrier
 }
 
 // One block (NW waves) per tile of up to G rows of one sentence.  The rows'
@@ -1379,19 +1451,20 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
 // scores; finally every thread accumulates a float4 piece of the context of
 // all rows, reading each annotation once.
 template <int G, int NQ, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attention_grouped(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NQ <= 4 ? 8 : 1))) void k_attention_grouped(
     int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ pctx,
     const int32_t* __restrict__ kbig, const float* __restrict__ ctx, const int32_t* __restrict__ len,
     const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
-    float* __restrict__ alpha, int c_bf16, int round) {
-  extern __shared__ f32x4 dyn[];  // queries [G][A/4], then scores [G][Tpad]
+    float* __restrict__ alpha, int c_bf16, int round, int npg) {
+  // queries [G][A/4] (later the context's partial sums [npg-1][G][C/4]), then scores [G][Tpad]
+  extern __shared__ f32x4 dyn[];
   __shared__ int rows[G];
   const int nt = *n_tiles;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int A4 = A / 4, C4 = C / 4;
   f32x4* qs = dyn;
-  float* e = (float*)(dyn + G * A4);
+  float* e = (float*)(dyn + max(G * A4, (npg - 1) * G * C4));
   int t = blockIdx.x;
   if (t >= nt) return;
   // Blocks are handed to the CUs in order, one per CU per round of `round`
@@ -1403,7 +1476,7 @@ __global__ __launch_bounds__(NW * 64) void k_attention_grouped(
     if (r & 1) t = r * round + (min(round, nt - r * round) - 1 - p);
   }
   attention_tile<G, NQ, NW>(tiles[t], A, C, Tpad, q, kfac, pctx, kbig, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
-                            lane, A4, C4, c_bf16);
+                            lane, A4, C4, c_bf16, npg);
 }
 
 template <int G, int NQ>
@@ -1411,19 +1484,30 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
                               const int32_t* kbig, const float* ctx, const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
                               float* alpha, int c_bf16, int cus, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
-  const size_t lds = ((size_t)G * A + (size_t)G * Tpad) * 4;
   const int round = NMT_ATTN_SNAKE ? cus : 0;
+  // Position groups of the context phase: whole waves per group (C/4 a
+  // multiple of 64), so every wave meets its one barrier.
+  const int C4 = C / 4;
+  auto groups = [&](int nt) { return (C4 % 64 == 0 && nt >= 2 * C4) ? nt / C4 : 1; };
+  auto lds_bytes = [&](int npg) {
+    return (size_t)std::max(G * (A / 4), (npg - 1) * G * C4) * 16 + (size_t)G * Tpad * 4;
+  };
   // Few tiles (about two per CU or fewer, e.g. 2,000 rows in 20 sentences)
   // leave the CUs short of waves to hide memory latency with: twice the
   // waves per tile then take half the positions each (fp32 enru_b2000
   // 41.9 -> 36.1 us).  With four tiles per CU (4,096 rows) 8 waves measured
   // faster (70.6 against 75.1 us).
-  if (grid <= kAttnWideTiles)
-    hipLaunchKernelGGL((k_attention_grouped<G, NQ, 2 * kAttnWaves>), dim3(grid), dim3(2 * kAttnWaves * 64), lds, st, A,
-                       C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
-  else
-    hipLaunchKernelGGL((k_attention_grouped<G, NQ, kAttnWaves>), dim3(grid), dim3(kAttnWaves * 64), lds, st, A, C,
-                       Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16, round);
+  if (grid <= kAttnWideTiles) {
+    const int npg = groups(2 * kAttnWaves * 64);
+    hipLaunchKernelGGL((k_attention_grouped<G, NQ, 2 * kAttnWaves>), dim3(grid), dim3(2 * kAttnWaves * 64),
+                       lds_bytes(npg), st, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles,
+                       v, c, alpha, c_bf16, round, npg);
+  } else {
+    const int npg = groups(kAttnWaves * 64);
+    hipLaunchKernelGGL((k_attention_grouped<G, NQ, kAttnWaves>), dim3(grid), dim3(kAttnWaves * 64), lds_bytes(npg), st,
+                       A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16,
+                       round, npg);
+  }
 }
 
 template <int NQ>
@@ -1435,14 +1519,23 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
                        sent_id, S, v, c, alpha, c_bf16);
     return;
   }
-  // rows per tile: kAttnGroup when their queries and scores fit 64 KB of LDS, else 4
-  const int G = ((size_t)kAttnGroup * (A + Tpad) * 4 <= 65536) ? kAttnGroup : 4;
+  // Rows per tile: 4, so that a block reads each key and annotation once for
+  // four rows.  A tile runs on one CU, so with few tiles the longest
+  // sentence's tile sets the kernel's duration (about 26 us for 80 positions,
+  // whatever the batch): batches that would give fewer tiles than half the
+  // CUs take tiles of 2 rows, or 1, spreading the same work over more CUs.
+  // (At 1,000 rows of one sentence, 2-row tiles measured slower, 32 -> 40 us:
+  // twice the tiles read the one sentence's keys at once.)
+  int G = kAttnGroup;
+  while (G > 1 && 2 * ceil_div(B, G) < cus) G /= 2;
   hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                      grp.n_tiles);
-  if (G == kAttnGroup)
-    attention_grouped<kAttnGroup, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
-  else
+  if (G >= 4)
     attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
+  else if (G == 2)
+    attention_grouped<2, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
+  else
+    attention_grouped<1, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
 }
 
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,

@@ -156,9 +156,10 @@ def test_attention_at_paper_width_every_row(gpu, case):
     lane covers four float4 pieces of the query) with inputs where attention
     matters: unit-gain weights and N(0, 1) annotations, so each row's scores
     spread over its positions (zeroing att_v moves alpha by about 0.4, see
-    test_parity_inputs).  Three launch shapes: blocks of 16 waves (at most
-    640 tiles), of 8 waves (more tiles, as bf16_b4096 runs) and one row per
-    block (more than 8192 sentences).  Every row, every output."""
+    test_parity_inputs).  Every launch shape: tiles of 4, 2 and 1 rows in
+    blocks of 16 waves (at most 640 tiles), tiles of 4 rows in blocks of 8
+    waves (more tiles, as bf16_b4096 runs), and one row per block (more than
+    8192 sentences).  Every row, every output."""
     _torch()
     cfg = ATT.replace(**ATT_CASES[case])
     grid, waves = attention_grid(cfg.B, cfg.S, cfg.A)
@@ -190,7 +191,7 @@ def test_attention_signal_at_paper_dimensions_every_row(gpu, wtype):
     g.close()
 
 
-@pytest.mark.parametrize("case", ["grouped_16_waves", "per_row"])
+@pytest.mark.parametrize("case", ["g4_16w", "per_row"])
 def test_keys_beyond_the_factor_range_every_row(gpu, case):
     """Keys up to about |pctx| = 66 against queries of either sign up to about
     75, so many terms tanh(k + q) pair a key whose factor 2^{2 log2(e) k}

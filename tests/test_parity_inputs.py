@@ -31,7 +31,7 @@ def _zero_upper_query(p):  # what a bug in the lanes past the first 256 attentio
     p["att_Wq"] = q
 
 
-@pytest.mark.parametrize("cfg,seed", [(ATT.replace(**ATT_CASES["grouped_16_waves"]), 72), (PAPER_SIGNAL, 74)],
+@pytest.mark.parametrize("cfg,seed", [(ATT.replace(**ATT_CASES["g1_16w"]), 72), (PAPER_SIGNAL, 74)],
                          ids=["A1024_small", "paper_dims"])
 @pytest.mark.parametrize("broken", [_zero_v, _zero_upper_query], ids=["uniform_attention", "upper_query_lanes"])
 def test_attention_mistakes_move_outputs_far_beyond_the_bar(cfg, seed, broken):
@@ -67,7 +67,7 @@ def _clamped_factor_alpha(pctx, q, v, sent_id, src_len):
     return out
 
 
-@pytest.mark.parametrize("case", ["grouped_16_waves", "per_row"])
+@pytest.mark.parametrize("case", ["g4_16w", "per_row"])
 def test_large_keys_defeat_clamped_factors(case):
     """On the inputs of test_keys_beyond_the_factor_range_every_row, scoring
     every term from clamped factors would miss the oracle's attention weights
