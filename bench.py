@@ -517,6 +517,26 @@ def bench_workload(name, args, cpu_seconds, headline=False):
         raise SystemExit(f"{name}: non-finite log-probabilities")
 
     ms_step = ms_total / K
+    graph = None
+    if not cfg.phrase_max and cfg.B <= 128:
+        # Small batches are launch-bound: the same step captured once in a
+        # HIP graph (torch.cuda.CUDAGraph over the library's launches on the
+        # capture stream) and replayed, K replays between two events.
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            for _ in range(3):
+                nb.nmt_score_batch(model, src, s_prev, y_prev, sent_id, req, logp, s_new, logZ, workspace=ws)
+        stream.wait_stream(cap)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            nb.nmt_score_batch(model, src, s_prev, y_prev, sent_id, req, logp, s_new, logZ, workspace=ws)
+        for _ in range(args.warmup):
+            g.replay()
+        per_g, tot_g = _events_pass(torch, stream, g.replay, K)
+        graph = {"ms_per_step": tot_g / K, "ms_per_step_median": float(np.median(per_g)),
+                 "note": "the step captured once in a HIP graph and replayed (same kernels, same inputs)"}
     total_flops, vocab_flops = step_flops(cfg, wl.src_len, row_sent)
     peak = PEAK_TFLOPS[cfg.wtype]
     vocab_ms = phases["vocab"] / K
@@ -542,6 +562,8 @@ def bench_workload(name, args, cpu_seconds, headline=False):
         "encode": {"ms": float(np.median(enc_ms)), "sentences": cfg.S,
                    "ms_per_sentence": float(np.median(enc_ms)) / cfg.S},
     }
+    if graph:
+        res["graph"] = graph
     if cfg.phrase_max:
         res["config"].update(hypotheses=cfg.B, phrase_tokens="U{1..%d}" % cfg.phrase_max, scored_tokens=scored)
         res["timing"] = ("one step = nmt_score_forest over the 500 phrases: one batched step per depth, the "
@@ -629,8 +651,9 @@ def main():
     if "cpu_baseline" in head:
         out["cpu_baseline"] = head["cpu_baseline"]
     for k in ("ms_per_step_median", "ms_per_step_p10_p90", "step_tflops", "mfma_util_step_pct", "phase_ms",
-              "ms_per_step_with_phase_events", "encode"):
-        out[k] = head[k]
+              "ms_per_step_with_phase_events", "encode", "graph"):
+        if k in head:
+            out[k] = head[k]
     out["mfma_util_vocab_pct"] = 100.0 * out["roofline"]["frac"]
     if not args.only:
         # The other workloads, each timed the same way in this process (their

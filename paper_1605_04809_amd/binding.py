@@ -36,7 +36,8 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_profile_end", "nmt_score_forest_step", "nmt_forest_build", "nmt_forest_shape",
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
            "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
-           "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy")
+           "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy",
+           "nmt_debug_alloc_hook")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -113,6 +114,8 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_rescorer_info.argtypes = [_VP, _I32, P(_VP), IP, IP, IP, IP, IP]
     lib.nmt_rescorer_destroy.argtypes = [_VP]
     lib.nmt_rescorer_destroy.restype = None
+    lib.nmt_debug_alloc_hook.argtypes = [_I32]
+    lib.nmt_debug_alloc_hook.restype = ctypes.c_int64
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
@@ -123,6 +126,13 @@ def load_library(path: str = LIB_PATH):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def debug_alloc_hook(fail_after: int) -> int:
+    """Test hook (nmt_debug.h): make device allocations fail after
+    ``fail_after`` more (negative: never); returns the library's live
+    device allocations."""
+    return int(load_library().nmt_debug_alloc_hook(fail_after))
 
 
 def last_error() -> str:

@@ -14,8 +14,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmt.so")
 SOURCES = ("kernels.hip", "api.hip", "forest.hip")
+HOST_SOURCES = ("forest_host.cpp",)   # plain C++, compiled by the host compiler
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CXX = os.environ.get("CXX", "g++")
 # Packed-FP32 VALU instructions are disabled for all device code.
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-munsafe-fp-atomics"]
@@ -37,6 +39,16 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
             r = subprocess.run(cmd, capture_output=True, text=True)
             if r.returncode != 0:
                 raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr[-6000:]}")
+            objs.append(obj)
+        for src in HOST_SOURCES:
+            obj = os.path.join(tmp, src.replace(".cpp", ".o"))
+            cmd = [CXX, "-O2", "-std=c++17", "-fPIC", "-Wall", "-I", "/opt/rocm/include", "-c",
+                   os.path.join(CSRC, src), "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"{CXX} failed on {src}:\n{r.stderr[-6000:]}")
             objs.append(obj)
         out_tmp = out + ".tmp"
         cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", out_tmp]

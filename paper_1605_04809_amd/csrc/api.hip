@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <cmath>
 #include <mutex>
 #include <string>
@@ -14,6 +15,7 @@
 #include <vector>
 
 #include "../../include/nmt.h"
+#include "../../include/nmt_debug.h"
 #include "../../include/nmt_profile.h"
 #include "internal.hpp"
 
@@ -22,6 +24,11 @@ using namespace nmt;
 namespace {
 
 thread_local std::string g_err;
+
+// The allocation test hook (nmt_debug.h): allocations left before injected
+// failures (-1: none), and the library's live device allocations.
+std::atomic<int64_t> g_alloc_budget{-1};
+std::atomic<int64_t> g_live_allocs{0};
 
 nmt_status fail(nmt_status st, const char* fmt, ...) {
   char buf[512];
@@ -50,7 +57,7 @@ struct Allocs {
   std::vector<size_t> bytes;
   std::vector<uint8_t> kind;
   hipError_t alloc(void** p, size_t n, uint8_t k = kOther) {
-    hipError_t e = hipMalloc(p, n < 256 ? 256 : n);
+    hipError_t e = device_malloc(p, n < 256 ? 256 : n);
     if (e == hipSuccess) {
       ptrs.push_back(*p);
       bytes.push_back(n);
@@ -59,7 +66,7 @@ struct Allocs {
     return e;
   }
   void release() {
-    for (void* p : ptrs) (void)hipFree(p);
+    for (void* p : ptrs) device_free(p);
     ptrs.clear();
     bytes.clear();
     kind.clear();
@@ -439,7 +446,35 @@ hipError_t noalloc_scratch(int dev, void** out) {
 
 }  // namespace
 
+namespace nmt {
+
+hipError_t device_malloc(void** p, size_t bytes) {
+  int64_t b = g_alloc_budget.load();
+  while (b >= 0) {
+    if (b == 0) {
+      *p = nullptr;
+      return hipErrorOutOfMemory;
+    }
+    if (g_alloc_budget.compare_exchange_weak(b, b - 1)) break;
+  }
+  const hipError_t e = hipMalloc(p, bytes);
+  if (e == hipSuccess) ++g_live_allocs;
+  return e;
+}
+
+void device_free(void* p) {
+  if (!p) return;
+  if (hipFree(p) == hipSuccess) --g_live_allocs;
+}
+
+}  // namespace nmt
+
 extern "C" {
+
+int64_t nmt_debug_alloc_hook(int32_t fail_after) {
+  g_alloc_budget.store(fail_after < 0 ? -1 : fail_after);
+  return g_live_allocs.load();
+}
 
 const char* nmt_last_error(void) { return g_err.c_str(); }
 

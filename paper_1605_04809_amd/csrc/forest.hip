@@ -1,61 +1,21 @@
-// forest.hip -- the ScoreBatch procedure of the paper (Section 5.1,
-// Figure 2) over a forest of per-hypothesis prefix trees (Figure 1).
-//
-// Given (hypothesis, target phrase) pairs, the phrases of each hypothesis
-// are collapsed into a prefix tree, and every tree depth costs one batched
-// decoder step, so the number of steps is the longest phrase length however
-// many pairs there are.  With the step's convention (input: previous word and
-// the state before it; output: the distribution over the next word and the
-// state after it), one step row serves a whole tree node: a node with
-// children is a row whose input is the node's word (the hypothesis' last word
-// for a root) and the state produced by its parent's row, and whose requested
-// words are its children's words.  The requests of a level are the edges of
-// the paper's per-depth dashed boxes; rows requesting the same parent state
-// are not duplicated.  Input states are gathered on the device from the
-// previous level's output rows, so states stay in device memory across
-// depths.
+// forest.hip -- the device side of the ScoreBatch procedure of the paper
+// (Section 5.1, Figure 2) over a forest of per-hypothesis prefix trees
+// (Figure 1), and of stack rescoring (Section 5.3, Figure 4).  The trees
+// and their per-depth step rows are built on the host (forest_host.cpp);
+// here every tree depth costs one batched decoder step, so the number of
+// steps is the longest phrase length however many pairs there are.  Input
+// states are gathered on the device from the previous level's output rows,
+// so states stay in device memory across depths.
 #include <stdint.h>
 
-#include <string>
-#include <unordered_map>
 #include <vector>
 
-#include "../../include/nmt.h"
+#include "forest.hpp"
 #include "internal.hpp"
 
 using namespace nmt;
 
-struct nmt_forest {
-  int32_t n_hyp = 0, n_pairs = 0, depth = 0;
-  int32_t n_rows = 0, n_req = 0, max_rows = 0;
-  std::vector<int32_t> rows_lv, req_lv;      // per level (1-based level d at index d-1)
-  std::vector<int32_t> row_base, req_base;   // first global row / request of each level
-  std::vector<int32_t> off_base;             // first offset entry of each level
-  // per global row
-  std::vector<int32_t> state_row;  // level 1: hypothesis index; deeper: global row of the parent node's row
-  std::vector<int32_t> y_prev, sent;
-  std::vector<int32_t> req_off;   // per level, rows+1 offsets local to the level
-  std::vector<int32_t> req;       // per global request: the requested word
-  std::vector<int32_t> req_row;   // per global request: its global row
-  std::vector<int32_t> pair_path; // [n_pairs x depth] global request index per depth, -1 past the end
-  std::vector<int32_t> upload;    // all of the above index arrays, in the device workspace order
-};
-
-namespace nmt {
-nmt_status forest_fail(nmt_status st, const char* msg);
-}
-
 namespace {
-
-struct Node {
-  int32_t parent;  // -1 for roots
-  int32_t word;    // edge word (roots: the hypothesis' last word)
-  int32_t hyp;
-  int32_t depth;
-  int32_t row = -1;               // global row of this node's step (if it has children)
-  std::vector<int32_t> children;  // in creation order
-  std::vector<int32_t> child_req; // global request index of each child edge
-};
 
 __global__ void k_path_sum(int n_pairs, int depth, const int32_t* __restrict__ path, const float* __restrict__ logp,
                            float* __restrict__ out) {
@@ -105,147 +65,6 @@ static ForestWs forest_ws(const nmt_model* m, const nmt_forest* f) {
 }
 
 extern "C" {
-
-nmt_status nmt_forest_build(int32_t n_hyp, const int32_t* h_hyp_word, const int32_t* h_hyp_sent, int32_t n_pairs,
-                            const int32_t* h_pair_hyp, const int32_t* h_phrase_off, const int32_t* h_phrase_words,
-                            nmt_forest** out) {
-  if (!out) return forest_fail(NMT_EINVAL, "NULL output");
-  *out = nullptr;
-  if (n_hyp < 0 || n_pairs < 0) return forest_fail(NMT_EINVAL, "negative count");
-  if ((n_hyp > 0 && (!h_hyp_word || !h_hyp_sent)) || (n_pairs > 0 && (!h_pair_hyp || !h_phrase_off)))
-    return forest_fail(NMT_EINVAL, "a required host array is NULL");
-  if (n_pairs > 0 && h_phrase_off[0] != 0) return forest_fail(NMT_EINVAL, "phrase offsets must start at 0");
-  for (int p = 0; p < n_pairs; ++p) {
-    if (h_pair_hyp[p] < 0 || h_pair_hyp[p] >= n_hyp) return forest_fail(NMT_ERANGE, "pair hypothesis out of range");
-    if (h_phrase_off[p + 1] < h_phrase_off[p]) return forest_fail(NMT_EINVAL, "phrase offsets must not decrease");
-  }
-  if (n_pairs > 0 && h_phrase_off[n_pairs] > 0 && !h_phrase_words)
-    return forest_fail(NMT_EINVAL, "phrase words are NULL");
-
-  nmt_forest* f = new nmt_forest();
-  f->n_hyp = n_hyp;
-  f->n_pairs = n_pairs;
-  // prefix trees: one root per hypothesis with a non-empty phrase
-  std::vector<Node> nodes;
-  std::vector<int32_t> root(n_hyp, -1);
-  std::unordered_map<uint64_t, int32_t> child_of;  // (node, word) -> child node
-  std::vector<std::vector<int32_t>> pair_nodes(n_pairs);
-  int32_t depth = 0;
-  for (int p = 0; p < n_pairs; ++p) {
-    const int h = h_pair_hyp[p], len = h_phrase_off[p + 1] - h_phrase_off[p];
-    if (len == 0) continue;
-    if (root[h] < 0) {
-      root[h] = (int32_t)nodes.size();
-      nodes.push_back(Node{-1, h_hyp_word[h], h, 0});
-    }
-    int32_t cur = root[h];
-    for (int k = 0; k < len; ++k) {
-      const int32_t w = h_phrase_words[h_phrase_off[p] + k];
-      const uint64_t key = ((uint64_t)(uint32_t)cur << 32) | (uint32_t)w;
-      auto it = child_of.find(key);
-      int32_t nxt;
-      if (it == child_of.end()) {
-        nxt = (int32_t)nodes.size();
-        nodes.push_back(Node{cur, w, h, nodes[cur].depth + 1});
-        nodes[cur].children.push_back(nxt);
-        child_of.emplace(key, nxt);
-      } else {
-        nxt = it->second;
-      }
-      pair_nodes[p].push_back(nxt);
-      cur = nxt;
-    }
-    if (len > depth) depth = len;
-  }
-  f->depth = depth;
-  // levels: level d holds the nodes of depth d-1 that have children, in creation order
-  std::vector<std::vector<int32_t>> by_depth(depth + 1);
-  for (int32_t i = 0; i < (int32_t)nodes.size(); ++i)
-    if (nodes[i].depth < depth && !nodes[i].children.empty()) by_depth[nodes[i].depth].push_back(i);
-  f->rows_lv.resize(depth);
-  f->req_lv.resize(depth);
-  f->row_base.resize(depth);
-  f->req_base.resize(depth);
-  f->off_base.resize(depth);
-  int32_t grow = 0, greq = 0, goff = 0;
-  for (int d = 1; d <= depth; ++d) {
-    const auto& lv = by_depth[d - 1];
-    f->row_base[d - 1] = grow;
-    f->req_base[d - 1] = greq;
-    f->off_base[d - 1] = goff;
-    f->rows_lv[d - 1] = (int32_t)lv.size();
-    int32_t local = 0;
-    for (int32_t id : lv) {
-      Node& n = nodes[id];
-      n.row = grow++;
-      f->state_row.push_back(n.parent < 0 ? n.hyp : nodes[n.parent].row);
-      f->y_prev.push_back(n.word);
-      f->sent.push_back(h_hyp_sent[n.hyp]);
-      f->req_off.push_back(local);
-      for (int32_t c : n.children) {
-        n.child_req.push_back(greq++);
-        f->req.push_back(nodes[c].word);
-        f->req_row.push_back(n.row);
-        ++local;
-      }
-    }
-    f->req_off.push_back(local);
-    goff += (int32_t)lv.size() + 1;
-    f->req_lv[d - 1] = local;
-    if ((int32_t)lv.size() > f->max_rows) f->max_rows = (int32_t)lv.size();
-  }
-  f->n_rows = grow;
-  f->n_req = greq;
-  // each pair's path: the request of its edge at every depth
-  f->pair_path.assign((size_t)n_pairs * depth, -1);
-  for (int p = 0; p < n_pairs; ++p)
-    for (size_t k = 0; k < pair_nodes[p].size(); ++k) {
-      const Node& child = nodes[pair_nodes[p][k]];
-      const Node& par = nodes[child.parent];
-      for (size_t c = 0; c < par.children.size(); ++c)
-        if (par.children[c] == pair_nodes[p][k]) f->pair_path[(size_t)p * depth + k] = par.child_req[c];
-    }
-  for (const std::vector<int32_t>* v : {&f->state_row, &f->y_prev, &f->sent, &f->req_off, &f->req, &f->pair_path})
-    f->upload.insert(f->upload.end(), v->begin(), v->end());
-  *out = f;
-  return NMT_OK;
-}
-
-void nmt_forest_destroy(nmt_forest* f) { delete f; }
-
-nmt_status nmt_forest_shape(const nmt_forest* f, int32_t* depth, int32_t* n_rows, int32_t* n_req, int32_t* max_rows) {
-  if (!f) return forest_fail(NMT_EINVAL, "NULL forest");
-  if (depth) *depth = f->depth;
-  if (n_rows) *n_rows = f->n_rows;
-  if (n_req) *n_req = f->n_req;
-  if (max_rows) *max_rows = f->max_rows;
-  return NMT_OK;
-}
-
-nmt_status nmt_forest_level(const nmt_forest* f, int32_t d, int32_t* rows, int32_t* nreq, int32_t* h_state_row,
-                            int32_t* h_y_prev, int32_t* h_sent_id, int32_t* h_req_off, int32_t* h_req) {
-  if (!f) return forest_fail(NMT_EINVAL, "NULL forest");
-  if (d < 1 || d > f->depth) return forest_fail(NMT_EINVAL, "level out of range");
-  const int32_t R = f->rows_lv[d - 1], Q = f->req_lv[d - 1], r0 = f->row_base[d - 1], q0 = f->req_base[d - 1];
-  if (rows) *rows = R;
-  if (nreq) *nreq = Q;
-  for (int32_t i = 0; i < R; ++i) {
-    if (h_state_row) h_state_row[i] = f->state_row[r0 + i];
-    if (h_y_prev) h_y_prev[i] = f->y_prev[r0 + i];
-    if (h_sent_id) h_sent_id[i] = f->sent[r0 + i];
-  }
-  if (h_req_off)
-    for (int32_t i = 0; i <= R; ++i) h_req_off[i] = f->req_off[f->off_base[d - 1] + i];
-  if (h_req)
-    for (int32_t j = 0; j < Q; ++j) h_req[j] = f->req[q0 + j];
-  return NMT_OK;
-}
-
-nmt_status nmt_forest_pair_paths(const nmt_forest* f, int32_t* h_path) {
-  if (!f || !h_path) return forest_fail(NMT_EINVAL, "NULL argument");
-  for (size_t i = 0; i < f->pair_path.size(); ++i) h_path[i] = f->pair_path[i];
-  return NMT_OK;
-}
 
 size_t nmt_forest_workspace_bytes(const nmt_model* m, const nmt_forest* f) {
   if (!m || !f) return 0;
@@ -328,16 +147,16 @@ struct DevBuf {
   // Grows to at least `bytes` (contents are not kept); the stream is idle here.
   hipError_t ensure(size_t bytes) {
     if (bytes <= cap) return hipSuccess;
-    if (p) (void)hipFree(p);
+    device_free(p);
     p = nullptr;
     cap = 0;
     const size_t want = bytes + bytes / 4 + 4096;
-    hipError_t e = hipMalloc(&p, want);
+    hipError_t e = device_malloc(&p, want);
     if (e == hipSuccess) cap = want;
     return e;
   }
   void release() {
-    if (p) (void)hipFree(p);
+    device_free(p);
     p = nullptr;
     cap = 0;
   }
@@ -392,7 +211,7 @@ nmt_status nmt_rescorer_create(int32_t K, nmt_model* const* models, const nmt_so
     const int32_t H = nmt_internal_hidden(models[k]);
     r->H.push_back(H);
     float* p = nullptr;
-    e = hipMalloc((void**)&p, (size_t)capacity * H * 4);
+    e = device_malloc((void**)&p, (size_t)capacity * H * 4);
     if (e == hipSuccess) {
       r->pool.push_back(p);
       // hypotheses 0..S-1: the empty hypothesis of each sentence, state s0
@@ -414,7 +233,7 @@ nmt_status nmt_rescorer_create(int32_t K, nmt_model* const* models, const nmt_so
 void nmt_rescorer_destroy(nmt_rescorer* r) {
   if (!r) return;
   (void)hipDeviceSynchronize();
-  for (float* p : r->pool) (void)hipFree(p);
+  for (float* p : r->pool) device_free(p);
   r->ws.release();
   r->nodes.release();
   r->pair_logp.release();
@@ -441,29 +260,13 @@ nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent
   hipStream_t st = (hipStream_t)stream;
 
   // Predecessor extraction: identical (parent, phrase) pairs are one entry of L.
-  std::unordered_map<std::string, int32_t> seen;
-  std::vector<int32_t> pair_of(n), pair_hyp, pair_off{0}, pair_words;
-  for (int32_t j = 0; j < n; ++j) {
-    const int32_t len = h_off[j + 1] - h_off[j];
-    std::string key((const char*)&h_parent[j], 4);
-    key.append((const char*)(h_words + h_off[j]), (size_t)len * 4);
-    auto it = seen.find(key);
-    if (it != seen.end()) {
-      pair_of[j] = it->second;
-      continue;
-    }
-    const int32_t p = (int32_t)pair_hyp.size();
-    seen.emplace(std::move(key), p);
-    pair_of[j] = p;
-    pair_hyp.push_back(h_parent[j]);
-    pair_words.insert(pair_words.end(), h_words + h_off[j], h_words + h_off[j + 1]);
-    pair_off.push_back((int32_t)pair_words.size());
-  }
-  const int32_t np = (int32_t)pair_hyp.size();
+  Predecessors P;
+  extract_predecessors(n, h_parent, h_off, h_words, &P);
+  const int32_t np = (int32_t)P.pair_hyp.size();
   // ScoreBatch over all predecessors: hypothesis ids index the forest's roots and the pools.
   nmt_forest* f = nullptr;
-  nmt_status rc = nmt_forest_build(r->n_hyp, r->last_word.data(), r->sent.data(), np, pair_hyp.data(),
-                                   pair_off.data(), pair_words.data(), &f);
+  nmt_status rc = nmt_forest_build(r->n_hyp, r->last_word.data(), r->sent.data(), np, P.pair_hyp.data(),
+                                   P.pair_off.data(), P.pair_words.data(), &f);
   if (rc != NMT_OK) return rc;
   const int32_t depth = f->depth, n_rows = f->n_rows;
   int32_t maxH = 0;
@@ -482,14 +285,8 @@ nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent
     nmt_forest_destroy(f);
     return forest_fail(e == hipErrorOutOfMemory ? NMT_ENOMEM : NMT_EDEVICE, hipGetErrorString(e));
   }
-  // Where each new hypothesis' state comes from: the forest row that requested
-  // its phrase's last word, or its parent's state for an empty phrase.
-  r->h_gather.resize((size_t)2 * n);
-  for (int32_t j = 0; j < n; ++j) {
-    const int32_t p = pair_of[j], len = pair_off[p + 1] - pair_off[p];
-    r->h_gather[j] = len == 0 ? -(pair_hyp[p] + 1) : f->req_row[f->pair_path[(size_t)p * depth + len - 1]];
-    r->h_gather[n + j] = r->n_hyp + j;
-  }
+  // Where each new hypothesis' state comes from, and where it goes.
+  gather_plan(f, P, n, r->n_hyp, &r->h_gather);
   int32_t* d_gather = (int32_t*)r->gather.p;
   float* d_pair_logp = (float*)r->pair_logp.p;
   e = hipMemcpyAsync(d_gather, r->h_gather.data(), (size_t)2 * n * 4, hipMemcpyHostToDevice, st);
@@ -515,7 +312,7 @@ nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent
   if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
   // Look up p for each hypothesis' predecessor; number the new hypotheses.
   for (int k = 0; k < r->K; ++k)
-    for (int32_t j = 0; j < n; ++j) h_logp[(size_t)k * n + j] = r->h_pair_logp[(size_t)k * np + pair_of[j]];
+    for (int32_t j = 0; j < n; ++j) h_logp[(size_t)k * n + j] = r->h_pair_logp[(size_t)k * np + P.pair_of[j]];
   for (int32_t j = 0; j < n; ++j) {
     const int32_t len = h_off[j + 1] - h_off[j];
     r->last_word.push_back(len > 0 ? h_words[h_off[j + 1] - 1] : r->last_word[h_parent[j]]);

@@ -208,6 +208,11 @@ hipError_t launch_average(int K, int64_t n, const ModelTable& tab, int kind, boo
                           hipStream_t st);
 hipError_t launch_weighted_sum(int K, int B, const float* logp, const ModelTable& tab, float* out, hipStream_t st);
 
+// Every device allocation and release of the library (the test hook of
+// nmt_debug.h can make allocations fail, and counts live ones).
+hipError_t device_malloc(void** p, size_t bytes);
+void device_free(void* p);
+
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
