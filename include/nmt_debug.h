@@ -3,7 +3,9 @@
  *
  * Lets a test make the library's device allocations fail, to check that
  * every call that allocates reports NMT_ENOMEM and releases what it had
- * allocated when an allocation fails part-way.
+ * allocated when an allocation fails part-way, and choose which of the two
+ * bf16 GRU kernel forms a call takes, so that both are checked at sizes the
+ * reference implementation finishes quickly.
  */
 #ifndef NMT_DEBUG_H
 #define NMT_DEBUG_H
@@ -20,6 +22,16 @@ extern "C" {
  * not thread-safe against concurrent library calls.  Returns the number of
  * the library's device allocations alive at the time of the call. */
 int64_t nmt_debug_alloc_hook(int32_t fail_after);
+
+/* The kernel form of the bf16 GRUs of Section 5.1's decoder step: 0 (the
+ * default) streams the weights from L2 into registers where the operand
+ * shape allows it (H a multiple of 128, state side then input side) and the
+ * batch gives every compute unit a block; 1 streams wherever the shape
+ * allows it, whatever the batch; 2 always stages both operands through LDS.
+ * The two forms add the same products in a different order, so results
+ * agree to rounding, not bit for bit.  Process-wide.  Returns the previous
+ * form, or -1 (and changes nothing) for a form outside 0..2. */
+int32_t nmt_debug_gru_form(int32_t form);
 
 #ifdef __cplusplus
 }

@@ -476,6 +476,11 @@ int64_t nmt_debug_alloc_hook(int32_t fail_after) {
   return g_live_allocs.load();
 }
 
+int32_t nmt_debug_gru_form(int32_t form) {
+  if (form < 0 || form > 2) return -1;
+  return nmt::g_gru_form.exchange(form);
+}
+
 const char* nmt_last_error(void) { return g_err.c_str(); }
 
 nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out) {

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "device.hpp"
 
 namespace nmt {
@@ -46,6 +48,10 @@ inline int gru_hb(bool bf16) { return bf16 ? kGruHB16 : kGruHB; }
 #define NMT_GRU_SMALL_TM 64
 #endif
 constexpr int kGruSmallTM = NMT_GRU_SMALL_TM;
+// Which GRU kernel form bf16 problems take: 0 the weight-streaming one where
+// it applies and fills the chip, 1 wherever it applies, 2 never (a test
+// switch, set through nmt_debug_gru_form).
+extern std::atomic<int> g_gru_form;
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 

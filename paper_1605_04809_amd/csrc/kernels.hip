@@ -348,6 +348,8 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
   }
 }
 
+static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream_t st);
+
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, int cus, hipStream_t st) {
   if (nprob < 1 || nprob > 2) return hipErrorInvalidValue;
   GruBatch b{};
@@ -367,6 +369,7 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
     dim3 grid(ceil_div(M, TM), ceil_div(H, HB), nprob);
     hipLaunchKernelGGL((k_gemm_gru<TM, HB, WM, P>), grid, dim3((TM / WM) * (HB / 32) * 64), 0, st, b);
   };
+  if (nprob == 1 && try_gru_ws(probs[0], H, bf16, cus, st)) return hipGetLastError();
   const int tm_large = bf16 ? kGruTM16 : kGruTM, hb = gru_hb(bf16);
   // fp32 also when the large tile's last round would be at most half full
   // (B = 2500 and 3000: GRU2 544 -> 434-440 us); bf16 there measured slower.
@@ -463,6 +466,227 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gru_cell, dim3(ceil_div((int64_t)M * H, (int64_t)256), nprob), dim3(256), 0, st, b, H);
   return hipGetLastError();
+}
+
+// ------------------------------------- weight-streaming GRU GEMM (bf16 weights)
+//
+// With bf16 weights the LDS-staged GRU tile above runs MFMAs 8x faster per k
+// than with fp32 ones, so the fixed costs of each 64-k chunk (the staging
+// loads, the transposed LDS stores of both operands, the barrier) dominate
+// it (GRU2 at B = 4096: 38 % MFMA busy).  This form keeps only the
+// activations in LDS and streams the packed weights from L2 straight into
+// registers, as the vocabulary kernel does.  A block holds 128 rows x 128
+// hidden units; wave w computes rows 64 (w & 1) .. 64 (w & 1) + 63 and units
+// 32 (w >> 1) .. of the block, all three gates with the candidate split by
+// side, so each weight fragment feeds two MFMAs and each activation fragment
+// three.  Activations go through registers into one of two LDS stages in
+// chunks of 128 k, one barrier per 8 k steps.  The MFMA puts the weights on
+// its row operand and the activations on its column operand, so register r of
+// a lane's gate accumulator is unit 8 (r / 4) + 4 h + r % 4 of the wave's 32
+// for the lane's batch row: the cell runs lane-locally in the epilogue.
+// Used for an A operand of two bf16 segments, state side then input side,
+// each in whole 128-k chunks (the second GRU: [s1 | c]), when the grid
+// covers the CUs.
+constexpr int kWsTM = 128, kWsUB = 128, kWsKQ = 16, kWsVPF = 4;
+
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k_gru_ws(GruProblem Pb) {
+  using P = PrecBF16;
+  constexpr int TM = kWsTM, KQW = kWsKQ, NKS = KQW / 2, VPF = kWsVPF, NT = 512;
+  constexpr int NA = TM * KQW / NT;  // activation vectors per thread per chunk
+  static_assert(NKS % VPF == 0, "ring slots fixed within a chunk");
+  __shared__ f32x4 As[2 * KQW * TM];  // [stage][vector][row ^ (vector & 15)]
+  const AOperand& A = Pb.A;
+  const int M = A.M;
+  const int m0 = blockIdx.x * TM;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int h = lane >> 5, l32 = lane & 31, wr = wave & 1;
+  const int u0 = blockIdx.y * kWsUB + 32 * (wave >> 1);
+  const int64_t Npad = Pb.Npad;
+  const int nch = total_chunks(A) / 2;  // 128-k chunks
+  const int last_gk = nch * NKS - 1;
+  // weights: packed column tile u0 / HB holds [r | z | n] of HB units, and a
+  // wave's 32 units lie in one tile
+  constexpr int HB = kGruHB16;
+  static_assert(HB % 32 == 0, "a wave's units within one packed tile");
+  const int c_r = (u0 / HB) * 3 * HB + u0 % HB;
+  const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(Pb.Wp, (int64_t)nch * KQW * Npad * 16);
+  const int lo_r = (int)(((int64_t)h * Npad + c_r + l32) * 16);
+  const int lo_z = lo_r + HB * 16, lo_n = lo_r + 2 * HB * 16;
+  const int kbytes = (int)(2 * Npad * 16);  // one k step: two packed vector rows
+  auto wload = [&](f32x4(&d)[3], int gk) {
+    const int so = (gk < last_gk ? gk : last_gk) * kbytes;  // past the end: re-read the last step (unused)
+    d[0] = buf_load(wres, lo_r, so);
+    d[1] = buf_load(wres, lo_z, so);
+    d[2] = buf_load(wres, lo_n, so);
+  };
+
+  // activation staging: this thread's vectors are row (tid + i NT) / KQW,
+  // vector (tid + i NT) % KQW of each chunk, from segment 0 (state side, the
+  // first c1 chunks) or segment 1 (input side)
+  const ASeg sg0 = seg_at(A, 0), sg1 = seg_at(A, 1);
+  const int c1 = sg0.nchunk / 2;
+  const __amdgpu_buffer_rsrc_t res0 = buffer_rsrc(sg0.p, seg_bytes(sg0, M));
+  const __amdgpu_buffer_rsrc_t res1 = buffer_rsrc(sg1.p, seg_bytes(sg1, M));
+  int roff0[NA], roff1[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = m0 + ((int)threadIdx.x + i * NT) / KQW;
+    roff0[i] = seg_row_off(sg0, row, M);
+    roff1[i] = seg_row_off(sg1, row, M);
+  }
+  f32x4 ra[NA];
+  auto aload = [&](int c) {  // chunk c of the whole A
+    const bool second = c >= c1;
+    const int kseg = (second ? c - c1 : c) * KQW * P::KV;
+    const int K = second ? sg1.K : sg0.K;
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int kin = P::KV * (((int)threadIdx.x + i * NT) % KQW);
+      f32x4 unused;
+      load_a_raw<P, true>(second ? res1 : res0, second ? roff1[i] : roff0[i], K, kseg + kin, kin, kseg * 2, ra[i],
+                          unused);
+    }
+  };
+  auto astore = [&](int stage) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int idx = (int)threadIdx.x + i * NT, row = idx / KQW, v = idx % KQW;
+      As[stage * KQW * TM + v * TM + (row ^ (v & 15))] = ra[i];
+    }
+  };
+  // fragment of k step ks (vectors 2 ks + h) for the 32 rows at r0
+  auto afrag = [&](int stage, int ks, int r0) {
+    const int v = 2 * ks + h;
+    return As[stage * KQW * TM + v * TM + ((r0 + l32) ^ (v & 15))];
+  };
+
+  f32x16 ar[2], az[2], ani[2], ans[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) ar[i] = az[i] = ani[i] = ans[i] = f32x16{};
+  f32x4 ring[VPF][3];
+#pragma unroll
+  for (int p = 0; p < VPF; ++p) wload(ring[p], p);
+  aload(0);
+  astore(0);
+  if (nch > 1) aload(1);
+  __syncthreads();
+
+  const int r0 = 64 * wr;
+  // Chunks [cb, ce) of one segment, its side fixed at compile time (a
+  // per-chunk branch would shuttle the accumulators between register files).
+  auto run = [&](int cb, int ce, auto side_c) {
+    constexpr bool SIDE = decltype(side_c)::value;
+    for (int c = cb; c < ce; ++c) {
+      const int st = c & 1;
+      f32x4 a0 = afrag(st, 0, r0), a1 = afrag(st, 0, r0 + 32);
+      static_for<NKS>([&](auto kc) {
+        constexpr int ks = decltype(kc)::value, slot = ks % VPF;
+        f32x4 n0 = a0, n1 = a1;
+        if constexpr (ks + 1 < NKS) {
+          n0 = afrag(st, ks + 1, r0);
+          n1 = afrag(st, ks + 1, r0 + 32);
+        }
+        P::mma(ring[slot][0], a0, ar[0]);
+        P::mma(ring[slot][0], a1, ar[1]);
+        P::mma(ring[slot][1], a0, az[0]);
+        P::mma(ring[slot][1], a1, az[1]);
+        if constexpr (SIDE) {
+          P::mma(ring[slot][2], a0, ans[0]);
+          P::mma(ring[slot][2], a1, ans[1]);
+        } else {
+          P::mma(ring[slot][2], a0, ani[0]);
+          P::mma(ring[slot][2], a1, ani[1]);
+        }
+        wload(ring[slot], c * NKS + ks + VPF);  // refill the slot just consumed, VPF steps ahead
+        // one MFMA, the next step's fragment reads, the other MFMAs, the refill
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 3, 0);
+        a0 = n0;
+        a1 = n1;
+      });
+      if (c + 1 < nch) astore(st ^ 1);
+      if (c + 2 < nch) aload(c + 2);
+      __syncthreads();
+    }
+  };
+  // state side first, then input side (each segment's side fixed at compile
+  // time; a runtime choice between the two loops doubled the live registers)
+  run(0, c1, std::true_type{});
+  run(c1, nch, std::false_type{});
+
+  // the cell, lane-locally: register r of row fragment i is unit u0 + 8 (r / 4) + 4 h + r % 4 of row r0 + 32 i + l32
+  const GruEpi& ep = Pb.ep;
+  const int H = ep.H;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = m0 + r0 + 32 * i + l32;
+    if (row >= M) continue;
+    int hr = row;
+    bool hok = true;
+    if (ep.h && ep.hrow) {
+      hr = ep.hrow[row];
+      hok = hr >= 0 && hr < ep.hrows;
+    }
+    const bool keep = !ep.mask_len || ep.mask_pos < ep.mask_len[row];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j0 = u0 + 8 * q + 4 * h;
+      if (j0 >= H) continue;
+      const f32x4 br = *(const f32x4*)(ep.brz + j0), bz = *(const f32x4*)(ep.brz + H + j0);
+      const f32x4 bni = *(const f32x4*)(ep.bni + j0), bns = *(const f32x4*)(ep.bns + j0);
+      const f32x4 hp = (ep.h && hok) ? *(const f32x4*)(ep.h + (int64_t)hr * ep.ldh + j0) : zero4();
+      f32x4 xr = zero4(), xz = zero4(), xn = zero4();
+      if (ep.xin) {
+        const float* x = ep.xin + (int64_t)row * ep.ldx;
+        xr = *(const f32x4*)(x + j0);
+        xz = *(const f32x4*)(x + H + j0);
+        xn = *(const f32x4*)(x + 2 * H + j0);
+      }
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * q + e;
+        const float hn = gru_cell(ar[i][r], az[i][r], ani[i][r], ans[i][r], br[e], bz[e], bni[e], bns[e], xr[e],
+                                  xz[e], xn[e], hp[e]);
+        o[e] = keep ? hn : 0.f;
+      }
+      *(f32x4*)(ep.out + (int64_t)row * ep.ldo + j0) = o;
+      if (ep.out16) {
+        typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+        *(bf16x4_t*)(ep.out16 + (int64_t)row * ep.ldo + j0) = bf16x4_t{(__bf16)o[0], (__bf16)o[1], (__bf16)o[2],
+                                                                         (__bf16)o[3]};
+      }
+    }
+  }
+}
+
+std::atomic<int> g_gru_form{0};
+
+static bool aligned(const void* p, int bytes) { return ((uintptr_t)p % bytes) == 0; }
+
+// The weight-streaming form for one bf16 problem, if it applies (see above);
+// returns false to let the caller launch the LDS-staged tile instead.
+static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream_t st) {
+  const int form = g_gru_form.load(std::memory_order_relaxed);
+  if (form == 2) return false;
+  // H a multiple of the block's 128 units: every wave's packed columns then
+  // lie inside the matrix's rows, so no weight load leaves the matrix
+  if (!bf16 || H % kWsUB || p.A.M <= 0 || p.A.nseg != 2) return false;
+  for (int i = 0; i < 2; ++i)
+    if (!p.A.seg[i].bf16 || p.A.seg[i].nchunk % 2 || p.A.seg[i].side != 1 - i || p.A.seg[i].gather) return false;
+  // the epilogue's vector accesses: 16-byte aligned rows of the state,
+  // candidate input, output and bias arrays, 8-byte ones of the bf16 output
+  const GruEpi& ep = p.ep;
+  if ((ep.h && (ep.ldh % 4 || !aligned(ep.h, 16))) || ep.ldo % 4 || !aligned(ep.out, 16) ||
+      (ep.out16 && !aligned(ep.out16, 8)) || (ep.xin && (ep.ldx % 4 || !aligned(ep.xin, 16))) ||
+      !aligned(ep.brz, 16) || !aligned(ep.bni, 16) || !aligned(ep.bns, 16))
+    return false;
+  const int64_t blocks = (int64_t)ceil_div(p.A.M, kWsTM) * ceil_div(H, kWsUB);
+  if (form == 0 && blocks < cus) return false;
+  hipLaunchKernelGGL(k_gru_ws, dim3(ceil_div(p.A.M, kWsTM), ceil_div(H, kWsUB)), dim3(512), 0, st, p);
+  return true;
 }
 
 // ------------------------------------------------ vocabulary projection
