@@ -25,13 +25,19 @@ int64_t nmt_debug_alloc_hook(int32_t fail_after);
 
 /* The kernel form of the bf16 GRUs of Section 5.1's decoder step: 0 (the
  * default) streams the weights from L2 into registers where the operand
- * shape allows it (H a multiple of 128, state side then input side) and the
- * batch gives every compute unit a block; 1 streams wherever the shape
- * allows it, whatever the batch; 2 always stages both operands through LDS.
- * The two forms add the same products in a different order, so results
- * agree to rounding, not bit for bit.  Process-wide.  Returns the previous
- * form, or -1 (and changes nothing) for a form outside 0..2. */
+ * shape allows it (H a multiple of 128; for the first GRU, an embedding
+ * width padded to a multiple of 128) and the batch gives every compute unit
+ * a block; 1 streams wherever the shape allows it, whatever the batch, and
+ * skips the split over K that small batches otherwise take; 2 always stages
+ * both operands through LDS.  Both forms accumulate the same bf16 products
+ * 16 at a time in increasing k, so where neither splits K they give the same
+ * states.  Process-wide.  Returns the previous form, or -1 (and changes
+ * nothing) for a form outside 0..2. */
 int32_t nmt_debug_gru_form(int32_t form);
+
+/* How many GRU launches of the process took the weight-streaming form, so a
+ * test can tell which form ran. */
+int64_t nmt_debug_gru_streamed(void);
 
 #ifdef __cplusplus
 }

@@ -37,7 +37,7 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
            "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
            "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy",
-           "nmt_debug_alloc_hook", "nmt_debug_gru_form")
+           "nmt_debug_alloc_hook", "nmt_debug_gru_form", "nmt_debug_gru_streamed")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -118,6 +118,8 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_debug_alloc_hook.restype = ctypes.c_int64
     lib.nmt_debug_gru_form.argtypes = [_I32]
     lib.nmt_debug_gru_form.restype = _I32
+    lib.nmt_debug_gru_streamed.argtypes = []
+    lib.nmt_debug_gru_streamed.restype = ctypes.c_int64
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
@@ -141,6 +143,11 @@ def debug_gru_form(form: int) -> int:
     """Test hook (nmt_debug.h): 0 automatic, 1 weight-streaming bf16 GRU
     wherever its shape applies, 2 LDS-staged only; returns the previous."""
     return int(load_library().nmt_debug_gru_form(form))
+
+
+def debug_gru_streamed() -> int:
+    """Test hook (nmt_debug.h): GRU launches so far that streamed weights."""
+    return int(load_library().nmt_debug_gru_streamed())
 
 
 def last_error() -> str:

@@ -481,6 +481,8 @@ int32_t nmt_debug_gru_form(int32_t form) {
   return nmt::g_gru_form.exchange(form);
 }
 
+int64_t nmt_debug_gru_streamed(void) { return nmt::g_gru_streamed.load(); }
+
 const char* nmt_last_error(void) { return g_err.c_str(); }
 
 nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out) {
@@ -791,7 +793,10 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   g1.ep.out16 = s1h;
   float* gpart = (float*)(ws + L.gpart);
   auto run_gru = [&](const GruProblem& g, int ks) {
-    return ks > 1 ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, st)
+    // (the test switch's form 1 skips the K split, which the streamed form
+    // never takes, so that small batches reach the streamed form)
+    return ks > 1 && g_gru_form.load(std::memory_order_relaxed) != 1
+               ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, st)
                   : launch_gemm_gru(&g, 1, H, m->bf16, m->cus, st);
   };
   if (e == hipSuccess) e = run_gru(g1, L.ks_g1);

@@ -52,6 +52,7 @@ constexpr int kGruSmallTM = NMT_GRU_SMALL_TM;
 // it applies and fills the chip, 1 wherever it applies, 2 never (a test
 // switch, set through nmt_debug_gru_form).
 extern std::atomic<int> g_gru_form;
+extern std::atomic<int64_t> g_gru_streamed;  // launches of the weight-streaming form
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 

@@ -484,14 +484,24 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
 // its row operand and the activations on its column operand, so register r of
 // a lane's gate accumulator is unit 8 (r / 4) + 4 h + r % 4 of the wave's 32
 // for the lane's batch row: the cell runs lane-locally in the epilogue.
-// Used for an A operand of two bf16 segments, state side then input side,
-// each in whole 128-k chunks (the second GRU: [s1 | c]), when the grid
-// covers the CUs.
-constexpr int kWsTM = 128, kWsUB = 128, kWsKQ = 16, kWsVPF = 4;
+// Used for an A operand of two segments in whole 128-k chunks, one on each
+// side: FIRST_STATE says whether segment 0 is the state side (the second
+// GRU: [s1 | c]) or the input side (the first: [x | s_prev]), SRC16_i
+// whether segment i is stored in bf16 (else fp32, rounded to bf16 as it is
+// staged, which takes VPF = 2 weight steps in flight to keep the registers
+// within two waves per SIMD).  Taken when the grid covers the CUs.
+constexpr int kWsTM = 128, kWsUB = 128, kWsKQ = 16;
+#ifndef NMT_WS_VPF_BF16_SRC   // weight steps in flight, both segments bf16
+#define NMT_WS_VPF_BF16_SRC 4
+#endif
+#ifndef NMT_WS_VPF_F32_SRC    // weight steps in flight with an fp32 segment
+#define NMT_WS_VPF_F32_SRC 2
+#endif
 
+template <bool FIRST_STATE, bool SRC16_0, bool SRC16_1, int VPF>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k_gru_ws(GruProblem Pb) {
   using P = PrecBF16;
-  constexpr int TM = kWsTM, KQW = kWsKQ, NKS = KQW / 2, VPF = kWsVPF, NT = 512;
+  constexpr int TM = kWsTM, KQW = kWsKQ, NKS = KQW / 2, NT = 512;
   constexpr int NA = TM * KQW / NT;  // activation vectors per thread per chunk
   static_assert(NKS % VPF == 0, "ring slots fixed within a chunk");
   __shared__ f32x4 As[2 * KQW * TM];  // [stage][vector][row ^ (vector & 15)]
@@ -520,13 +530,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
     d[2] = buf_load(wres, lo_n, so);
   };
 
-  // activation staging: this thread's vectors are row (tid + i NT) / KQW,
-  // vector (tid + i NT) % KQW of each chunk, from segment 0 (state side, the
-  // first c1 chunks) or segment 1 (input side)
+  // activation staging: this thread's vectors are rows tid / KQW + 32 i,
+  // vector tid % KQW of each chunk, from segment 0 (the first c1 chunks) or
+  // segment 1
+  static_assert(NT / KQW == 32 && KQW == 16, "staging rows 32 apart");
   const ASeg sg0 = seg_at(A, 0), sg1 = seg_at(A, 1);
   const int c1 = sg0.nchunk / 2;
   const __amdgpu_buffer_rsrc_t res0 = buffer_rsrc(sg0.p, seg_bytes(sg0, M));
   const __amdgpu_buffer_rsrc_t res1 = buffer_rsrc(sg1.p, seg_bytes(sg1, M));
+  const int kin = P::KV * ((int)threadIdx.x % KQW);
   int roff0[NA], roff1[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
@@ -534,30 +546,45 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
     roff0[i] = seg_row_off(sg0, row, M);
     roff1[i] = seg_row_off(sg1, row, M);
   }
-  f32x4 ra[NA];
+  f32x4 ra[NA], rb[NA];  // rb: the second half of an fp32 source vector
   auto aload = [&](int c) {  // chunk c of the whole A
-    const bool second = c >= c1;
-    const int kseg = (second ? c - c1 : c) * KQW * P::KV;
-    const int K = second ? sg1.K : sg0.K;
+    if constexpr (SRC16_0 == SRC16_1) {
+      // one load sequence with the segment's resource, offsets and width
+      // selected (a branch here gets merged by the compiler into a
+      // dynamically indexed copy of the segments in scratch memory)
+      const bool second = c >= c1;
+      const int kseg = (second ? c - c1 : c) * KQW * P::KV;
+      const int K = second ? sg1.K : sg0.K;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int kin = P::KV * (((int)threadIdx.x + i * NT) % KQW);
-      f32x4 unused;
-      load_a_raw<P, true>(second ? res1 : res0, second ? roff1[i] : roff0[i], K, kseg + kin, kin, kseg * 2, ra[i],
-                          unused);
+      for (int i = 0; i < NA; ++i)
+        load_a_raw<P, SRC16_0>(second ? res1 : res0, second ? roff1[i] : roff0[i], K, kseg + kin, kin,
+                               kseg * (SRC16_0 ? 2 : 4), ra[i], rb[i]);
+    } else if (c < c1) {  // a uniform branch between the two load sequences
+      const int kseg = c * KQW * P::KV;
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        load_a_raw<P, SRC16_0>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * (SRC16_0 ? 2 : 4), ra[i], rb[i]);
+    } else {
+      const int kseg = (c - c1) * KQW * P::KV;
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        load_a_raw<P, SRC16_1>(res1, roff1[i], sg1.K, kseg + kin, kin, kseg * (SRC16_1 ? 2 : 4), ra[i], rb[i]);
     }
   };
-  auto astore = [&](int stage) {
+  // (row ^ v) = (tid / KQW ^ v) + 32 i for row = tid / KQW + 32 i and v < 16:
+  // one swizzled base per thread, the rest immediate offsets
+  const int st_base = ((int)threadIdx.x % KQW) * TM + (((int)threadIdx.x / KQW) ^ ((int)threadIdx.x % KQW));
+  auto astore = [&](int stage, int c) {  // c: the chunk the staged data belongs to
+    const bool s16 = c < c1 ? SRC16_0 : SRC16_1;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int idx = (int)threadIdx.x + i * NT, row = idx / KQW, v = idx % KQW;
-      As[stage * KQW * TM + v * TM + (row ^ (v & 15))] = ra[i];
-    }
+    for (int i = 0; i < NA; ++i)
+      As[stage * KQW * TM + st_base + 32 * i] = s16 ? ra[i] : a_from_raw<P, false>(ra[i], rb[i]);
   };
-  // fragment of k step ks (vectors 2 ks + h) for the 32 rows at r0
+  // fragment of k step ks (vectors 2 ks + h) for the 32 rows at r0;
+  // (r0 + l32) ^ v = r0 + (l32 ^ v) for r0 a multiple of 32 and v < 16
   auto afrag = [&](int stage, int ks, int r0) {
     const int v = 2 * ks + h;
-    return As[stage * KQW * TM + v * TM + ((r0 + l32) ^ (v & 15))];
+    return As[stage * KQW * TM + r0 + v * TM + (l32 ^ v)];
   };
 
   f32x16 ar[2], az[2], ani[2], ans[2];
@@ -567,7 +594,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
   for (int p = 0; p < VPF; ++p) wload(ring[p], p);
   aload(0);
-  astore(0);
+  astore(0, 0);
   if (nch > 1) aload(1);
   __syncthreads();
 
@@ -606,15 +633,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
         a0 = n0;
         a1 = n1;
       });
-      if (c + 1 < nch) astore(st ^ 1);
+      if (c + 1 < nch) astore(st ^ 1, c + 1);
       if (c + 2 < nch) aload(c + 2);
       __syncthreads();
     }
   };
-  // state side first, then input side (each segment's side fixed at compile
-  // time; a runtime choice between the two loops doubled the live registers)
-  run(0, c1, std::true_type{});
-  run(c1, nch, std::false_type{});
+  // segment 0's side, then segment 1's (each fixed at compile time; a runtime
+  // choice between the two loops doubled the live registers)
+  run(0, c1, std::integral_constant<bool, FIRST_STATE>{});
+  run(c1, nch, std::integral_constant<bool, !FIRST_STATE>{});
 
   // the cell, lane-locally: register r of row fragment i is unit u0 + 8 (r / 4) + 4 h + r % 4 of row r0 + 32 i + l32
   const GruEpi& ep = Pb.ep;
@@ -663,6 +690,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 }
 
 std::atomic<int> g_gru_form{0};
+std::atomic<int64_t> g_gru_streamed{0};
 
 static bool aligned(const void* p, int bytes) { return ((uintptr_t)p % bytes) == 0; }
 
@@ -674,8 +702,8 @@ static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream
   // H a multiple of the block's 128 units: every wave's packed columns then
   // lie inside the matrix's rows, so no weight load leaves the matrix
   if (!bf16 || H % kWsUB || p.A.M <= 0 || p.A.nseg != 2) return false;
-  for (int i = 0; i < 2; ++i)
-    if (!p.A.seg[i].bf16 || p.A.seg[i].nchunk % 2 || p.A.seg[i].side != 1 - i || p.A.seg[i].gather) return false;
+  const ASeg &s0 = p.A.seg[0], &s1 = p.A.seg[1];
+  if (s0.nchunk % 2 || s1.nchunk % 2 || s0.side == s1.side) return false;
   // the epilogue's vector accesses: 16-byte aligned rows of the state,
   // candidate input, output and bias arrays, 8-byte ones of the bf16 output
   const GruEpi& ep = p.ep;
@@ -685,7 +713,14 @@ static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream
     return false;
   const int64_t blocks = (int64_t)ceil_div(p.A.M, kWsTM) * ceil_div(H, kWsUB);
   if (form == 0 && blocks < cus) return false;
-  hipLaunchKernelGGL(k_gru_ws, dim3(ceil_div(p.A.M, kWsTM), ceil_div(H, kWsUB)), dim3(512), 0, st, p);
+  const dim3 grid(ceil_div(p.A.M, kWsTM), H / kWsUB), block(512);
+  if (s0.side == 1 && s0.bf16 && s1.bf16)  // the second GRU: [s1 | c]
+    hipLaunchKernelGGL((k_gru_ws<true, true, true, NMT_WS_VPF_BF16_SRC>), grid, block, 0, st, p);
+  else if (s0.side == 0 && s0.bf16 && !s1.bf16)  // the first: [x | s_prev (fp32)]
+    hipLaunchKernelGGL((k_gru_ws<false, true, false, NMT_WS_VPF_F32_SRC>), grid, block, 0, st, p);
+  else
+    return false;
+  g_gru_streamed.fetch_add(1, std::memory_order_relaxed);
   return true;
 }
 

@@ -1,18 +1,20 @@
 """GPU parity of the two kernel forms of the bf16 decoder GRUs (Section 5.1).
 
-With bf16 weights the second GRU of the step (operand [s1 | c], state side
-first) can run in a form that streams the packed weights from L2 straight
-into registers, instead of staging both operands through LDS.  The library
-takes it only where the batch fills the chip (4,096 rows at H = 1024), a size
-the oracle checks on sampled rows elsewhere; here the test switch
+With bf16 weights both GRUs of the step (operands [x | s_prev] and [s1 | c])
+can run in a form that streams the packed weights from L2 straight into
+registers, instead of staging both operands through LDS.  The library takes
+it only where the batch fills the chip (4,096 rows at H = 1024), a size the
+oracle checks on every row elsewhere; here the test switch
 (nmt_debug_gru_form) forces it at small, ragged sizes so that every row,
 every hidden unit and the tail of a 128-row block are checked against the
-oracle, with unit-gain weights so that the GRU carries signal.
+oracle, with unit-gain weights so that the GRUs carry signal.  The first GRU
+streams only where the embedding's padded width is a whole number of
+128-column chunks (E = 100, 128, 200 here; E = 64 keeps the staged form).
 
 Tolerances: log p within the stated 2e-2 of bf16 weights, intermediates
 within 2e-2 (bf16 rounding of operands of size about 1); the two forms add
-the same bf16 products in fp32 in different orders, so their new states agree
-to fp32 rounding of dot products of length K = 3H <= 1152 with terms of size
+the same bf16 products in fp32 in different orders, so their states agree to
+fp32 rounding of dot products of length K <= 3H = 1152 with terms of size
 about 1/sqrt(K): within 1e-5.
 """
 import numpy as np
@@ -29,10 +31,10 @@ TOL_FORMS = 1e-5
 BASE = Config("gru_forms", V=1000, V_src=500, E=64, H=128, A=128, B=300, S=4, len_lo=3, len_hi=20, Tpad=20,
               sigma_w=1.0, sigma_emb=1.0, seed=81, wtype="bf16")
 CASES = {
-    "h128_b300": dict(H=128, B=300),   # one unit block, two whole row blocks and a tail of 44
-    "h384_b129": dict(H=384, B=129),   # three unit blocks (packed tiles 0..5), a tail of one row
-    "h256_b1": dict(H=256, B=1),
-    "h256_b128": dict(H=256, B=128),   # exactly one row block
+    "h128_b300": dict(H=128, B=300, E=100),   # one unit block, two whole row blocks and a tail of 44
+    "h384_b129": dict(H=384, B=129, E=200),   # three unit blocks (packed tiles 0..5), a tail of one row
+    "h256_b1": dict(H=256, B=1, E=128),
+    "h256_b128": dict(H=256, B=128, E=64),    # exactly one row block; the first GRU stays staged
 }
 
 
@@ -67,13 +69,19 @@ def test_weight_streaming_gru_every_row(gpu, form, case):
     ctx = random_annotations(cfg, seed=82)
     g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
     args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    from paper_1605_04809_amd import binding as nb
     try:
         form(1)
+        n0 = nb.debug_gru_streamed()
         ws = g.step(*args)
+        n1 = nb.debug_gru_streamed()
         form(2)
         lds = g.step(*args)
+        n2 = nb.debug_gru_streamed()
     finally:
         form(0)
+    # both GRUs streamed under form 1 (the first only where E pads to whole chunks), neither under form 2
+    assert n1 - n0 == (1 if cfg.E == 64 else 2) and n2 == n1, (n0, n1, n2)
     ref = o.step(*args)
     for out in (ws, lds):
         assert np.all(np.isfinite(out["logp"]))
@@ -82,9 +90,10 @@ def test_weight_streaming_gru_every_row(gpu, form, case):
         assert errs["logp"] <= TOL_LOGP_BF16 and errs["logZ"] <= TOL_LOGP_BF16, errs
         for k in ("s1", "c", "s_new", "t", "alpha"):
             assert errs[k] <= TOL_INTER_BF16_SIGNAL, (k, errs)
-    # the first GRU and attention are the same kernels either way
-    assert np.array_equal(ws["s1"], lds["s1"]) and np.array_equal(ws["c"], lds["c"])
-    d = gpu.max_abs(ws["s_new"], lds["s_new"])
-    print(f"max |s_new(streamed) - s_new(staged)| = {d:.2e}", flush=True)
-    assert d <= TOL_FORMS
+    for k in ("s1", "s_new"):
+        d = gpu.max_abs(ws[k], lds[k])
+        print(f"max |{k}(streamed) - {k}(staged)| = {d:.2e}", flush=True)
+        assert d <= TOL_FORMS, k
+    if cfg.E == 64:  # the first GRU is the same kernel either way
+        assert np.array_equal(ws["s1"], lds["s1"])
     g.close()
