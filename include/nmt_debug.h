@@ -4,8 +4,8 @@
  * Lets a test make the library's device allocations fail, to check that
  * every call that allocates reports NMT_ENOMEM and releases what it had
  * allocated when an allocation fails part-way, and choose which of the two
- * bf16 GRU kernel forms a call takes, so that both are checked at sizes the
- * reference implementation finishes quickly.
+ * kernel forms the bf16 products of a step take, so that both are checked
+ * at sizes the reference implementation finishes quickly.
  */
 #ifndef NMT_DEBUG_H
 #define NMT_DEBUG_H
@@ -23,21 +23,23 @@ extern "C" {
  * the library's device allocations alive at the time of the call. */
 int64_t nmt_debug_alloc_hook(int32_t fail_after);
 
-/* The kernel form of the bf16 GRUs of Section 5.1's decoder step: 0 (the
- * default) streams the weights from L2 into registers where the operand
- * shape allows it (H a multiple of 128; for the first GRU, an embedding
- * width padded to a multiple of 128) and the batch gives every compute unit
- * a block; 1 streams wherever the shape allows it, whatever the batch, and
- * skips the split over K that small batches otherwise take; 2 always stages
- * both operands through LDS.  Both forms accumulate the same bf16 products
- * 16 at a time in increasing k, so where neither splits K they give the same
- * states.  Process-wide.  Returns the previous form, or -1 (and changes
- * nothing) for a form outside 0..2. */
-int32_t nmt_debug_gru_form(int32_t form);
+/* The kernel form of the bf16 products of Section 5.1's decoder step (the
+ * two GRUs, the attention query and the readout): 0 (the default) streams
+ * the weights from L2 into registers where the operand shapes allow it (H a
+ * multiple of 128; every A segment a whole number of 128-column chunks) and
+ * the batch gives every compute unit a block; 1 streams wherever the shapes
+ * allow it, whatever the batch, and skips the split over K that small
+ * batches otherwise take; 2 always stages both operands through LDS; 3 and 4
+ * are form 1 with the query's and readout's split of each chunk's k steps
+ * between two wave groups forced off (3) or on (4).  Where neither form
+ * splits K both accumulate the same bf16 products 16 at a time in
+ * increasing k and give the same values.  Process-wide.  Returns the
+ * previous form, or -1 (and changes nothing) for a form outside 0..4. */
+int32_t nmt_debug_gemm_form(int32_t form);
 
-/* How many GRU launches of the process took the weight-streaming form, so a
- * test can tell which form ran. */
-int64_t nmt_debug_gru_streamed(void);
+/* How many launches of the process took a weight-streaming form (GRU or
+ * plain product), so a test can tell which form ran. */
+int64_t nmt_debug_gemm_streamed(void);
 
 #ifdef __cplusplus
 }

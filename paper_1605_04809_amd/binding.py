@@ -37,7 +37,7 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
            "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
            "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy",
-           "nmt_debug_alloc_hook", "nmt_debug_gru_form", "nmt_debug_gru_streamed")
+           "nmt_debug_alloc_hook", "nmt_debug_gemm_form", "nmt_debug_gemm_streamed")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -116,10 +116,10 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_rescorer_destroy.restype = None
     lib.nmt_debug_alloc_hook.argtypes = [_I32]
     lib.nmt_debug_alloc_hook.restype = ctypes.c_int64
-    lib.nmt_debug_gru_form.argtypes = [_I32]
-    lib.nmt_debug_gru_form.restype = _I32
-    lib.nmt_debug_gru_streamed.argtypes = []
-    lib.nmt_debug_gru_streamed.restype = ctypes.c_int64
+    lib.nmt_debug_gemm_form.argtypes = [_I32]
+    lib.nmt_debug_gemm_form.restype = _I32
+    lib.nmt_debug_gemm_streamed.argtypes = []
+    lib.nmt_debug_gemm_streamed.restype = ctypes.c_int64
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
@@ -139,15 +139,17 @@ def debug_alloc_hook(fail_after: int) -> int:
     return int(load_library().nmt_debug_alloc_hook(fail_after))
 
 
-def debug_gru_form(form: int) -> int:
-    """Test hook (nmt_debug.h): 0 automatic, 1 weight-streaming bf16 GRU
-    wherever its shape applies, 2 LDS-staged only; returns the previous."""
-    return int(load_library().nmt_debug_gru_form(form))
+def debug_gemm_form(form: int) -> int:
+    """Test hook (nmt_debug.h): kernel form of the bf16 products: 0
+    automatic, 1 weight-streaming wherever the shapes allow, 2 LDS-staged
+    only, 3 / 4 as 1 with the plain products' in-block K split off / on;
+    returns the previous form."""
+    return int(load_library().nmt_debug_gemm_form(form))
 
 
-def debug_gru_streamed() -> int:
-    """Test hook (nmt_debug.h): GRU launches so far that streamed weights."""
-    return int(load_library().nmt_debug_gru_streamed())
+def debug_gemm_streamed() -> int:
+    """Test hook (nmt_debug.h): launches so far that streamed weights."""
+    return int(load_library().nmt_debug_gemm_streamed())
 
 
 def last_error() -> str:

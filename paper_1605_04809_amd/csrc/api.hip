@@ -476,12 +476,12 @@ int64_t nmt_debug_alloc_hook(int32_t fail_after) {
   return g_live_allocs.load();
 }
 
-int32_t nmt_debug_gru_form(int32_t form) {
-  if (form < 0 || form > 2) return -1;
-  return nmt::g_gru_form.exchange(form);
+int32_t nmt_debug_gemm_form(int32_t form) {
+  if (form < 0 || form > 4) return -1;
+  return nmt::g_gemm_form.exchange(form);
 }
 
-int64_t nmt_debug_gru_streamed(void) { return nmt::g_gru_streamed.load(); }
+int64_t nmt_debug_gemm_streamed(void) { return nmt::g_gemm_streamed.load(); }
 
 const char* nmt_last_error(void) { return g_err.c_str(); }
 
@@ -793,9 +793,9 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   g1.ep.out16 = s1h;
   float* gpart = (float*)(ws + L.gpart);
   auto run_gru = [&](const GruProblem& g, int ks) {
-    // (the test switch's form 1 skips the K split, which the streamed form
-    // never takes, so that small batches reach the streamed form)
-    return ks > 1 && g_gru_form.load(std::memory_order_relaxed) != 1
+    // (the test switch's forced streaming skips the K split, which the
+    // streamed form never takes, so that small batches reach it)
+    return ks > 1 && !gemm_stream_forced(g_gemm_form.load(std::memory_order_relaxed))
                ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, st)
                   : launch_gemm_gru(&g, 1, H, m->bf16, m->cus, st);
   };
@@ -804,7 +804,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // attention query q = s1 att_Wq
   if (e == hipSuccess) {
     PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1, L.ks_q, (float*)(ws + L.kpart)};
-    e = launch_gemm_plain(Tile::Small, make_a(B, {state_seg(s1, s1h, 0)}), m->att_Wq, ep, st);
+    e = launch_gemm_plain(Tile::Small, make_a(B, {state_seg(s1, s1h, 0)}), m->att_Wq, ep, st, m->cus);
   }
   mark(NMT_PHASE_QUERY + 1);
   // masked attention and context
@@ -834,7 +834,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     }
     e = launch_gemm_plain(Tile::Small,
                           make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}), m->ro,
-                          ep, st);
+                          ep, st, m->cus);
   }
   mark(NMT_PHASE_READOUT + 1);
   // vocabulary projection with an online log-sum-exp per slice, then the combine

@@ -48,11 +48,13 @@ inline int gru_hb(bool bf16) { return bf16 ? kGruHB16 : kGruHB; }
 #define NMT_GRU_SMALL_TM 64
 #endif
 constexpr int kGruSmallTM = NMT_GRU_SMALL_TM;
-// Which GRU kernel form bf16 problems take: 0 the weight-streaming one where
-// it applies and fills the chip, 1 wherever it applies, 2 never (a test
-// switch, set through nmt_debug_gru_form).
-extern std::atomic<int> g_gru_form;
-extern std::atomic<int64_t> g_gru_streamed;  // launches of the weight-streaming form
+// Which kernel form the bf16 GRU and small-tile plain products take: 0 the
+// weight-streaming one where it applies and fills the chip, 1 wherever it
+// applies, 2 never, 3 and 4 as 1 with the plain products' in-block K split
+// off or on (a test switch, set through nmt_debug_gemm_form).
+extern std::atomic<int> g_gemm_form;
+inline bool gemm_stream_forced(int form) { return form == 1 || form == 3 || form == 4; }
+extern std::atomic<int64_t> g_gemm_streamed;  // launches of the weight-streaming form
 constexpr int kVocabTN = 32;                    // packing granularity of the output weights
 constexpr int kVocabSpare = 32;                 // zero columns past the last block (group loads stay inside)
 
@@ -119,7 +121,9 @@ struct GruProblem {
 };
 
 // Launchers (all asynchronous on `st`).
-hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st);
+// cus > 0 lets a small-tile bf16 product take the weight-streaming form.
+hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st,
+                             int cus = 0);
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, int cus, hipStream_t st);
 // K splits for a GRU launch of M rows whose A operand has `nchunks` K chunks:
 // 1 when the launch fills the chip as it is, else enough splits of the

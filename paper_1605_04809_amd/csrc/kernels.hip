@@ -170,9 +170,13 @@ static bool segments_loadable(const AOperand& A, int64_t Npad, bool bf16) {
   return chunks * (bf16 ? PrecBF16::KQ : PrecF32::KQ) * Npad * 16 < ((int64_t)1 << 31);
 }
 
-hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st) {
+static bool try_plain_ws(const AOperand& A, const Packed& W, const PlainEpi& ep, int cus, hipStream_t st);
+
+hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi& ep, hipStream_t st,
+                             int cus) {
   if (A.M <= 0 || ep.N <= 0) return hipSuccess;
   if (!segments_loadable(A, W.Npad, W.bf16)) return hipErrorInvalidValue;
+  if (t == Tile::Small && try_plain_ws(A, W, ep, cus, st)) return hipGetLastError();
   return W.bf16 ? gemm_plain<PrecBF16>(t, A, W, ep, st) : gemm_plain<PrecF32>(t, A, W, ep, st);
 }
 
@@ -689,15 +693,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
 }
 
-std::atomic<int> g_gru_form{0};
-std::atomic<int64_t> g_gru_streamed{0};
+std::atomic<int> g_gemm_form{0};
+std::atomic<int64_t> g_gemm_streamed{0};
 
 static bool aligned(const void* p, int bytes) { return ((uintptr_t)p % bytes) == 0; }
 
 // The weight-streaming form for one bf16 problem, if it applies (see above);
 // returns false to let the caller launch the LDS-staged tile instead.
 static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream_t st) {
-  const int form = g_gru_form.load(std::memory_order_relaxed);
+  const int form = g_gemm_form.load(std::memory_order_relaxed);
   if (form == 2) return false;
   // H a multiple of the block's 128 units: every wave's packed columns then
   // lie inside the matrix's rows, so no weight load leaves the matrix
@@ -720,7 +724,229 @@ static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream
     hipLaunchKernelGGL((k_gru_ws<false, true, false, NMT_WS_VPF_F32_SRC>), grid, block, 0, st, p);
   else
     return false;
-  g_gru_streamed.fetch_add(1, std::memory_order_relaxed);
+  g_gemm_streamed.fetch_add(1, std::memory_order_relaxed);
+  return true;
+}
+
+// ---------------------------------- weight-streaming plain GEMM (bf16 weights)
+//
+// The bf16 query and readout products in the form of k_gru_ws: activations
+// staged through registers into LDS in 128-k chunks, packed weights streamed
+// from L2 straight into registers.  A wave computes 64 rows x 32 columns
+// (each weight fragment feeds two MFMAs); a block of 8 waves covers 128 rows
+// and 128 columns (KSPLIT = 1), or 64 columns with the 8 k steps of each
+// chunk shared between two groups of four waves (KSPLIT = 2, where 128-column
+// blocks would leave CUs idle: the readout's 512 columns), whose sums meet in
+// LDS before the epilogue.  Segment 0 of A may be fp32 (rounded to bf16 as it
+// is staged); the others are bf16.  The output layout matches the GRU form:
+// register r of row fragment i is column 8 (r / 4) + 4 h + r % 4 of the
+// wave's 32 for batch row 32 i + l32, so a lane stores 4 consecutive columns.
+constexpr int kPwTM = 128, kPwKQ = 16, kPwVPF = 4;
+
+template <int NSEG, bool SRC16_0, int KSPLIT>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k_plain_ws(AOperand A, const void* Wp,
+                                                                                         int64_t Npad, PlainEpi ep) {
+  using P = PrecBF16;
+  constexpr int TM = kPwTM, KQW = kPwKQ, NKS = KQW / 2, VPF = kPwVPF, NT = 512;
+  constexpr int NA = TM * KQW / NT;  // activation vectors per thread per chunk
+  constexpr int NKL = NKS / KSPLIT;  // k steps per chunk and wave
+  constexpr int CW = 4 / KSPLIT;     // 32-column fragments per block
+  static_assert(NKL % VPF == 0 && NA == 4, "ring slots fixed within a chunk");
+  static_assert(NT / KQW == 32 && KQW == 16, "staging rows 32 apart");
+  __shared__ f32x4 As[2 * KQW * TM];  // [stage][vector][row ^ (vector & 15)]
+  const int M = A.M;
+  const int m0 = blockIdx.x * TM;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int wr = wave & 1, wc = (wave >> 1) % CW, kg = wave / (2 * CW);
+  const int n0 = (blockIdx.y * CW + wc) * 32;  // the wave's first column
+  const int nch = total_chunks(A) / 2;         // 128-k chunks
+  const int last_gk = nch * NKS - 1;
+  const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(Wp, (int64_t)nch * KQW * Npad * 16);
+  const int lo = (int)(((int64_t)h * Npad + n0 + l32) * 16);
+  const int kbytes = (int)(2 * Npad * 16);  // one k step: two packed vector rows
+  // k step j of this wave's share of chunk c
+  auto wload = [&](f32x4& d, int c, int j) {
+    const int gk = c * NKS + kg * NKL + j;
+    d = buf_load(wres, lo, (gk < last_gk ? gk : last_gk) * kbytes);  // past the end: re-read the last step (unused)
+  };
+
+  // activation staging: this thread's vectors are rows tid / KQW + 32 i,
+  // vector tid % KQW of each chunk
+  const ASeg sg0 = seg_at(A, 0), sg1 = seg_at(A, NSEG > 1 ? 1 : 0), sg2 = seg_at(A, NSEG > 2 ? 2 : 0);
+  const int c1 = sg0.nchunk / 2, c2 = c1 + (NSEG > 1 ? sg1.nchunk / 2 : 0);
+  const __amdgpu_buffer_rsrc_t res0 = buffer_rsrc(sg0.p, seg_bytes(sg0, M));
+  const __amdgpu_buffer_rsrc_t res1 = buffer_rsrc(sg1.p, seg_bytes(sg1, M));
+  const __amdgpu_buffer_rsrc_t res2 = buffer_rsrc(sg2.p, seg_bytes(sg2, M));
+  const int kin = P::KV * ((int)threadIdx.x % KQW);
+  int roff0[NA], roff1[NA], roff2[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = m0 + ((int)threadIdx.x + i * NT) / KQW;
+    roff0[i] = seg_row_off(sg0, row, M);
+    roff1[i] = NSEG > 1 ? seg_row_off(sg1, row, M) : kNoLoad;
+    roff2[i] = NSEG > 2 ? seg_row_off(sg2, row, M) : kNoLoad;
+  }
+  f32x4 ra[NA], rb[NA];  // rb: the second half of an fp32 source vector
+  // The bf16 segments from chunk c on, by selects (a branch between segments
+  // of one type gets merged by the compiler into a dynamically indexed copy of
+  // the segments in scratch memory).
+  auto aload16 = [&](int c, bool with0) {
+    if constexpr (NSEG == 1) {  // one segment: nothing to select
+      const int kseg = c * KQW * P::KV;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) load_a_raw<P, true>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 2, ra[i], rb[i]);
+      return;
+    }
+    const int si = (with0 && c < c1) ? 0 : (c < c2 || NSEG == 2 ? 1 : 2);
+    const __amdgpu_buffer_rsrc_t res = si == 0 ? res0 : (si == 1 ? res1 : res2);
+    const int kseg = (c - (si == 0 ? 0 : (si == 1 ? c1 : c2))) * KQW * P::KV;
+    const int K = si == 0 ? sg0.K : (si == 1 ? sg1.K : sg2.K);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int ro = si == 0 ? roff0[i] : (si == 1 ? roff1[i] : roff2[i]);
+      load_a_raw<P, true>(res, ro, K, kseg + kin, kin, kseg * 2, ra[i], rb[i]);
+    }
+  };
+  auto aload = [&](int c) {  // chunk c of the whole A
+    if constexpr (SRC16_0) {
+      aload16(c, true);
+    } else if (c < c1) {  // a uniform branch to the fp32 segment's loads
+      const int kseg = c * KQW * P::KV;
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        load_a_raw<P, false>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 4, ra[i], rb[i]);
+    } else {
+      aload16(c, false);
+    }
+  };
+  const int st_base = ((int)threadIdx.x % KQW) * TM + (((int)threadIdx.x / KQW) ^ ((int)threadIdx.x % KQW));
+  auto astore = [&](int stage, int c) {  // c: the chunk the staged data belongs to
+    const bool s16 = SRC16_0 || c >= c1;
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      As[stage * KQW * TM + st_base + 32 * i] = s16 ? ra[i] : a_from_raw<P, false>(ra[i], rb[i]);
+  };
+  // fragment of k step ks (vectors 2 ks + h) for the 32 rows at r0 (a multiple of 32)
+  auto afrag = [&](int stage, int ks, int r0) {
+    const int v = 2 * ks + h;
+    return As[stage * KQW * TM + r0 + v * TM + (l32 ^ v)];
+  };
+
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
+  f32x4 ring[VPF];
+#pragma unroll
+  for (int p = 0; p < VPF; ++p) wload(ring[p], 0, p);
+  aload(0);
+  astore(0, 0);
+  if (nch > 1) aload(1);
+  __syncthreads();
+
+  const int r0 = 64 * wr, ks0 = kg * NKL;
+  for (int c = 0; c < nch; ++c) {
+    const int st = c & 1;
+    f32x4 a0 = afrag(st, ks0, r0), a1 = afrag(st, ks0, r0 + 32);
+    static_for<NKL>([&](auto jc) {
+      constexpr int j = decltype(jc)::value, slot = j % VPF;
+      f32x4 n0 = a0, n1 = a1;
+      if constexpr (j + 1 < NKL) {
+        n0 = afrag(st, ks0 + j + 1, r0);
+        n1 = afrag(st, ks0 + j + 1, r0 + 32);
+      }
+      P::mma(ring[slot], a0, acc[0]);
+      P::mma(ring[slot], a1, acc[1]);
+      wload(ring[slot], c + (j + VPF) / NKL, (j + VPF) % NKL);  // refill the slot, VPF steps ahead
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      a0 = n0;
+      a1 = n1;
+    });
+    if (c + 1 < nch) astore(st ^ 1, c + 1);
+    if (c + 2 < nch) aload(c + 2);
+    __syncthreads();
+  }
+
+  if constexpr (KSPLIT == 2) {  // the second group's sums to LDS, the first adds them
+    float* red = (float*)As;
+    if (kg == 1) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[(((wave - 4) * 2 + i) * 16 + r) * 64 + lane] = acc[i][r];
+    }
+    __syncthreads();
+    if (kg == 1) return;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][r] += red[((wave * 2 + i) * 16 + r) * 64 + lane];
+  }
+
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = m0 + r0 + 32 * i + l32;
+    if (row >= M) continue;
+    const bool masked = ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j0 = n0 + 8 * q + 4 * h;
+      if (j0 >= ep.N) continue;
+      const f32x4 b = ep.bias ? *(const f32x4*)(ep.bias + j0) : zero4();
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float v = acc[i][4 * q + e] + b[e];
+        if (ep.act == 1) v = tanhf_(v);
+        o[e] = masked ? 0.f : v;
+      }
+      if (ep.out16) {
+        typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+        *(bf16x4_t*)(ep.out16 + (int64_t)row * ep.ldo + j0) = bf16x4_t{(__bf16)o[0], (__bf16)o[1], (__bf16)o[2],
+                                                                         (__bf16)o[3]};
+      } else {
+        *(f32x4*)(ep.out + (int64_t)row * ep.ldo + j0) = o;
+      }
+    }
+  }
+}
+
+// The weight-streaming form of a bf16 plain GEMM, if it applies (see above);
+// returns false to let the caller launch the LDS-staged tile instead.
+static bool try_plain_ws(const AOperand& A, const Packed& W, const PlainEpi& ep, int cus, hipStream_t st) {
+  const int form = g_gemm_form.load(std::memory_order_relaxed);
+  if (form == 2 || !W.bf16 || cus <= 0 || A.M <= 0 || A.nseg < 1 || A.nseg > 3 || ep.N % 4) return false;
+  for (int i = 0; i < A.nseg; ++i)
+    if (A.seg[i].nchunk % 2 || (i > 0 && !A.seg[i].bf16)) return false;
+  // the epilogue's vector accesses: 16-byte aligned fp32 rows and bias,
+  // 8-byte aligned bf16 rows
+  if (ep.ldo % 4 || (ep.bias && !aligned(ep.bias, 16)) || (ep.out16 ? !aligned(ep.out16, 8) : !aligned(ep.out, 16)))
+    return false;
+  // the split over K of the staged tile (small batches) stays with it
+  if (form == 0 && ep.ksplit > 1) return false;
+  const int nbx = ceil_div(A.M, kPwTM);
+  int ksplit = (int64_t)nbx * ceil_div(ep.N, 128) < cus ? 2 : 1;
+  if (form == 3 || form == 4) ksplit = form - 2;
+  if (form == 0 && ksplit == 2 && (int64_t)nbx * ceil_div(ep.N, 64) < cus) return false;
+  const int bn = 128 / ksplit;
+  if ((int64_t)ceil_div(ep.N, bn) * bn > W.Npad) return false;  // every wave's columns inside the packed matrix
+  const dim3 grid(nbx, ceil_div(ep.N, bn)), block(512);
+  const bool f32_0 = !A.seg[0].bf16;
+  if (A.nseg == 1 && !f32_0) {
+    if (ksplit == 1)
+      hipLaunchKernelGGL((k_plain_ws<1, true, 1>), grid, block, 0, st, A, W.d, W.Npad, ep);
+    else
+      hipLaunchKernelGGL((k_plain_ws<1, true, 2>), grid, block, 0, st, A, W.d, W.Npad, ep);
+  } else if (A.nseg == 3 && f32_0) {
+    if (ksplit == 1)
+      hipLaunchKernelGGL((k_plain_ws<3, false, 1>), grid, block, 0, st, A, W.d, W.Npad, ep);
+    else
+      hipLaunchKernelGGL((k_plain_ws<3, false, 2>), grid, block, 0, st, A, W.d, W.Npad, ep);
+  } else {
+    return false;
+  }
+  g_gemm_streamed.fetch_add(1, std::memory_order_relaxed);
   return true;
 }
 

@@ -87,15 +87,16 @@ def test_noalloc_scratch_size_and_host_errors():
     assert "NULL" in nb.last_error()
 
 
-def test_gru_form_switch_needs_no_device():
-    """The test switch between the bf16 GRU kernel forms (nmt_debug.h)
-    returns the previous form and refuses forms outside 0..2."""
-    prev = nb.debug_gru_form(0)
+def test_gemm_form_switch_needs_no_device():
+    """The test switch between the bf16 products' kernel forms (nmt_debug.h)
+    returns the previous form and refuses forms outside 0..4."""
+    prev = nb.debug_gemm_form(0)
     try:
-        assert nb.debug_gru_form(3) == -1
-        assert nb.debug_gru_form(-1) == -1
-        assert nb.debug_gru_form(2) == 0
-        assert nb.debug_gru_form(1) == 2
-        assert nb.debug_gru_form(0) == 1
+        assert nb.debug_gemm_form(5) == -1
+        assert nb.debug_gemm_form(-1) == -1
+        assert nb.debug_gemm_form(2) == 0
+        assert nb.debug_gemm_form(4) == 2
+        assert nb.debug_gemm_form(1) == 4
+        assert nb.debug_gemm_form(0) == 1
     finally:
-        nb.debug_gru_form(prev)
+        nb.debug_gemm_form(prev)

@@ -1,0 +1,108 @@
+"""GPU parity of the two kernel forms of the bf16 products of the decoder
+step (Section 5.1): the two GRUs ([x | s_prev] and [s1 | c]), the attention
+query (s1 W_q) and the readout ([s_new | x | c]).
+
+With bf16 weights these products can run in a form that streams the packed
+weights from L2 straight into registers instead of staging both operands
+through LDS.  The library takes it only where the batch fills the chip (4,096
+rows at H = A = 1024), a size the oracle checks on every row elsewhere; here
+the test switch (nmt_debug_gemm_form) forces it at small, ragged sizes so
+that every row, every output column and the tail of a 128-row block are
+checked against the oracle, with unit-gain weights so that every product
+carries signal.  Forms 3 and 4 force the query's and readout's split of each
+chunk's k steps between two wave groups off and on, so both shapes of that
+kernel run.  The first GRU and the readout stream only where the embedding's
+padded width is a whole number of 128-column chunks (E = 100, 128, 200 here;
+E = 64 keeps them staged).
+
+Tolerances: log p within the stated 2e-2 of bf16 weights, intermediates
+within 2e-2 (bf16 rounding of operands of size about 1), for every form.
+The forms add the same bf16 products in fp32 in different orders, so the
+values computed before any bf16-stored intermediate (s1, alpha) agree to
+fp32 rounding of dot products of length K <= 3H = 1152 with terms of size
+about 1/sqrt(K): within 1e-5; so does s_new where the context rounded to the
+same bf16 values.
+"""
+import numpy as np
+import pytest
+
+from paper_1605_04809_amd.workloads import Config, random_annotations, unit_gain
+
+pytestmark = pytest.mark.gpu
+
+TOL_LOGP_BF16 = 2e-2
+TOL_INTER_BF16_SIGNAL = 2e-2
+TOL_FORMS = 1e-5
+
+BASE = Config("stream_forms", V=1000, V_src=500, E=64, H=128, A=128, B=300, S=4, len_lo=3, len_hi=20, Tpad=20,
+              sigma_w=1.0, sigma_emb=1.0, seed=81, wtype="bf16")
+CASES = {
+    "h128_b300": dict(H=128, B=300, E=100),   # one unit block, two whole row blocks and a tail of 44
+    "h384_b129": dict(H=384, B=129, E=200),   # three unit blocks (packed tiles 0..5), a tail of one row
+    "h256_b1": dict(H=256, B=1, E=128),
+    "h256_b128": dict(H=256, B=128, E=64),    # exactly one row block; the first GRU and the readout stay staged
+    "a1024_b700": dict(H=128, A=1024, B=700, E=100),   # query of 1024 columns: eight column blocks
+}
+
+
+def _torch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    _torch()
+    from tests import gpu_cases
+    return gpu_cases
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_weight_streaming_forms_every_row(gpu, case):
+    from paper_1605_04809_amd import binding as nb
+    cfg = BASE.replace(name=case, **CASES[case])
+    print(f"stream forms {case}: H={cfg.H} A={cfg.A} E={cfg.E} B={cfg.B}", flush=True)
+    wl = unit_gain(cfg)
+    wl.y_prev[::7] = -1
+    ctx = random_annotations(cfg, seed=82)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    # streamed launches per step: both GRUs, the query and the readout, less
+    # the first GRU and the readout where E does not pad to whole chunks
+    n_stream = 4 if cfg.E != 64 else 2
+    prev = nb.debug_gemm_form(0)
+    out, counts = {}, {}
+    try:
+        for form in (3, 4, 2):
+            nb.debug_gemm_form(form)
+            n0 = nb.debug_gemm_streamed()
+            out[form] = g.step(*args)
+            counts[form] = nb.debug_gemm_streamed() - n0
+    finally:
+        nb.debug_gemm_form(prev)
+    assert counts == {3: n_stream, 4: n_stream, 2: 0}, counts
+    ref = o.step(*args)
+    for form, res in out.items():
+        assert np.all(np.isfinite(res["logp"]))
+        errs = {k: gpu.max_abs(res[k], ref[k]) for k in ("logp", "logZ", "s1", "c", "s_new", "t", "alpha")}
+        print(f"form {form} max |gpu - oracle|:", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+        assert errs["logp"] <= TOL_LOGP_BF16 and errs["logZ"] <= TOL_LOGP_BF16, errs
+        for k in ("s1", "c", "s_new", "t", "alpha"):
+            assert errs[k] <= TOL_INTER_BF16_SIGNAL, (k, errs)
+    for form in (3, 4):
+        # s1 and alpha come before anything the forms could round to bf16
+        # differently, so they agree to fp32 rounding
+        for k in ("s1", "alpha"):
+            d = gpu.max_abs(out[form][k], out[2][k])
+            print(f"max |{k}(form {form}) - {k}(staged)| = {d:.2e}", flush=True)
+            assert d <= TOL_FORMS, (form, k)
+        # the context is stored in bf16: where the forms' queries round it to
+        # the same values, the new states agree to fp32 rounding too (a
+        # context value one bf16 step apart moves them by about 1e-4)
+        if np.array_equal(out[form]["c"], out[2]["c"]):
+            d = gpu.max_abs(out[form]["s_new"], out[2]["s_new"])
+            print(f"max |s_new(form {form}) - s_new(staged)| = {d:.2e}", flush=True)
+            assert d <= TOL_FORMS, (form, "s_new")
+    g.close()
