@@ -737,7 +737,7 @@ namespace {
 nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const float* pool, int32_t pool_rows,
                       const int32_t* state_row, const int32_t* d_y_prev, const int32_t* d_sent_id, Requests rq,
                       float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace, size_t ws_bytes, hipStream_t st,
-                      float* d_alpha, float* d_c, float* d_s1, float* d_t) {
+                      float* d_alpha, float* d_c, float* d_s1, float* d_t, const AttnGroups* pre_grp = nullptr) {
   const WsLayout L = ws_layout(m, B);
   if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < L.total) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
@@ -809,9 +809,11 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   mark(NMT_PHASE_QUERY + 1);
   // masked attention and context
   if (e == hipSuccess) {
-    const AttnGroups grp{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
+    // (a forest's levels come with their grouping done, all in one launch)
+    const AttnGroups grp =
+        pre_grp ? *pre_grp : AttnGroups{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
     e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
-                         src->S, m->att_v, c, d_alpha, grp, c16, m->cus, st);
+                         src->S, m->att_v, c, d_alpha, grp, c16, m->cus, st, pre_grp != nullptr);
   }
   mark(NMT_PHASE_ATTENTION + 1);
   // second GRU: s_new = GRU(c, s1)
@@ -1096,11 +1098,25 @@ nmt_status forest_fail(nmt_status st, const char* msg) { return fail(st, "%s", m
 nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t B, const float* pool,
                                    int32_t pool_rows, const int32_t* state_row, const int32_t* y_prev,
                                    const int32_t* sent_id, const int32_t* req_off, const int32_t* req, int32_t nreq,
-                                   float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st) {
+                                   float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st,
+                                   const AttnGroups* grp) {
   if (B == 0) return ok();
   Requests rq{req_off, req, nreq, state_row, pool_rows};
   return score_step(m, src, B, pool, pool_rows, state_row, y_prev, sent_id, rq, logp, s_new, nullptr, ws, ws_bytes, st,
-                    nullptr, nullptr, nullptr, nullptr);
+                    nullptr, nullptr, nullptr, nullptr, grp);
+}
+
+// The attention grouping of several batches over one source in one launch
+// (the levels of a forest): sets each level's rows per tile; false where the
+// attention would not use a grouping (too many sentences), so the levels
+// take the per-row kernel as single steps do.
+bool nmt_internal_group_levels(const nmt_model* m, const nmt_source* src, GroupLevel* lv, int n, hipStream_t st,
+                               hipError_t* err) {
+  *err = hipSuccess;
+  if (src->S > kGroupMaxS || src->Tpad > kMaxTpad) return false;
+  for (int i = 0; i < n; ++i) lv[i].G = attn_rows_per_tile(lv[i].B, m->cus);
+  *err = launch_group_levels(lv, n, src->S, src->len, src->Tpad, st);
+  return *err == hipSuccess;
 }
 
 int32_t nmt_internal_hidden(const nmt_model* m) { return m->dims.H; }

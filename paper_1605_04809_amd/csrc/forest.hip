@@ -30,7 +30,7 @@ __global__ void k_path_sum(int n_pairs, int depth, const int32_t* __restrict__ p
 }
 
 struct ForestWs {
-  size_t idx, logp, states, step, total;
+  size_t idx, logp, states, perm, tiles, ntiles, step, total;
   size_t n_idx;
 };
 
@@ -42,7 +42,10 @@ size_t al256(size_t x) { return (x + 255) / 256 * 256; }
 nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t B, const float* pool,
                                    int32_t pool_rows, const int32_t* state_row, const int32_t* y_prev,
                                    const int32_t* sent_id, const int32_t* req_off, const int32_t* req, int32_t nreq,
-                                   float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st);
+                                   float* logp, float* s_new, void* ws, size_t ws_bytes, hipStream_t st,
+                                   const AttnGroups* grp);
+bool nmt_internal_group_levels(const nmt_model* m, const nmt_source* src, GroupLevel* lv, int n, hipStream_t st,
+                               hipError_t* err);
 int32_t nmt_internal_hidden(const nmt_model* m);
 int32_t nmt_internal_vocab(const nmt_model* m);
 int nmt_internal_device(const nmt_model* m);
@@ -58,6 +61,13 @@ static ForestWs forest_ws(const nmt_model* m, const nmt_forest* f) {
   off += al256((size_t)f->n_req * 4);
   L.states = off;
   off += al256((size_t)f->n_rows * nmt_internal_hidden(m) * 4);
+  // every level's grouping of rows by sentence (at most one tile per row)
+  L.perm = off;
+  off += al256((size_t)f->n_rows * 4);
+  L.tiles = off;
+  off += al256((size_t)f->n_rows * 16);
+  L.ntiles = off;
+  off += al256((size_t)f->depth * 4);
   L.step = off;
   off += al256(nmt_score_workspace_bytes(m, f->max_rows));
   L.total = off;
@@ -99,13 +109,24 @@ nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_fores
   int32_t* d_path = d_req + f->n_req;
   hipError_t e = hipMemcpyAsync(idx, f->upload.data(), f->upload.size() * 4, hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
+  // the attention's grouping of rows by sentence, for all levels at once
+  std::vector<GroupLevel> lv((size_t)f->depth);
+  for (int d = 1; d <= f->depth; ++d) {
+    const int32_t r0 = f->row_base[d - 1];
+    lv[d - 1] = GroupLevel{f->rows_lv[d - 1], 0, d_sent + r0,
+                           AttnGroups{(int32_t*)(ws + L.perm) + r0, (int4*)(ws + L.tiles) + r0,
+                                      (int32_t*)(ws + L.ntiles) + (d - 1)}};
+  }
+  const bool grouped = nmt_internal_group_levels(m, src, lv.data(), f->depth, st, &e);
+  if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
   for (int d = 1; d <= f->depth; ++d) {
     const int32_t r0 = f->row_base[d - 1], q0 = f->req_base[d - 1];
     const float* pool = d == 1 ? d_hyp_states : states;
     const int32_t pool_rows = d == 1 ? f->n_hyp : f->n_rows;
     nmt_status rc = nmt_internal_score_step(m, src, f->rows_lv[d - 1], pool, pool_rows, d_state_row + r0, d_y + r0,
                                             d_sent + r0, d_off + f->off_base[d - 1], d_req + q0, f->req_lv[d - 1],
-                                            logp + q0, states + (int64_t)r0 * H, ws + L.step, ws_bytes - L.step, st);
+                                            logp + q0, states + (int64_t)r0 * H, ws + L.step, ws_bytes - L.step, st,
+                                            grouped ? &lv[d - 1].grp : nullptr);
     if (rc != NMT_OK) return rc;
   }
   hipLaunchKernelGGL(k_path_sum, dim3(ceil_div(f->n_pairs, 256)), dim3(256), 0, st, f->n_pairs, f->depth, d_path,

@@ -191,10 +191,24 @@ struct AttnGroups {
 // sentences whose keys are too large for them (launch_key_factors); pctx the
 // keys themselves, which tiles with such keys and large queries score from.
 // c_bf16: the context c [B x C] is written in bf16 (nearest even) instead of fp32.
+// grouped: grp already holds this batch's grouping (launch_group_levels, with
+// G = attn_rows_per_tile(B, cus)), so no grouping kernel runs.
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
-                            int cus, hipStream_t st);
+                            int cus, hipStream_t st, bool grouped = false);
+// Rows per attention tile for a batch of B rows: kAttnGroup, halved while the
+// tiles would leave more than half the CUs idle.
+int attn_rows_per_tile(int B, int cus);
+// The grouping of several batches (the levels of a forest) in one launch,
+// one block per batch: rows B of sentences sent_id, tiles of G rows.
+struct GroupLevel {
+  int32_t B, G;
+  const int32_t* sent_id;
+  AttnGroups grp;
+};
+constexpr int kMaxGroupLevels = 16;  // batches per launch
+hipError_t launch_group_levels(const GroupLevel* lv, int n, int S, const int32_t* len, int Tpad, hipStream_t st);
 hipError_t launch_bf16_to_f32(const void* x, int64_t rows, int cols, int64_t ld, float* y, hipStream_t st);
 // Per sentence of the keys pctx [S x Tpad x A] (A a multiple of 4):
 // kfac = 2^{2 log2(e) pctx}, exponent clamped to [-126, 126], and big[s] = 1

@@ -1698,15 +1698,23 @@ __device__ __forceinline__ int2 block_scan2(int& a, int& b, int (*wsum)[16]) {
   return tot;
 }
 
-__global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const int32_t* __restrict__ sent_id,
-                                                     const int32_t* __restrict__ len, int Tpad,
-                                                     int32_t* __restrict__ perm, int4* __restrict__ tiles,
-                                                     int32_t* __restrict__ n_tiles) {
-  __shared__ int cnt[kGroupMaxS + 1];    // rows per bucket, then the bucket's write cursor
-  __shared__ int order[kGroupMaxS + 1];  // buckets longest sentence first, the invalid bucket last
-  __shared__ int keyv[kGroupMaxS + 1];   // sort key of each bucket
-  __shared__ int keyc[kMaxTpad + 2];     // buckets per key, then the key's write cursor
-  __shared__ int wsum[2][16];
+struct GroupScratch {
+  int cnt[kGroupMaxS + 1];    // rows per bucket, then the bucket's write cursor
+  int order[kGroupMaxS + 1];  // buckets longest sentence first, the invalid bucket last
+  int keyv[kGroupMaxS + 1];   // sort key of each bucket
+  int keyc[kMaxTpad + 2];     // buckets per key, then the key's write cursor
+  int wsum[2][16];
+};
+
+// The grouping of one batch by the 1024 threads of a block.
+__device__ void group_rows_block(int B, int S, int G, const int32_t* __restrict__ sent_id,
+                                 const int32_t* __restrict__ len, int Tpad, int32_t* __restrict__ perm,
+                                 int4* __restrict__ tiles, int32_t* __restrict__ n_tiles, GroupScratch& sh) {
+  int* cnt = sh.cnt;
+  int* order = sh.order;
+  int* keyv = sh.keyv;
+  int* keyc = sh.keyc;
+  auto& wsum = sh.wsum;
   const int tid = threadIdx.x, NB = S + 1, NK = Tpad + 1;
   for (int i = tid; i < NB; i += 1024) cnt[i] = 0;
   for (int k = tid; k < NK; k += 1024) keyc[k] = 0;
@@ -1758,6 +1766,45 @@ __global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const 
     const int s = sent_id[b];
     perm[atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1)] = b;
   }
+}
+
+__global__ __launch_bounds__(1024) void k_group_rows(int B, int S, int G, const int32_t* __restrict__ sent_id,
+                                                     const int32_t* __restrict__ len, int Tpad,
+                                                     int32_t* __restrict__ perm, int4* __restrict__ tiles,
+                                                     int32_t* __restrict__ n_tiles) {
+  __shared__ GroupScratch sh;
+  group_rows_block(B, S, G, sent_id, len, Tpad, perm, tiles, n_tiles, sh);
+}
+
+struct GroupLevels {
+  GroupLevel l[kMaxGroupLevels];
+};
+
+// Block b groups batch b of the launch.
+__global__ __launch_bounds__(1024) void k_group_levels(GroupLevels lv, int S, const int32_t* __restrict__ len,
+                                                       int Tpad) {
+  __shared__ GroupScratch sh;
+  const GroupLevel& g = lv.l[blockIdx.x];
+  group_rows_block(g.B, S, g.G, g.sent_id, len, Tpad, g.grp.perm, g.grp.tiles, g.grp.n_tiles, sh);
+}
+
+hipError_t launch_group_levels(const GroupLevel* lv, int n, int S, const int32_t* len, int Tpad, hipStream_t st) {
+  if (S > kGroupMaxS || Tpad > kMaxTpad) return hipErrorInvalidValue;
+  for (int i0 = 0; i0 < n; i0 += kMaxGroupLevels) {
+    GroupLevels g{};
+    const int k = std::min(kMaxGroupLevels, n - i0);
+    for (int i = 0; i < k; ++i) g.l[i] = lv[i0 + i];
+    hipLaunchKernelGGL(k_group_levels, dim3(k), dim3(1024), 0, st, g, S, len, Tpad);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+int attn_rows_per_tile(int B, int cus) {
+  int G = kAttnGroup;
+  while (G > 1 && 2 * ceil_div(B, G) < cus) G /= 2;
+  return G;
 }
 
 // Sums G values (G a power of two, 1 <= G <= 64) over the 64 lanes of a
@@ -1998,7 +2045,7 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
 template <int NQ>
 static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                          const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
-                         float* c, float* alpha, int c_bf16, int cus, hipStream_t st) {
+                         float* c, float* alpha, int c_bf16, int cus, hipStream_t st, bool grouped) {
   if (S > kGroupMaxS || !grp.perm) {
     hipLaunchKernelGGL(k_attention<NQ>, dim3(B), dim3(256), 0, st, B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len,
                        sent_id, S, v, c, alpha, c_bf16);
@@ -2011,10 +2058,10 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
   // CUs take tiles of 2 rows, or 1, spreading the same work over more CUs.
   // (At 1,000 rows of one sentence, 2-row tiles measured slower, 32 -> 40 us:
   // twice the tiles read the one sentence's keys at once.)
-  int G = kAttnGroup;
-  while (G > 1 && 2 * ceil_div(B, G) < cus) G /= 2;
-  hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
-                     grp.n_tiles);
+  const int G = attn_rows_per_tile(B, cus);
+  if (!grouped)
+    hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
+                       grp.n_tiles);
   if (G >= 4)
     attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
   else if (G == 2)
@@ -2025,17 +2072,17 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
 
 hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
-                            const AttnGroups& grp, bool c_bf16, int cus, hipStream_t st) {
+                            const AttnGroups& grp, bool c_bf16, int cus, hipStream_t st, bool grouped) {
   if (B <= 0) return hipSuccess;
   const int nq = ceil_div(A, 256);
   if (nq <= 1)
-    attention_nq<1>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
+    attention_nq<1>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st, grouped);
   else if (nq <= 2)
-    attention_nq<2>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
+    attention_nq<2>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st, grouped);
   else if (nq <= 4)
-    attention_nq<4>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
+    attention_nq<4>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st, grouped);
   else if (nq <= 8)
-    attention_nq<8>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st);
+    attention_nq<8>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, sent_id, grp, S, v, c, alpha, c_bf16 ? 1 : 0, cus, st, grouped);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
