@@ -106,3 +106,40 @@ def test_weight_streaming_forms_every_row(gpu, case):
             print(f"max |s_new(form {form}) - s_new(staged)| = {d:.2e}", flush=True)
             assert d <= TOL_FORMS, (form, "s_new")
     g.close()
+
+
+def test_streamed_step_at_full_size_with_signal_every_row(gpu):
+    """bf16_b4096's shapes (B = 4096 over 32 sentences, E = 500, H = A =
+    1024, V = 100,000), where the library streams all four products by
+    itself (form 0), with unit-gain weights and N(0, 1) annotations so that
+    every product carries signal: every row against the oracle, and the
+    staged form's first-GRU state bit for bit (neither splits K here)."""
+    from paper_1605_04809_amd import binding as nb
+    from paper_1605_04809_amd.workloads import CONFIGS
+    cfg = CONFIGS["bf16_b4096"]
+    wl = unit_gain(cfg)
+    ctx = random_annotations(cfg, seed=83)
+    g, o = gpu.GpuRun(wl, ctx_f32=ctx), gpu.OracleRun(wl, ctx_f32=ctx)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    prev = nb.debug_gemm_form(0)
+    try:
+        n0 = nb.debug_gemm_streamed()
+        out = g.step(*args)
+        streamed = nb.debug_gemm_streamed() - n0
+        nb.debug_gemm_form(2)
+        staged = g.step(*args)
+    finally:
+        nb.debug_gemm_form(prev)
+    assert streamed == 4, streamed
+    ref = o.step(*args)
+    assert np.all(np.isfinite(out["logp"]))
+    errs = {k: gpu.max_abs(out[k], ref[k]) for k in ("logp", "logZ", "s1", "c", "s_new", "t", "alpha")}
+    print("max |gpu - oracle|:", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert errs["logp"] <= TOL_LOGP_BF16 and errs["logZ"] <= TOL_LOGP_BF16, errs
+    for k in ("s1", "c", "s_new", "t", "alpha"):
+        assert errs[k] <= TOL_INTER_BF16_SIGNAL, (k, errs)
+    assert np.array_equal(out["s1"], staged["s1"])
+    d = gpu.max_abs(out["alpha"], staged["alpha"])
+    print(f"max |alpha(streamed) - alpha(staged)| = {d:.2e}", flush=True)
+    assert d <= TOL_FORMS
+    g.close()
