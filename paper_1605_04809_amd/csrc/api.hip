@@ -802,9 +802,14 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   if (e == hipSuccess) e = run_gru(g1, L.ks_g1);
   mark(NMT_PHASE_GRU1 + 1);
   // attention query q = s1 att_Wq
+  QuerySrc qsrc{q, 1, 0};
   if (e == hipSuccess) {
     PlainEpi ep{q, Aw, nullptr, Aw, 0, nullptr, 1, L.ks_q, (float*)(ws + L.kpart)};
+    // a split query leaves its sums for the attention to add as it loads
+    // them (the test switch's forced streaming writes q itself)
+    ep.defer_reduce = L.ks_q > 1 && !gemm_stream_forced(g_gemm_form.load(std::memory_order_relaxed));
     e = launch_gemm_plain(Tile::Small, make_a(B, {state_seg(s1, s1h, 0)}), m->att_Wq, ep, st, m->cus);
+    qsrc = ep.defer_reduce ? QuerySrc{ep.part, L.ks_q, (int64_t)B * Aw} : QuerySrc{q, 1, 0};
   }
   mark(NMT_PHASE_QUERY + 1);
   // masked attention and context
@@ -812,7 +817,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     // (a forest's levels come with their grouping done, all in one launch)
     const AttnGroups grp =
         pre_grp ? *pre_grp : AttnGroups{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
-    e = launch_attention(B, Aw, C, src->Tpad, q, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
+    e = launch_attention(B, Aw, C, src->Tpad, qsrc, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
                          src->S, m->att_v, c, d_alpha, grp, c16, m->cus, st, pre_grp != nullptr);
   }
   mark(NMT_PHASE_ATTENTION + 1);

@@ -92,6 +92,7 @@ struct PlainEpi {
   int32_t ksplit = 1;
   float* part = nullptr;
   __bf16* out16 = nullptr;  // nullable: the output goes here in bf16 (nearest even) instead of to out
+  int32_t defer_reduce = 0;  // ksplit > 1: leave the raw sums in part for the consumer to add (no epilogue)
 };
 
 // Epilogue of the GRU gate GEMM (see device.hpp for the cell).
@@ -191,9 +192,25 @@ struct AttnGroups {
 // sentences whose keys are too large for them (launch_key_factors); pctx the
 // keys themselves, which tiles with such keys and large queries score from.
 // c_bf16: the context c [B x C] is written in bf16 (nearest even) instead of fp32.
+// The attention's queries: q [B x A], or (ks > 1) the query GEMM's unreduced
+// split-K sums, ks blocks of `stride` floats laid out like q, which the
+// attention adds in split order as it loads them (the GEMM's own reduction,
+// without its launch).
+struct QuerySrc {
+  const float* q;
+  int32_t ks;
+  int64_t stride;
+};
+__device__ __forceinline__ f32x4 load_q(const QuerySrc& q, int row, int A, int a4) {
+  const float* p = q.q + (int64_t)row * A + 4 * a4;
+  if (q.ks <= 1) return *(const f32x4*)p;
+  f32x4 v = zero4();
+  for (int z = 0; z < q.ks; ++z) v += *(const f32x4*)(p + z * q.stride);
+  return v;
+}
 // grouped: grp already holds this batch's grouping (launch_group_levels, with
 // G = attn_rows_per_tile(B, cus)), so no grouping kernel runs.
-hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+hipError_t launch_attention(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S,
                             const float* v, float* c, float* alpha, const AttnGroups& grp, bool c_bf16,
                             int cus, hipStream_t st, bool grouped = false);

@@ -149,7 +149,7 @@ hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi
     plain_tile<kPlainSmallTM, kPlainSmallTN, 32, 32, P>(A, Wp, W, ep, ks, st);
   else
     plain_tile<kPlainLargeTM, kPlainLargeTN, 64, 64, P>(A, Wp, W, ep, ks, st);
-  if (ep.ksplit > 1) {
+  if (ep.ksplit > 1 && !ep.defer_reduce) {
     const int64_t n = (int64_t)A.M * ep.N;
     hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
   }
@@ -917,6 +917,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 static bool try_plain_ws(const AOperand& A, const Packed& W, const PlainEpi& ep, int cus, hipStream_t st) {
   const int form = g_gemm_form.load(std::memory_order_relaxed);
   if (form == 2 || !W.bf16 || cus <= 0 || A.M <= 0 || A.nseg < 1 || A.nseg > 3 || ep.N % 4) return false;
+  if (ep.defer_reduce) return false;  // the caller reads the split sums
   for (int i = 0; i < A.nseg; ++i)
     if (A.seg[i].nchunk % 2 || (i > 0 && !A.seg[i].bf16)) return false;
   // the epilogue's vector accesses: 16-byte aligned fp32 rows and bias,
@@ -1554,7 +1555,7 @@ hipError_t launch_key_factors(int S, int Tpad, int A, const float* pctx, float* 
 // scores over the row's sentence length, then every thread accumulates
 // float4 pieces of the context over the unmasked positions.
 template <int NQ>
-__global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, const float* __restrict__ q,
+__global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad, QuerySrc q,
                                                    const float* __restrict__ kfac, const float* __restrict__ pctx,
                                                    const int32_t* __restrict__ kbig, const float* __restrict__ ctx,
                                                    const int32_t* __restrict__ len,
@@ -1579,7 +1580,7 @@ __global__ __launch_bounds__(256) void k_attention(int B, int A, int C, int Tpad
 #pragma unroll
   for (int k = 0; k < NQ; ++k) {
     const int a4 = lane + 64 * k;
-    qv[k] = a4 < A4 ? *(const f32x4*)(q + (int64_t)row * A + 4 * a4) : zero4();
+    qv[k] = a4 < A4 ? load_q(q, row, A, a4) : zero4();
     vv[k] = a4 < A4 ? *(const f32x4*)(v + 4 * a4) * -2.f : zero4();
     big |= factor_big(qv[k]);
   }
@@ -1832,7 +1833,7 @@ __device__ __forceinline__ float wave_sums(float (&v)[G]) {
 }
 
 template <int G, int NQ, int NW>
-__device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int Tpad, const float* __restrict__ q,
+__device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int Tpad, QuerySrc q,
                                                const float* __restrict__ kfac, const float* __restrict__ pctx,
                                                const int32_t* __restrict__ kbig, const float* __restrict__ ctx,
                                                const int32_t* __restrict__ len, const int32_t* __restrict__ perm,
@@ -1856,7 +1857,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
   bool big = false;
   for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
     const int g = idx / A4, a4 = idx - g * A4;
-    const f32x4 qv = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+    const f32x4 qv = g < n ? load_q(q, rows[g], A, a4) : zero4();
     big |= factor_big(qv);
     qs[idx] = g < n ? tanh_factor(qv) : zero4();
   }
@@ -1894,7 +1895,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
   if (exact) {  // the queries themselves replace their factors (see kFactorSafe)
     for (int idx = threadIdx.x; idx < G * A4; idx += NT) {
       const int g = idx / A4, a4 = idx - g * A4;
-      qs[idx] = g < n ? *(const f32x4*)(q + (int64_t)rows[g] * A + 4 * a4) : zero4();
+      qs[idx] = g < n ? load_q(q, rows[g], A, a4) : zero4();
     }
     __syncthreads();
     score(std::true_type{}, pctx + (int64_t)s * Tpad * A);
@@ -1984,7 +1985,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
 // all rows, reading each annotation once.
 template <int G, int NQ, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NQ <= 4 ? 8 : 1))) void k_attention_grouped(
-    int A, int C, int Tpad, const float* __restrict__ q, const float* __restrict__ kfac, const float* __restrict__ pctx,
+    int A, int C, int Tpad, QuerySrc q, const float* __restrict__ kfac, const float* __restrict__ pctx,
     const int32_t* __restrict__ kbig, const float* __restrict__ ctx, const int32_t* __restrict__ len,
     const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
@@ -2012,7 +2013,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NQ <= 4
 }
 
 template <int G, int NQ>
-static void attention_grouped(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+static void attention_grouped(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,
                               const int32_t* kbig, const float* ctx, const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
                               float* alpha, int c_bf16, int cus, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
@@ -2043,7 +2044,7 @@ static void attention_grouped(int B, int A, int C, int Tpad, const float* q, con
 }
 
 template <int NQ>
-static void attention_nq(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+static void attention_nq(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,
                          const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, const AttnGroups& grp, int S, const float* v,
                          float* c, float* alpha, int c_bf16, int cus, hipStream_t st, bool grouped) {
   if (S > kGroupMaxS || !grp.perm) {
@@ -2070,7 +2071,7 @@ static void attention_nq(int B, int A, int C, int Tpad, const float* q, const fl
     attention_grouped<1, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
 }
 
-hipError_t launch_attention(int B, int A, int C, int Tpad, const float* q, const float* kfac, const float* pctx,
+hipError_t launch_attention(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,
                             const int32_t* kbig, const float* ctx, const int32_t* len, const int32_t* sent_id, int S, const float* v, float* c, float* alpha,
                             const AttnGroups& grp, bool c_bf16, int cus, hipStream_t st, bool grouped) {
   if (B <= 0) return hipSuccess;
