@@ -647,7 +647,7 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
                     m->enc_bias.bns, src->ctx + (int64_t)pos * C + dir * H, ldc, src->len, pos, H};
     }
     const bool split = src->enc_ks > 1 && p[0].A.nseg > 0 && p[1].A.nseg > 0;
-    e = split ? launch_gemm_gru_split(p, 2, H, m->bf16, src->enc_ks, src->gru_part, S, st)
+    e = split ? launch_gemm_gru_split(p, 2, H, m->bf16, src->enc_ks, src->gru_part, S, kGruSmallTM, st)
               : launch_gemm_gru(p, 2, H, m->bf16, m->cus, st);
   }
   if (e == hipSuccess) e = source_keys(m, src, st);
@@ -796,7 +796,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     // (the test switch's forced streaming skips the K split, which the
     // streamed form never takes, so that small batches reach it)
     return ks > 1 && !gemm_stream_forced(g_gemm_form.load(std::memory_order_relaxed))
-               ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, st)
+               ? launch_gemm_gru_split(&g, 1, H, m->bf16, ks, gpart, B, gru_split_tm(B, H, m->bf16, m->cus), st)
                   : launch_gemm_gru(&g, 1, H, m->bf16, m->cus, st);
   };
   if (e == hipSuccess) e = run_gru(g1, L.ks_g1);

@@ -127,15 +127,19 @@ hipError_t launch_gemm_plain(Tile t, const AOperand& A, const Packed& W, const P
                              int cus = 0);
 hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16, int cus, hipStream_t st);
 // K splits for a GRU launch of M rows whose A operand has `nchunks` K chunks:
-// 1 when the launch fills the chip as it is, else enough splits of the
-// small-row tile for about two blocks per compute unit (each split at least
-// four chunks, at most 8 splits).  Its launch needs part [ksplit][M][4][H].
+// 1 when the launch fills the chip as it is, else enough splits of the tile
+// gru_split_tm picks for about two 4-wave blocks (64 rows) or one 8-wave
+// block (128 rows) per compute unit (each split at least four chunks, at
+// most 8 splits).  Its launch needs part [ksplit][M][4][H].
 int gru_ksplit(int M, int H, int nchunks, bool bf16, int cus);
+// Rows of a split launch's tile: 128 where those tiles alone give half the
+// CUs a block (so two splits fill the chip), else 64.
+int gru_split_tm(int M, int H, bool bf16, int cus);
 // The same with the K chunks split over ksplit blocks per tile: raw sums go
 // to part [nprob][ksplit][part_M][4][H] (part_M >= every problem's rows), a
 // second kernel adds them in split order and applies the cell.
 hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool bf16, int ksplit, float* part,
-                                 int part_M, hipStream_t st);
+                                 int part_M, int tm, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
 int vocab_slices(int M, int V, bool bf16, int cus);

@@ -398,9 +398,16 @@ hipError_t launch_gemm_gru(const GruProblem* probs, int nprob, int H, bool bf16,
   return hipGetLastError();
 }
 
+int gru_split_tm(int M, int H, bool bf16, int cus) {
+  return 2 * (int64_t)ceil_div(M, kGruTM) * ceil_div(H, gru_hb(bf16)) >= cus ? kGruTM : kGruSmallTM;
+}
+
 int gru_ksplit(int M, int H, int nchunks, bool bf16, int cus) {
-  const int64_t blocks = (int64_t)ceil_div(M, kGruSmallTM) * ceil_div(H, gru_hb(bf16));
-  int ks = (int)std::min<int64_t>(8, (2 * (int64_t)cus) / std::max<int64_t>(blocks, 1));
+  const int tm = gru_split_tm(M, H, bf16, cus);
+  const int64_t blocks = (int64_t)ceil_div(M, tm) * ceil_div(H, gru_hb(bf16));
+  // about two 4-wave blocks per CU, or one 8-wave block
+  const int64_t target = tm == kGruSmallTM ? 2 * (int64_t)cus : (int64_t)cus;
+  int ks = (int)std::min<int64_t>(8, target / std::max<int64_t>(blocks, 1));
   ks = std::min(ks, nchunks / 4);
   return ks < 2 ? 1 : ks;
 }
@@ -442,7 +449,7 @@ __global__ void k_gru_cell(GruBatch batch, int H) {
 }
 
 hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool bf16, int ksplit, float* part,
-                                 int part_M, hipStream_t st) {
+                                 int part_M, int tm, hipStream_t st) {
   if (nprob < 1 || nprob > 2 || ksplit < 1 || !part) return hipErrorInvalidValue;
   GruBatch b{};
   b.p[0] = probs[0];
@@ -457,15 +464,22 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
     M = M > probs[i].A.M ? M : probs[i].A.M;
   }
   if (M <= 0) return hipSuccess;
-  constexpr int TM = kGruSmallTM;
-  if (bf16)
-    hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB16, kGruWM16, PrecBF16, true>),
-                       dim3(ceil_div(M, TM), ceil_div(H, kGruHB16), nprob * ksplit),
-                       dim3((TM / kGruWM16) * (kGruHB16 / 32) * 64), 0, st, b);
+  if (tm != kGruSmallTM && tm != kGruTM) return hipErrorInvalidValue;
+  auto run = [&](auto tmc) {
+    constexpr int TM = decltype(tmc)::value;
+    if (bf16)
+      hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB16, kGruWM16, PrecBF16, true>),
+                         dim3(ceil_div(M, TM), ceil_div(H, kGruHB16), nprob * ksplit),
+                         dim3((TM / kGruWM16) * (kGruHB16 / 32) * 64), 0, st, b);
+    else
+      hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB, kGruWM, PrecF32, true>),
+                         dim3(ceil_div(M, TM), ceil_div(H, kGruHB), nprob * ksplit),
+                         dim3((TM / kGruWM) * (kGruHB / 32) * 64), 0, st, b);
+  };
+  if (tm == kGruTM)
+    run(std::integral_constant<int, kGruTM>{});
   else
-    hipLaunchKernelGGL((k_gemm_gru<TM, kGruHB, kGruWM, PrecF32, true>),
-                       dim3(ceil_div(M, TM), ceil_div(H, kGruHB), nprob * ksplit),
-                       dim3((TM / kGruWM) * (kGruHB / 32) * 64), 0, st, b);
+    run(std::integral_constant<int, kGruSmallTM>{});
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gru_cell, dim3(ceil_div((int64_t)M * H, (int64_t)256), nprob), dim3(256), 0, st, b, H);

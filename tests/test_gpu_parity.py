@@ -373,12 +373,13 @@ def test_paper_sized_step_every_row(gpu, name):
     g.close()
 
 
-@pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "bf16")])
+@pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "bf16"), (1000, "bf16")])
 def test_launch_shape_boundaries_every_row(gpu, B, wtype):
     """Batches between the tile choices at the paper's dimensions: B = 2600
     takes the 64-row GRU tile with more than a round of 128-row blocks
     (fp32), B = 1445 takes 32 vocabulary slices over 23 row tiles, B = 667
-    (bf16) 64-row GRU blocks and 40 slices; every row."""
+    (bf16) 64-row GRU blocks split over K and 40 slices, B = 1000 (bf16)
+    128-row GRU blocks split over K in two; every row."""
     _torch()
     wl = make_workload(CONFIGS["enru_b2000"].replace(B=B, wtype=wtype, seed=43))
     g = gpu.GpuRun(wl)
