@@ -280,14 +280,14 @@ nmt_status hip_fail(hipError_t e, const char* what) {
 }
 
 // K split of a small-tile plain GEMM: at least four K chunks per block, and
-// enough blocks for about four per CU with fp32 weights, two with bf16
-// (measured on the readout at 256 CUs: fp32 1024 blocks, so 4 splits at
-// B = 2000; bf16 512, which leaves B = 4096 unsplit, 6.5 us faster than 2
-// splits and their reduction).
-int plain_ksplit(int M, int N, int K_total, int kc, Tile t, bool bf16, int cus) {
+// enough blocks for about two per CU (measured on the readout at 256 CUs:
+// bf16 512 blocks leave B = 4096 unsplit, 6.5 us faster than 2 splits and
+// their reduction; fp32 512 rather than 1024 blocks, 2 splits at B = 2000
+// and 4 at B = 1000, are 1.5-2 us faster).
+int plain_ksplit(int M, int N, int K_total, int kc, Tile t, int cus) {
   const int tiles = ceil_div(M, tile_m(t)) * ceil_div(N, tile_n(t));
   const int nc = ceil_div(K_total, kc);
-  int ks = ceil_div((bf16 ? 2 : 4) * cus, tiles);
+  int ks = ceil_div(2 * cus, tiles);
   if (ks > nc / 4) ks = nc / 4;
   if (ks > 8) ks = 8;
   return ks < 1 ? 1 : ks;
@@ -327,9 +327,9 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   // CUs idle (the shrinking batches of a forest or phrase loop); at B = 1000
   // (256 tiles) a split measured slower (28 -> 32 us).
   const int tiles_q = ceil_div(B, kPlainSmallTM) * ceil_div(d.A, kPlainSmallTN);
-  L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->bf16, m->cus) : 1;
+  L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->cus) : 1;
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->bf16, m->cus);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->cus);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
