@@ -1883,27 +1883,43 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
   }
   const bool exact = __syncthreads_or(big) && kbig[s];
   const int L = len[s];
+  // Tiles of fewer than 4 rows come from batches that leave the CUs short of
+  // tiles, where a tile's latency sets the kernel's: a wave then loads the
+  // keys of U positions (16 vectors a lane) before scoring any of them.
+  constexpr int U = G < 4 ? (16 / NQ < 4 ? 16 / NQ : 4) : 1;
   auto score = [&](auto exact_tag, const float* P) {
     constexpr bool EX = decltype(exact_tag)::value;
-    for (int i = wave; i < L; i += NW) {
-      float acc[G];
+    for (int i0 = wave; i0 < L; i0 += NW * U) {
+      f32x4 p[U][NQ];
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] = 0.f;
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int k = 0; k < NQ; ++k) {
-        const int a4 = lane + 64 * k;
-        if (a4 < A4) {
-          const f32x4 p = *(const f32x4*)(P + (int64_t)i * A + 4 * a4);
+        for (int k = 0; k < NQ; ++k) {
+          const int i = i0 + u * NW, a4 = lane + 64 * k;
+          p[u][k] = (i < L && a4 < A4) ? *(const f32x4*)(P + (int64_t)i * A + 4 * a4) : zero4();
+        }
 #pragma unroll
-          for (int g = 0; g < G; ++g) {
-            const f32x4 qq = qs[g * A4 + a4];
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * NW;
+        if (i >= L) break;  // uniform over the wave
+        float acc[G];
 #pragma unroll
-            for (int x = 0; x < 4; ++x) acc[g] = score_term_t<EX>(p[x], qq[x], vv[k][x], acc[g]);
+        for (int g = 0; g < G; ++g) acc[g] = 0.f;
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+          const int a4 = lane + 64 * k;
+          if (a4 < A4) {
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+              const f32x4 qq = qs[g * A4 + a4];
+#pragma unroll
+              for (int x = 0; x < 4; ++x) acc[g] = score_term_t<EX>(p[u][k][x], qq[x], vv[k][x], acc[g]);
+            }
           }
         }
+        const float r = wave_sums<G>(acc);
+        if ((lane & (64 / G - 1)) == 0) e[(lane / (64 / G)) * Tpad + i] = r;
       }
-      const float r = wave_sums<G>(acc);
-      if ((lane & (64 / G - 1)) == 0) e[(lane / (64 / G)) * Tpad + i] = r;
     }
   };
   if (exact) {  // the queries themselves replace their factors (see kFactorSafe)
@@ -1998,7 +2014,8 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
 // scores; finally every thread accumulates a float4 piece of the context of
 // all rows, reading each annotation once.
 template <int G, int NQ, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NQ <= 4 ? 8 : 1))) void k_attention_grouped(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NQ <= 4 ? (G < 4 ? 4 : 8) : 1))) void
+k_attention_grouped(
     int A, int C, int Tpad, QuerySrc q, const float* __restrict__ kfac, const float* __restrict__ pctx,
     const int32_t* __restrict__ kbig, const float* __restrict__ ctx, const int32_t* __restrict__ len,
     const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
