@@ -18,11 +18,23 @@ def _torch():
     return torch
 
 
-@pytest.mark.parametrize("name,B", [("tiny", 8), ("enru_b2000", 96)])
-def test_graph_replays_match_eager_step(name, B):
+@pytest.mark.parametrize("name,B,wtype,form", [("tiny", 8, "f32", 0), ("enru_b2000", 96, "f32", 0),
+                                               ("enru_b2000", 96, "bf16", 1)],
+                         ids=["tiny", "enru_b96", "enru_b96_bf16_streamed"])
+def test_graph_replays_match_eager_step(name, B, wtype, form):
+    """form 1 (nmt_debug.h) makes the bf16 products take the weight-streaming
+    kernels at this size, so they are captured too."""
     torch = _torch()
     from paper_1605_04809_amd import binding as nb
-    wl = make_workload(CONFIGS[name].replace(B=B, seed=91))
+    prev = nb.debug_gemm_form(form)
+    try:
+        _graph_replays(torch, nb, name, B, wtype)
+    finally:
+        nb.debug_gemm_form(prev)
+
+
+def _graph_replays(torch, nb, name, B, wtype):
+    wl = make_workload(CONFIGS[name].replace(B=B, seed=91, wtype=wtype))
     c = wl.cfg
     model = nb.Model.from_workload(wl)
     cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
@@ -57,6 +69,6 @@ def test_graph_replays_match_eager_step(name, B):
                            e_logZ, workspace=ws)
         torch.cuda.synchronize()
     assert nb.nmt_stream_status(model) == nb.NMT_OK
-    print(f"{name} B={B}: 4 graph replays equal the eager step", flush=True)
+    print(f"{name} B={B} {wtype}: 4 graph replays equal the eager step", flush=True)
     src.close()
     model.close()
