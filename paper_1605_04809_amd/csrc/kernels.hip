@@ -506,8 +506,8 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
 // side: FIRST_STATE says whether segment 0 is the state side (the second
 // GRU: [s1 | c]) or the input side (the first: [x | s_prev]), SRC16_i
 // whether segment i is stored in bf16 (else fp32, rounded to bf16 as it is
-// staged, which takes VPF = 2 weight steps in flight to keep the registers
-// within two waves per SIMD).  Taken when the grid covers the CUs.
+// staged; its second staging register set leaves room for 2 weight steps in
+// flight, which measured the same as 4).  Taken when the grid covers the CUs.
 constexpr int kWsTM = 128, kWsUB = 128, kWsKQ = 16;
 #ifndef NMT_WS_VPF_BF16_SRC   // weight steps in flight, both segments bf16
 #define NMT_WS_VPF_BF16_SRC 4
