@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 from paper_1605_04809_amd.workloads import CONFIGS, high_signal, make_forest, make_workload, random_annotations
+from paper_1605_04809_amd.workloads import unit_gain
 
 pytestmark = pytest.mark.gpu
 
@@ -53,23 +54,41 @@ def run_forest(g, fw, with_nodes=False):
     return f, pair_logp.cpu().numpy(), req_logp.cpu().numpy(), nodes
 
 
-@pytest.mark.parametrize("variant", ["tiny", "tiny_high_signal", "tiny_bf16"])
+@pytest.mark.parametrize("variant", ["tiny", "tiny_high_signal", "tiny_bf16", "bf16_streamed"])
 def test_forest_matches_naive_stepping(variant):
+    """bf16_streamed: H = A = 128 with unit-gain weights and the test switch
+    (nmt_debug.h) forcing the weight-streaming GEMMs, so that they run with
+    the forest's gathered input states and embedding rows."""
     _torch()
     from tests import gpu_cases
+    from paper_1605_04809_amd import binding as nb
     cfg = CONFIGS["tiny"].replace(S=3, len_lo=2, len_hi=10)
     ctx = None
     tol = TOL_TOKEN
+    form = 0
     if variant == "tiny_high_signal":
         cfg = high_signal(cfg).replace(sigma_w=0.3)
         ctx = random_annotations(cfg, seed=21)
     if variant == "tiny_bf16":
         cfg = cfg.replace(wtype="bf16")
         tol = TOL_TOKEN_BF16
-    wl = make_workload(cfg)
+    if variant == "bf16_streamed":
+        cfg = cfg.replace(wtype="bf16", H=128, A=128, E=100)
+        ctx = random_annotations(cfg, seed=22)
+        tol = TOL_TOKEN_BF16
+        form = 1
+    wl = unit_gain(cfg) if variant == "bf16_streamed" else make_workload(cfg)
     fw = make_forest(cfg, n_hyp=60, seed=5, max_phrases=6, max_len=5, branch=2)
     g, o = gpu_cases.GpuRun(wl, ctx_f32=ctx), gpu_cases.OracleRun(wl, ctx_f32=ctx)
-    f, got, _, _ = run_forest(g, fw)
+    prev = nb.debug_gemm_form(form)
+    try:
+        n0 = nb.debug_gemm_streamed()
+        f, got, _, _ = run_forest(g, fw)
+        streamed = nb.debug_gemm_streamed() - n0
+    finally:
+        nb.debug_gemm_form(prev)
+    if form == 1:  # four streamed products per tree depth
+        assert streamed == 4 * f.shape()["depth"], streamed
     want, lens = oracle_pairs(o, fw, np.arange(len(fw.phrases)))
     err = np.abs(got - want)
     print(f"{variant}: {len(fw.phrases)} pairs, depth {f.shape()['depth']}, "
