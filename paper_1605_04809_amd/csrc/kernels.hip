@@ -755,15 +755,19 @@ static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream
 // is staged); the others are bf16.  The output layout matches the GRU form:
 // register r of row fragment i is column 8 (r / 4) + 4 h + r % 4 of the
 // wave's 32 for batch row 32 i + l32, so a lane stores 4 consecutive columns.
-constexpr int kPwTM = 128, kPwKQ = 16, kPwVPF = 4;
+#ifndef NMT_PW_VPF  // weight steps in flight
+#define NMT_PW_VPF 4
+#endif
+constexpr int kPwTM = 128, kPwKQ = 16, kPwVPF = NMT_PW_VPF;
 
 template <int NSEG, bool SRC16_0, int KSPLIT>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k_plain_ws(AOperand A, const void* Wp,
                                                                                          int64_t Npad, PlainEpi ep) {
   using P = PrecBF16;
-  constexpr int TM = kPwTM, KQW = kPwKQ, NKS = KQW / 2, VPF = kPwVPF, NT = 512;
+  constexpr int TM = kPwTM, KQW = kPwKQ, NKS = KQW / 2, NT = 512;
   constexpr int NA = TM * KQW / NT;  // activation vectors per thread per chunk
   constexpr int NKL = NKS / KSPLIT;  // k steps per chunk and wave
+  constexpr int VPF = kPwVPF < NKL ? kPwVPF : NKL;
   constexpr int CW = 4 / KSPLIT;     // 32-column fragments per block
   static_assert(NKL % VPF == 0 && NA == 4, "ring slots fixed within a chunk");
   static_assert(NT / KQW == 32 && KQW == 16, "staging rows 32 apart");
@@ -1417,13 +1421,22 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
                                                      float* logZ, int* err, const float* __restrict__ zreq) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= B) return;
+  // Every load that depends on no other is issued before any is used, so the
+  // kernel waits for one round trip to memory instead of a chain of them: the
+  // row's ids, its first 64 partials, its requested logit, and (one request
+  // per row, no offsets) its requested word.
+  const int y = y_prev[row], s = sent_id[row];
+  const int sr = rq.state_row ? rq.state_row[row] : 0;
+  const float2 p0 = lane < nS ? part[(int64_t)lane * B + row] : make_float2(-INFINITY, 0.f);
+  const float zr = zreq ? zreq[row] : 0.f;
+  const int w_row = rq.req_off ? 0 : rq.req[row];
   const int j0 = rq.req_off ? rq.req_off[row] : row, j1 = rq.req_off ? rq.req_off[row + 1] : row + 1;
   const bool span_ok = 0 <= j0 && j0 <= j1 && j1 <= rq.nreq;
-  bool ok = span_ok;
-  const int y = y_prev[row], s = sent_id[row];
-  ok = ok && y >= -1 && y < V && s >= 0 && s < S;
-  if (rq.state_row) ok = ok && rq.state_row[row] >= 0 && rq.state_row[row] < rq.pool_rows;
-  if (span_ok)
+  bool ok = span_ok && y >= -1 && y < V && s >= 0 && s < S;
+  if (rq.state_row) ok = ok && sr >= 0 && sr < rq.pool_rows;
+  if (!rq.req_off)
+    ok = ok && w_row >= 0 && w_row < V;
+  else if (span_ok)
     for (int j = j0; j < j1; ++j) ok = ok && rq.req[j] >= 0 && rq.req[j] < V;
   if (!ok) {
     if (lane == 0) {
@@ -1434,11 +1447,13 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
     }
     return;
   }
-  float mx = -INFINITY;
-  for (int i = lane; i < nS; i += 64) mx = fmaxf(mx, part[(int64_t)i * B + row].x);
+  // the same arithmetic, in the same order, as a lane-strided pass over the slices
+  float mx = fmaxf(-INFINITY, p0.x);
+  for (int i = lane + 64; i < nS; i += 64) mx = fmaxf(mx, part[(int64_t)i * B + row].x);
   mx = wave_max(mx);
   float sum = 0.f;
-  for (int i = lane; i < nS; i += 64) {
+  if (p0.x != -INFINITY) sum += p0.y * expf(p0.x - mx);
+  for (int i = lane + 64; i < nS; i += 64) {
     const float2 p = part[(int64_t)i * B + row];
     if (p.x != -INFINITY) sum += p.y * expf(p.x - mx);
   }
@@ -1446,7 +1461,7 @@ __global__ __launch_bounds__(256) void k_lse_combine(int B, const float2* __rest
   const float lz = mx + logf(sum);
   if (lane == 0 && logZ) logZ[row] = lz;
   if (zreq && j1 == j0 + 1) {  // one request: its logit taken by the vocabulary kernel
-    if (lane == 0) logp[j0] = zreq[row] - lz;
+    if (lane == 0) logp[j0] = zr - lz;
     return;
   }
   const char* tr = t16 ? (const char*)((const __bf16*)t + (int64_t)row * bf16_row(E))
@@ -1713,6 +1728,8 @@ __device__ __forceinline__ int2 block_scan2(int& a, int& b, int (*wsum)[16]) {
   return tot;
 }
 
+constexpr int kGroupRowsHeld = 8;  // rows per thread whose bucket stays in registers
+
 struct GroupScratch {
   int cnt[kGroupMaxS + 1];    // rows per bucket, then the bucket's write cursor
   int order[kGroupMaxS + 1];  // buckets longest sentence first, the invalid bucket last
@@ -1731,17 +1748,36 @@ __device__ void group_rows_block(int B, int S, int G, const int32_t* __restrict_
   int* keyc = sh.keyc;
   auto& wsum = sh.wsum;
   const int tid = threadIdx.x, NB = S + 1, NK = Tpad + 1;
+  // The first kGroupRowsHeld rows per thread keep their bucket in registers
+  // from the count to the scatter, and every id and length is loaded before
+  // any is used, so the block waits for one round trip to memory, not one per
+  // row.  Rows past the first 1024 x kGroupRowsHeld are read again.
+  constexpr int RH = kGroupRowsHeld;
+  int bk[RH];
+#pragma unroll
+  for (int r = 0; r < RH; ++r) {
+    const int b = tid + 1024 * r;
+    bk[r] = b < B ? sent_id[b] : 0;
+  }
+  const int l0 = tid < S ? len[tid] : 0;
   for (int i = tid; i < NB; i += 1024) cnt[i] = 0;
   for (int k = tid; k < NK; k += 1024) keyc[k] = 0;
   __syncthreads();
   // rows per bucket, and the key of each bucket: Tpad - length (0 for the
   // longest sentence); the invalid bucket sorts last
-  for (int b = tid; b < B; b += 1024) {
+#pragma unroll
+  for (int r = 0; r < RH; ++r) {
+    const int b = tid + 1024 * r, s = bk[r];
+    bk[r] = (s >= 0 && s < S) ? s : S;
+    if (b < B) atomicAdd(&cnt[bk[r]], 1);
+  }
+  for (int b = tid + 1024 * RH; b < B; b += 1024) {
     const int s = sent_id[b];
     atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1);
   }
   for (int i = tid; i < NB; i += 1024) {
-    const int k = i < S ? Tpad - min(max(len[i], 0), Tpad) : Tpad;
+    const int li = i == tid ? l0 : (i < S ? len[i] : 0);
+    const int k = i < S ? Tpad - min(max(li, 0), Tpad) : Tpad;
     keyv[i] = k;
     atomicAdd(&keyc[k], 1);
   }
@@ -1777,7 +1813,12 @@ __device__ void group_rows_block(int B, int S, int G, const int32_t* __restrict_
     roff += n;
   }
   __syncthreads();
-  for (int b = tid; b < B; b += 1024) {
+#pragma unroll
+  for (int r = 0; r < RH; ++r) {
+    const int b = tid + 1024 * r;
+    if (b < B) perm[atomicAdd(&cnt[bk[r]], 1)] = b;
+  }
+  for (int b = tid + 1024 * RH; b < B; b += 1024) {
     const int s = sent_id[b];
     perm[atomicAdd(&cnt[(s >= 0 && s < S) ? s : S], 1)] = b;
   }
