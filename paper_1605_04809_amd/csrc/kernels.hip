@@ -1047,7 +1047,12 @@ struct VocabTune {
 // two named register sets; otherwise the compiler drains every load and
 // rotates registers at each loop back-edge.  No other vector-memory load is
 // issued in the loop: its wait would drain the prefetch ring.
-template <class P, int VPF>
+//
+// PAD_LAST: the last k group of the packed matrix is all padding (no weight
+// or bias row reaches it: fp32 with E + nb <= Kpad - 8), so its MFMAs, which
+// would only add zeros, are skipped; its loads stay, keeping the ring's
+// schedule.  With E = 500 that is 1 of 64 k groups.
+template <class P, int VPF, bool PAD_LAST = false>
 __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int t16, int M, int E,
                                                                       int nb, int Kpad, const f32x4* __restrict__ Wp,
                                                                       int64_t Npad, int V, int nM, int nS,
@@ -1178,24 +1183,29 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
         }
       }
       // weights as the MFMA's row operand, activations as its column operand
+      constexpr bool pad_step = PAD_LAST && decltype(last_blk)::value && p == VPF - 1;
+      if constexpr (!pad_step) {
 #pragma unroll
-      for (int f = 0; f < VFN; ++f)
+        for (int f = 0; f < VFN; ++f)
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          if constexpr (decltype(zc)::value)
-            acc[i][f] = P::mma0(ring[p][f], a[i]);
-          else
-            P::mma(ring[p][f], a[i], acc[i][f]);
-        }
+          for (int i = 0; i < FM; ++i) {
+            if constexpr (decltype(zc)::value)
+              acc[i][f] = P::mma0(ring[p][f], a[i]);
+            else
+              P::mma(ring[p][f], a[i], acc[i][f]);
+          }
+      }
       load(ring[p], soff);  // refill the slot just consumed, VPF steps ahead
       // Instruction order within the step: one MFMA, the next step's A
       // fragment reads (so they have the remaining MFMAs to land), the rest
       // of the MFMAs, then the refill.
-      constexpr int kMfmaPerStep = FM * VFN * (P::kBF16 ? 1 : 4);  // fp32: four MFMAs per fragment pair
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, FM, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
+      if constexpr (!pad_step) {
+        constexpr int kMfmaPerStep = FM * VFN * (P::kBF16 ? 1 : 4);  // fp32: four MFMAs per fragment pair
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, FM, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerStep - 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, VFN, 0);
+      }
     };
     // Blocks of VPF steps (a group has at least two): the first starts from
     // zero, the last refills the ring from the next group.  MFMA steps run at raised priority and the
@@ -1361,7 +1371,12 @@ hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int
   constexpr int PF = VocabTune<P>::VPF_MAX;
   // the deepest prefetch that divides the k groups into at least two blocks
   auto fits = [&](int vpf) { return PF >= vpf && nkg % vpf == 0 && nkg >= 2 * vpf; };
-  if (fits(16))
+  // the last k group only padding (see PAD_LAST; taken with the deepest prefetch)
+  const bool pad_last = !P::kBF16 && E + W.nbias <= W.Kpad - 2 * P::KV;
+  if (fits(16) && pad_last)
+    hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2), !P::kBF16>), grid, block, 0, st, t, t16, M, E, W.nbias,
+                       (int)W.Kpad, Wp, W.Npad, V, nM, nS, part, req1, req_off, nreq, zreq);
+  else if (fits(16))
     hipLaunchKernelGGL((k_vocab_lse<P, (PF >= 16 ? 16 : 2)>), grid, block, 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp,
                        W.Npad, V, nM, nS, part, req1, req_off, nreq, zreq);
   else if (fits(8))
