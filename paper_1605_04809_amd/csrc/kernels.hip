@@ -805,15 +805,23 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
     roff1[i] = NSEG > 1 ? seg_row_off(sg1, row, M) : kNoLoad;
     roff2[i] = NSEG > 2 ? seg_row_off(sg2, row, M) : kNoLoad;
   }
-  f32x4 ra[NA], rb[NA];  // rb: the second half of an fp32 source vector
+  // Activation chunks in flight in registers: the readout (three segments,
+  // one of them fp32) alternates two register sets, so a chunk's loads have
+  // two chunks' MFMAs to land (bf16_b4096 readout 38.8 -> 36.5 us); the
+  // query gained nothing from it.
+  constexpr int kPwADepth = NSEG == 3 ? 2 : 1;
+  // rb: the second half of an fp32 source vector
+  f32x4 ra[kPwADepth][NA], rb[kPwADepth][NA];
   // The bf16 segments from chunk c on, by selects (a branch between segments
   // of one type gets merged by the compiler into a dynamically indexed copy of
   // the segments in scratch memory).
-  auto aload16 = [&](int c, bool with0) {
+  auto aload16 = [&](auto sc, int c, bool with0) {
+    constexpr int S = decltype(sc)::value;
     if constexpr (NSEG == 1) {  // one segment: nothing to select
       const int kseg = c * KQW * P::KV;
 #pragma unroll
-      for (int i = 0; i < NA; ++i) load_a_raw<P, true>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 2, ra[i], rb[i]);
+      for (int i = 0; i < NA; ++i)
+        load_a_raw<P, true>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 2, ra[S][i], rb[S][i]);
       return;
     }
     const int si = (with0 && c < c1) ? 0 : (c < c2 || NSEG == 2 ? 1 : 2);
@@ -823,46 +831,51 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int ro = si == 0 ? roff0[i] : (si == 1 ? roff1[i] : roff2[i]);
-      load_a_raw<P, true>(res, ro, K, kseg + kin, kin, kseg * 2, ra[i], rb[i]);
+      load_a_raw<P, true>(res, ro, K, kseg + kin, kin, kseg * 2, ra[S][i], rb[S][i]);
     }
   };
-  auto aload = [&](int c) {  // chunk c of the whole A
+  auto aload = [&](auto sc, int c) {  // chunk c of the whole A into register set sc
+    constexpr int S = decltype(sc)::value;
     if constexpr (SRC16_0) {
-      aload16(c, true);
+      aload16(sc, c, true);
     } else if (c < c1) {  // a uniform branch to the fp32 segment's loads
       const int kseg = c * KQW * P::KV;
 #pragma unroll
       for (int i = 0; i < NA; ++i)
-        load_a_raw<P, false>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 4, ra[i], rb[i]);
+        load_a_raw<P, false>(res0, roff0[i], sg0.K, kseg + kin, kin, kseg * 4, ra[S][i], rb[S][i]);
     } else {
-      aload16(c, false);
+      aload16(sc, c, false);
     }
   };
   const int st_base = ((int)threadIdx.x % KQW) * TM + (((int)threadIdx.x / KQW) ^ ((int)threadIdx.x % KQW));
-  auto astore = [&](int stage, int c) {  // c: the chunk the staged data belongs to
+  auto astore = [&](int stage, auto sc, int c) {  // c: the chunk the staged data belongs to
+    constexpr int S = decltype(sc)::value;
     const bool s16 = SRC16_0 || c >= c1;
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      As[stage * KQW * TM + st_base + 32 * i] = s16 ? ra[i] : a_from_raw<P, false>(ra[i], rb[i]);
+      As[stage * KQW * TM + st_base + 32 * i] = s16 ? ra[S][i] : a_from_raw<P, false>(ra[S][i], rb[S][i]);
   };
   // fragment of k step ks (vectors 2 ks + h) for the 32 rows at r0 (a multiple of 32)
   auto afrag = [&](int stage, int ks, int r0) {
     const int v = 2 * ks + h;
     return As[stage * KQW * TM + r0 + v * TM + (l32 ^ v)];
   };
+  constexpr std::integral_constant<int, 0> I0{};
+  constexpr std::integral_constant<int, kPwADepth - 1> I1{};
 
   f32x16 acc[2] = {f32x16{}, f32x16{}};
   f32x4 ring[VPF];
 #pragma unroll
   for (int p = 0; p < VPF; ++p) wload(ring[p], 0, p);
-  aload(0);
-  astore(0, 0);
-  if (nch > 1) aload(1);
+  aload(I0, 0);
+  astore(0, I0, 0);
+  if (nch > 1) aload(I1, 1);
+  if (kPwADepth == 2 && nch > 2) aload(I0, 2);
   __syncthreads();
 
   const int r0 = 64 * wr, ks0 = kg * NKL;
-  for (int c = 0; c < nch; ++c) {
-    const int st = c & 1;
+  // the MFMAs of chunk c from LDS stage st
+  auto compute = [&](int c, int st) {
     f32x4 a0 = afrag(st, ks0, r0), a1 = afrag(st, ks0, r0 + 32);
     static_for<NKL>([&](auto jc) {
       constexpr int j = decltype(jc)::value, slot = j % VPF;
@@ -881,9 +894,28 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
       a0 = n0;
       a1 = n1;
     });
-    if (c + 1 < nch) astore(st ^ 1, c + 1);
-    if (c + 2 < nch) aload(c + 2);
-    __syncthreads();
+  };
+  if constexpr (kPwADepth == 1) {
+    for (int c = 0; c < nch; ++c) {
+      const int st = c & 1;
+      compute(c, st);
+      if (c + 1 < nch) astore(st ^ 1, I0, c + 1);
+      if (c + 2 < nch) aload(I0, c + 2);
+      __syncthreads();
+    }
+  } else {
+    // two chunks per trip: set 1 holds the odd chunks, set 0 the even ones
+    for (int c = 0; c < nch; c += 2) {
+      compute(c, 0);
+      if (c + 1 < nch) astore(1, I1, c + 1);
+      if (c + 3 < nch) aload(I1, c + 3);
+      __syncthreads();
+      if (c + 1 >= nch) break;
+      compute(c + 1, 1);
+      if (c + 2 < nch) astore(0, I0, c + 2);
+      if (c + 4 < nch) aload(I0, c + 4);
+      __syncthreads();
+    }
   }
 
   if constexpr (KSPLIT == 2) {  // the second group's sums to LDS, the first adds them
