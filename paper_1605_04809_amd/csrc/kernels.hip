@@ -767,6 +767,13 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
   constexpr int TM = kPwTM, KQW = kPwKQ, NKS = KQW / 2, NT = 512;
   constexpr int NA = TM * KQW / NT;  // activation vectors per thread per chunk
   constexpr int NKL = NKS / KSPLIT;  // k steps per chunk and wave
+  // Activation chunks in flight in registers: the readout (three segments,
+  // one of them fp32) alternates two register sets, so a chunk's loads have
+  // two chunks' MFMAs to land (bf16_b4096 readout 38.8 -> 36.5 us); the
+  // query gained nothing from it.
+  constexpr int kPwADepth = NSEG == 3 ? 2 : 1;
+  // weight steps in flight, up to a chunk's (a ring over two chunks' steps
+  // for the readout, slots following the chunk's parity, gained nothing)
   constexpr int VPF = kPwVPF < NKL ? kPwVPF : NKL;
   constexpr int CW = 4 / KSPLIT;     // 32-column fragments per block
   static_assert(NKL % VPF == 0 && NA == 4, "ring slots fixed within a chunk");
@@ -805,11 +812,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
     roff1[i] = NSEG > 1 ? seg_row_off(sg1, row, M) : kNoLoad;
     roff2[i] = NSEG > 2 ? seg_row_off(sg2, row, M) : kNoLoad;
   }
-  // Activation chunks in flight in registers: the readout (three segments,
-  // one of them fp32) alternates two register sets, so a chunk's loads have
-  // two chunks' MFMAs to land (bf16_b4096 readout 38.8 -> 36.5 us); the
-  // query gained nothing from it.
-  constexpr int kPwADepth = NSEG == 3 ? 2 : 1;
   // rb: the second half of an fp32 source vector
   f32x4 ra[kPwADepth][NA], rb[kPwADepth][NA];
   // The bf16 segments from chunk c on, by selects (a branch between segments
