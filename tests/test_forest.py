@@ -104,3 +104,18 @@ def test_bad_pairs_are_rejected():
     with pytest.raises(nb.NmtError) as ei:
         build([1], [0], [1], [[3]])
     assert ei.value.status == nb.NMT_ERANGE
+
+
+def test_phrases_flatten_for_the_rescorer():
+    """The rescorer binding's flat form of a stack's phrases: phrase j is
+    words[off[j]:off[j+1]], in order, empty phrases included."""
+    off, words = nb.phrases_csr([[5, 6], [], (7,), np.array([8, 9, 10]), []])
+    assert off.dtype == np.int32 and words.dtype == np.int32
+    assert off.tolist() == [0, 2, 2, 3, 6, 6]
+    assert words.tolist() == [5, 6, 7, 8, 9, 10]
+    off, words = nb.phrases_csr([])
+    assert off.tolist() == [0] and words.size == 0
+    rng = np.random.default_rng(3)
+    phrases = [rng.integers(0, 1000, size=rng.integers(0, 5)).tolist() for _ in range(200)]
+    off, words = nb.phrases_csr(phrases)
+    assert [words[off[j]:off[j + 1]].tolist() for j in range(len(phrases))] == phrases
