@@ -769,8 +769,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
   constexpr int NKL = NKS / KSPLIT;  // k steps per chunk and wave
   // Activation chunks in flight in registers: the readout (three segments,
   // one of them fp32) alternates two register sets, so a chunk's loads have
-  // two chunks' MFMAs to land (bf16_b4096 readout 38.8 -> 36.5 us); the
-  // query gained nothing from it.
+  // two chunks' MFMAs to land (bf16_b4096 readout 35.8 -> 32.9 us by trace);
+  // the query gained nothing from it.
   constexpr int kPwADepth = NSEG == 3 ? 2 : 1;
   // weight steps in flight, up to a chunk's (a ring over two chunks' steps
   // for the readout, slots following the chunk's parity, gained nothing)
