@@ -115,7 +115,21 @@ def cpu_baseline(wl, min_seconds=10.0, max_seconds=30.0):
         chunk = int(max(threads, min(4 * B, rate * min(min_seconds - elapsed + 1.0, max_seconds - elapsed))))
     return {"value": done / elapsed, "unit": UNIT, "cores": threads, "kind": "oracle",
             "sample": f"{done} rows of the same workload (consecutive rows of the {B}-row batch, wrapping "
-                      f"round it), one step each, fp64, {elapsed:.1f} s wall; source encoding excluded"}
+                      f"round it), one step each, fp64, {elapsed:.1f} s wall; source encoding excluded",
+            "host": {"nproc": os.cpu_count(), "cpu_model": cpu_model(),
+                     "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_probe(nbytes: int, reps: int = 5):
