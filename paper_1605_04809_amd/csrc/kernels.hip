@@ -1912,28 +1912,53 @@ int attn_rows_per_tile(int B, int cus) {
   return G;
 }
 
-// Sums G values (G a power of two, 1 <= G <= 64) over the 64 lanes of a
-// wave: each butterfly step halves the values a lane keeps, so the G sums
-// cost about log2(64) + G shuffles instead of G * log2(64).  On return the
-// sum of value g sits in every lane whose bits 5, 4, ... (the top log2(G)
-// lane bits, most significant first) spell g; the caller reads it from lane
-// g * (64 / G).
+// Cross-lane exchanges of gfx950 for the wave sums below.  swap32(x, y)
+// returns [x's two 32-lane halves added | y's halves added]: one
+// v_permlane32_swap trades x's upper half for y's lower half.  swap16 does
+// the same for the rows of 16 lanes: [x0 + x1, y0 + y1, x2 + x3, y2 + y3] for
+// rows x0..x3 and y0..y3.  (The pair's elements are read into scalars before
+// any bit cast: a bit cast of an element of the returned vector read
+// element 0 for both.)
+__device__ __forceinline__ float swap32_add(float x, float y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, y),
+                                                  false, false);
+  const unsigned a = r[0], b = r[1];
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+__device__ __forceinline__ float swap16_add(float x, float y) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, y),
+                                                  false, false);
+  const unsigned a = r[0], b = r[1];
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+// x plus the value of the lane n places higher in its row of 16 (0 past the
+// row's end): a DPP row shift.
+template <int N>
+__device__ __forceinline__ float add_row_shl(float x) {
+  const int y = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x100 + N, 0xf, 0xf, false);
+  return x + __builtin_bit_cast(float, y);
+}
+
+// Sums of G values (G = 1, 2 or 4) over the 64 lanes of a wave: the sum of
+// v[g] ends in lane g * (64 / G).  Two halving exchanges (32 lanes, then
+// 16) each add two values per exchange, then four DPP shifts sum each row
+// of 16 lanes into its first lane: seven cross-lane operations with no
+// selects, where a butterfly over lane-chosen array elements compiled to
+// chains of compares and selects around seven LDS permutes.
 template <int G>
 __device__ __forceinline__ float wave_sums(float (&v)[G]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int n = G, o = 32; n > 1; n >>= 1, o >>= 1) {
-    const bool hi = (lane & o) != 0;
-#pragma unroll
-    for (int j = 0; j < n / 2; ++j) {
-      const float keep = hi ? v[j + n / 2] : v[j], give = hi ? v[j] : v[j + n / 2];
-      v[j] = keep + __shfl_xor(give, o, 64);
-    }
+  static_assert(G == 1 || G == 2 || G == 4, "one, two or four values per lane");
+  float w;
+  if constexpr (G == 4) {
+    w = swap16_add(swap32_add(v[0], v[2]), swap32_add(v[1], v[3]));  // rows 0..3 in 16-lane rows 0..3
+  } else {
+    const float h = swap32_add(v[0], v[G - 1]);  // G = 2: [v0 | v1]; G = 1: both halves v0
+    w = swap16_add(h, h);
   }
-  float r = v[0];
-#pragma unroll
-  for (int o = 32 / G; o >= 1; o >>= 1) r += __shfl_xor(r, o, 64);
-  return r;
+  w = add_row_shl<1>(w);
+  w = add_row_shl<2>(w);
+  w = add_row_shl<4>(w);
+  return add_row_shl<8>(w);
 }
 
 template <int G, int NQ, int NW>
