@@ -246,6 +246,22 @@ def test_minimal_dimensions(gpu, V, wtype):
     g.close()
 
 
+@pytest.mark.parametrize("E", [244, 248, 500, 504, 508])
+def test_vocabulary_padding_boundary(gpu, E):
+    """Readout widths on both sides of the vocabulary kernel's skipped
+    padding: the fp32 kernel leaves out the MFMAs of its last k group when no
+    weight or bias row reaches it (E + 1 <= Kpad - 8, i.e. E = 244 and 500
+    here, with Kpad = 256 and 512), and runs every k group otherwise (248,
+    504, 508; E is a multiple of 4).  Unit-gain weights, so every readout value and the bias (row
+    E) move log p well beyond the bar; every row against the oracle."""
+    _torch()
+    wl = unit_gain(CONFIGS["tiny"].replace(E=E, V=3001, B=70, S=2, len_lo=3, len_hi=9, Tpad=9, seed=31 + E))
+    g, o = gpu.GpuRun(wl), gpu.OracleRun(wl)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    compare(g.step(*args), o.step(*args), tol=TOL_INTER_HS)
+    g.close()
+
+
 @pytest.mark.parametrize("wtype,V", [("f32", 1000), ("bf16", 1000), ("bf16", 3001)])
 def test_output_bias_is_exact(gpu, wtype, V):
     """With zero output weights every logit is its bias, so log Z is the
