@@ -83,3 +83,34 @@ def test_large_keys_defeat_clamped_factors(case):
     d = np.abs(a - ref["alpha"]).max()
     print(f"max |pctx| {np.abs(pctx).max():.1f}, max |q| {np.abs(q).max():.1f}, clamped-factor |d alpha| {d:.3g}")
     assert d >= 100 * TOL_ALPHA
+
+
+def _drop_bias(p):  # what skipping the k group that holds the bias row would do
+    p["out_b"] = np.zeros_like(p["out_b"])
+
+
+def _drop_last_readout_rows(p):  # what skipping the last real k rows (E - 4 .. E - 1) would do
+    w = p["out_W"].copy()
+    w[-4:, :] = 0
+    p["out_W"] = w
+
+
+@pytest.mark.parametrize("E", [244, 500])
+@pytest.mark.parametrize("broken", [_drop_bias, _drop_last_readout_rows], ids=["bias", "last_rows"])
+def test_vocabulary_padding_mistakes_move_log_p(E, broken):
+    """The inputs of the GPU test at the vocabulary kernel's skipped padding:
+    dropping the bias row or the readout's last four rows from the output
+    projection moves log p far beyond the 1e-4 bar."""
+    from paper_1605_04809_amd.workloads import CONFIGS
+    wl = unit_gain(CONFIGS["tiny"].replace(E=E, V=3001, B=70, S=2, len_lo=3, len_hi=9, Tpad=9, seed=31 + E))
+    c = wl.cfg
+    m = oracle.Model(wl.params, c.V_src, c.V, c.E, c.H, c.A)
+    ctx, pctx, _ = oracle.encode(m, wl.src_ids, wl.src_len)
+    ref = oracle.score_batch(m, ctx, pctx, wl.src_len, wl.s_prev, wl.y_prev, wl.sent_id, wl.req, intermediates=False)
+    p = dict(wl.params)
+    broken(p)
+    mb = oracle.Model(p, c.V_src, c.V, c.E, c.H, c.A)
+    bad = oracle.score_batch(mb, ctx, pctx, wl.src_len, wl.s_prev, wl.y_prev, wl.sent_id, wl.req, intermediates=False)
+    d = np.abs(bad["logp"] - ref["logp"]).max()
+    print(f"E={E}: max |d logp| {d:.3g}")
+    assert d >= 100 * TOL_HS
