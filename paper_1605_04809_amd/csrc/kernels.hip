@@ -1144,6 +1144,15 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
       }
     }
   }
+  // The group of this slice whose MFMAs produce each slot's requested logit
+  // in this lane (column 32 cb + acc_row(r, h) sits in lane half h when bit 2
+  // of the column is h), or -1: the loop then tests one integer per slot.
+  int rq_g[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int cb = rq[i] >> 5;
+    rq_g[i] = (rq[i] >= 0 && cb >= cb_begin && cb < cb_end && ((rq[i] >> 2) & 1) == h) ? (cb - cb_begin) / VFN : -1;
+  }
 
   // Weight fragments are read through a buffer resource over the packed
   // matrix: a lane's offset (its column and k half) is fixed, and one scalar
@@ -1286,19 +1295,26 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
     // sits in register r of block f of lane half h.  Only the group's blocks
     // below cb_end are this slice's (the rest belong to the next slice and
     // were masked above), so every column has exactly one writer; columns
-    // past V are never requested by a valid id.  Rarely taken.
-    const unsigned own = 32u * (unsigned)min(VFN, cb_end - cb0);
+    // past V are never requested by a valid id.  A wave-uniform branch, taken
+    // only when some lane of the wave holds a requested logit here (the
+    // per-lane test alone was if-converted into some 400 mask and select
+    // instructions per group, with SGPR spills into vector lanes).
+    bool hit = false;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int d = rq[i] - 32 * cb0;
-      if ((unsigned)d < own && ((d >> 2) & 1) == h) {
-        const int ff = d >> 5, rr = ((d & 31) >> 3) * 4 + (d & 3);
-        float z = 0.f;
+    for (int i = 0; i < FM; ++i) hit |= rq_g[i] == gcur;
+    if (__builtin_amdgcn_ballot_w64(hit)) {
 #pragma unroll
-        for (int f = 0; f < VFN; ++f)
+      for (int i = 0; i < FM; ++i) {
+        if (rq_g[i] == gcur) {
+          const int d = rq[i] - 32 * cb0;
+          const int idx = (d >> 5) * 16 + ((d & 31) >> 3) * 4 + (d & 3);  // 16 f + r
+          float z = 0.f;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) z = (f == ff && r == rr) ? acc[i][f][r] : z;
-        zreq[m0 + 32 * i + l32] = z;
+          for (int f = 0; f < VFN; ++f)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) z = idx == 16 * f + r ? acc[i][f][r] : z;
+          zreq[m0 + 32 * i + l32] = z;
+        }
       }
     }
     // fold the group into each row slot's running log-sum-exp
