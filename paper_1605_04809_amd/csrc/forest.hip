@@ -297,11 +297,17 @@ nmt_status nmt_rescore_stack(nmt_rescorer* r, int32_t n, const int32_t* h_parent
     const size_t b = nmt_forest_workspace_bytes(r->models[k], f);
     ws_need = b > ws_need ? b : ws_need;
   }
-  hipError_t e = hipStreamSynchronize(st);  // buffers may be reallocated below
+  // A buffer that grows is freed first: wait for the stream only then (the
+  // previous call's work ended with a synchronisation of its own).
+  const size_t nodes_need = (size_t)n_rows * maxH * 4, logp_need = (size_t)r->K * np * 4,
+               gather_need = (size_t)2 * n * 4;
+  const bool grow = ws_need > r->ws.cap || nodes_need > r->nodes.cap || logp_need > r->pair_logp.cap ||
+                    gather_need > r->gather.cap;
+  hipError_t e = grow ? hipStreamSynchronize(st) : hipSuccess;
   if (e == hipSuccess) e = r->ws.ensure(ws_need);
-  if (e == hipSuccess) e = r->nodes.ensure((size_t)n_rows * maxH * 4);
-  if (e == hipSuccess) e = r->pair_logp.ensure((size_t)r->K * np * 4);
-  if (e == hipSuccess) e = r->gather.ensure((size_t)2 * n * 4);
+  if (e == hipSuccess) e = r->nodes.ensure(nodes_need);
+  if (e == hipSuccess) e = r->pair_logp.ensure(logp_need);
+  if (e == hipSuccess) e = r->gather.ensure(gather_need);
   if (e != hipSuccess) {
     nmt_forest_destroy(f);
     return forest_fail(e == hipErrorOutOfMemory ? NMT_ENOMEM : NMT_EDEVICE, hipGetErrorString(e));
