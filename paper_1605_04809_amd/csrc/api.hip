@@ -1125,6 +1125,7 @@ bool nmt_internal_group_levels(const nmt_model* m, const nmt_source* src, GroupL
 }
 
 int32_t nmt_internal_hidden(const nmt_model* m) { return m->dims.H; }
+int32_t nmt_internal_sentences(const nmt_source* src) { return src->S; }
 int32_t nmt_internal_vocab(const nmt_model* m) { return m->dims.V; }
 int nmt_internal_device(const nmt_model* m) { return m->device; }
 

@@ -47,6 +47,7 @@ nmt_status nmt_internal_score_step(nmt_model* m, const nmt_source* src, int32_t 
 bool nmt_internal_group_levels(const nmt_model* m, const nmt_source* src, GroupLevel* lv, int n, hipStream_t st,
                                hipError_t* err);
 int32_t nmt_internal_hidden(const nmt_model* m);
+int32_t nmt_internal_sentences(const nmt_source* src);
 int32_t nmt_internal_vocab(const nmt_model* m);
 int nmt_internal_device(const nmt_model* m);
 
@@ -109,15 +110,21 @@ nmt_status nmt_score_forest(nmt_model* m, const nmt_source* src, const nmt_fores
   int32_t* d_path = d_req + f->n_req;
   hipError_t e = hipMemcpyAsync(idx, f->upload.data(), f->upload.size() * 4, hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
-  // the attention's grouping of rows by sentence, for all levels at once
+  // the attention's grouping of rows by sentence, for all levels at once;
+  // when every row is of one (valid) sentence, as in the stack rescoring of
+  // one sentence, no grouping: each level's attention tiles its rows in order
+  int32_t s_one = f->n_rows > 0 ? f->sent[0] : -1;
+  for (int32_t i = 1; i < f->n_rows && s_one >= 0; ++i)
+    if (f->sent[i] != s_one) s_one = -1;
+  if (s_one < 0 || s_one >= nmt_internal_sentences(src)) s_one = -1;
   std::vector<GroupLevel> lv((size_t)f->depth);
   for (int d = 1; d <= f->depth; ++d) {
     const int32_t r0 = f->row_base[d - 1];
     lv[d - 1] = GroupLevel{f->rows_lv[d - 1], 0, d_sent + r0,
                            AttnGroups{(int32_t*)(ws + L.perm) + r0, (int4*)(ws + L.tiles) + r0,
-                                      (int32_t*)(ws + L.ntiles) + (d - 1)}};
+                                      (int32_t*)(ws + L.ntiles) + (d - 1), s_one}};
   }
-  const bool grouped = nmt_internal_group_levels(m, src, lv.data(), f->depth, st, &e);
+  const bool grouped = s_one >= 0 || nmt_internal_group_levels(m, src, lv.data(), f->depth, st, &e);
   if (e != hipSuccess) return forest_fail(NMT_EDEVICE, hipGetErrorString(e));
   for (int d = 1; d <= f->depth; ++d) {
     const int32_t r0 = f->row_base[d - 1], q0 = f->req_base[d - 1];

@@ -191,6 +191,7 @@ struct AttnGroups {
   int32_t* perm;
   int4* tiles;
   int32_t* n_tiles;
+  int32_t one_sentence = -1;  // >= 0: every row is this sentence, tiled in row order with no grouping
 };
 // kfac [S x Tpad x A]: the keys' factors 2^{2 log2(e) pctx}, kbig [S] the
 // sentences whose keys are too large for them (launch_key_factors); pctx the

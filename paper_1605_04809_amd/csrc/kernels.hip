@@ -1987,7 +1987,7 @@ __device__ __forceinline__ void attention_tile(const int4 tl, int A, int C, int 
                                                int lane, int A4, int C4, int c_bf16, int npg) {
   constexpr int NT = NW * 64;
   const int s = tl.x, n = tl.z;
-  if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? perm[tl.y + threadIdx.x] : 0;
+  if (threadIdx.x < G) rows[threadIdx.x] = (int)threadIdx.x < n ? (perm ? perm[tl.y + threadIdx.x] : tl.y + (int)threadIdx.x) : 0;
   __syncthreads();
   if (s < 0) {  // rows with an invalid sentence: flagged and NaN-ed by the combine kernel
     for (int g = 0; g < n; ++g) {
@@ -2151,11 +2151,13 @@ k_attention_grouped(
     const int32_t* __restrict__ kbig, const float* __restrict__ ctx, const int32_t* __restrict__ len,
     const int32_t* __restrict__ perm, const int4* __restrict__ tiles,
     const int32_t* __restrict__ n_tiles, const float* __restrict__ v, float* __restrict__ c,
-    float* __restrict__ alpha, int c_bf16, int round, int npg) {
+    float* __restrict__ alpha, int c_bf16, int round, int npg, int one_s, int one_sentence_B) {
   // queries [G][A/4] (later the context's partial sums [npg-1][G][C/4]), then scores [G][Tpad]
   extern __shared__ f32x4 dyn[];
   __shared__ int rows[G];
-  const int nt = *n_tiles;
+  // one_sentence_B > 0: a batch of that many rows, all of sentence one_s,
+  // tiled in row order with no grouping kernel (every tile the same length)
+  const int nt = one_sentence_B > 0 ? (one_sentence_B + G - 1) / G : *n_tiles;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int A4 = A / 4, C4 = C / 4;
   f32x4* qs = dyn;
@@ -2166,19 +2168,22 @@ k_attention_grouped(
   // blocks, and the tiles come longest first.  Every other round takes its
   // tiles in reverse, so the CU that got the longest tile of one round gets
   // the shortest of the next, and the CUs' total lengths even out.
-  if (round > 0) {
+  if (round > 0 && one_sentence_B == 0) {
     const int r = t / round, p = t - r * round;
     if (r & 1) t = r * round + (min(round, nt - r * round) - 1 - p);
   }
-  attention_tile<G, NQ, NW>(tiles[t], A, C, Tpad, q, kfac, pctx, kbig, ctx, len, perm, v, c, alpha, qs, e, rows, wave,
-                            lane, A4, C4, c_bf16, npg);
+  const int4 tl = one_sentence_B > 0 ? make_int4(one_s, t * G, min(G, one_sentence_B - t * G), 0) : tiles[t];
+  attention_tile<G, NQ, NW>(tl, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, one_sentence_B > 0 ? nullptr : perm, v, c,
+                            alpha, qs, e, rows, wave, lane, A4, C4, c_bf16, npg);
 }
 
 template <int G, int NQ>
 static void attention_grouped(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,
                               const int32_t* kbig, const float* ctx, const int32_t* len, const AttnGroups& grp, int S, const float* v, float* c,
-                              float* alpha, int c_bf16, int cus, hipStream_t st) {
-  const int grid = (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);  // at least the number of tiles
+                              float* alpha, int c_bf16, int cus, hipStream_t st, int one_s) {
+  // at least the number of tiles (exactly, for one sentence)
+  const int grid = one_s >= 0 ? ceil_div(B, G) : (int)std::min<int64_t>(B, (int64_t)ceil_div(B, G) + S + 1);
+  const int one_B = one_s >= 0 ? B : 0;
   const int round = NMT_ATTN_SNAKE ? cus : 0;
   // Position groups of the context phase: whole waves per group (C/4 a
   // multiple of 64), so every wave meets its one barrier.
@@ -2196,12 +2201,12 @@ static void attention_grouped(int B, int A, int C, int Tpad, QuerySrc q, const f
     const int npg = groups(2 * kAttnWaves * 64);
     hipLaunchKernelGGL((k_attention_grouped<G, NQ, 2 * kAttnWaves>), dim3(grid), dim3(2 * kAttnWaves * 64),
                        lds_bytes(npg), st, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles,
-                       v, c, alpha, c_bf16, round, npg);
+                       v, c, alpha, c_bf16, round, npg, one_s, one_B);
   } else {
     const int npg = groups(kAttnWaves * 64);
     hipLaunchKernelGGL((k_attention_grouped<G, NQ, kAttnWaves>), dim3(grid), dim3(kAttnWaves * 64), lds_bytes(npg), st,
                        A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp.perm, grp.tiles, grp.n_tiles, v, c, alpha, c_bf16,
-                       round, npg);
+                       round, npg, one_s, one_B);
   }
 }
 
@@ -2222,15 +2227,21 @@ static void attention_nq(int B, int A, int C, int Tpad, QuerySrc q, const float*
   // (At 1,000 rows of one sentence, 2-row tiles measured slower, 32 -> 40 us:
   // twice the tiles read the one sentence's keys at once.)
   const int G = attn_rows_per_tile(B, cus);
-  if (!grouped)
+  // Rows of a single sentence need no grouping: their tiles are runs of
+  // consecutive rows.  That holds for a source of one sentence (a row with
+  // another sentence id is still flagged, and its log p made NaN, by the
+  // combine; its attention then reads sentence 0), or when the caller knows
+  // every row's sentence (grp.one_sentence, checked against S on the host).
+  const int one = grp.one_sentence >= 0 ? grp.one_sentence : (!grouped && S == 1 ? 0 : -1);
+  if (!grouped && one < 0)
     hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(1024), 0, st, B, S, G, sent_id, len, Tpad, grp.perm, grp.tiles,
                        grp.n_tiles);
   if (G >= 4)
-    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
+    attention_grouped<4, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st, one);
   else if (G == 2)
-    attention_grouped<2, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
+    attention_grouped<2, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st, one);
   else
-    attention_grouped<1, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st);
+    attention_grouped<1, NQ>(B, A, C, Tpad, q, kfac, pctx, kbig, ctx, len, grp, S, v, c, alpha, c_bf16, cus, st, one);
 }
 
 hipError_t launch_attention(int B, int A, int C, int Tpad, QuerySrc q, const float* kfac, const float* pctx,

@@ -246,6 +246,32 @@ def test_minimal_dimensions(gpu, V, wtype):
     g.close()
 
 
+@pytest.mark.parametrize("B", [300, 1100, 2800])
+def test_one_sentence_tiling_equals_the_grouped_one(gpu, B):
+    """Rows of a one-sentence source are tiled in row order with no grouping
+    kernel; the same rows over a two-sentence source (all of them in its
+    first sentence) go through the grouping.  Each row's arithmetic is the
+    same in any tile, so every output matches bit for bit (attention at the
+    paper's width: 16-wave blocks of 4-row tiles at 1,100 rows, 8-wave blocks
+    at 2,800, 2-row tiles at 300)."""
+    torch = _torch()
+    cfg = ATT.replace(B=B, S=2, Tpad=24, len_lo=17, len_hi=24, seed=91)
+    wl2 = unit_gain(cfg)
+    ctx2 = random_annotations(cfg, seed=92)
+    wl2.sent_id = np.zeros(B, np.int32)
+    g2 = gpu.GpuRun(wl2, ctx_f32=ctx2)
+    wl1 = unit_gain(cfg)  # the same draws; only the source differs
+    wl1.cfg = cfg.replace(S=1)
+    wl1.src_len = wl2.src_len[:1]
+    g1 = gpu.GpuRun(wl1, ctx_f32=np.ascontiguousarray(ctx2[:1]), model=g2.model)
+    args = (wl2.s_prev, wl2.y_prev, wl2.sent_id, wl2.req)
+    one, grouped = g1.step(*args), g2.step(*args)
+    for k in ("logp", "logZ", "s_new", "c", "alpha", "t", "s1"):
+        np.testing.assert_array_equal(one[k], grouped[k], err_msg=k)
+    g1.src.close()
+    g2.close()
+
+
 @pytest.mark.parametrize("E", [244, 248, 500, 504, 508])
 def test_vocabulary_padding_boundary(gpu, E):
     """Readout widths on both sides of the vocabulary kernel's skipped
