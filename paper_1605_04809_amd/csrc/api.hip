@@ -1157,9 +1157,12 @@ nmt_status nmt_profile_begin(nmt_model* m, int32_t max_steps) {
   drop_profile_events(m);
   const size_t n = (size_t)max_steps * (NMT_NUM_PHASES + 1);
   m->prof_events.reserve(n);
+  // Timing-only events: without the system-scope fence a recorded event
+  // would otherwise add (an L2 write-back and invalidate), so the kernel
+  // after each event runs as it does in an untimed step.
   for (size_t i = 0; i < n; ++i) {
     hipEvent_t ev;
-    hipError_t e = hipEventCreate(&ev);
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableSystemFence);
     if (e != hipSuccess) {
       drop_profile_events(m);
       return hip_fail(e, "nmt_profile_begin");
