@@ -60,13 +60,18 @@ def kernel_source_hash() -> str:
 
 
 def step_flops(cfg, src_len, sent_id):
-    """Algorithmic flops of one step (padding and never-stored logits excluded)."""
+    """Flops one step computes (padding and never-stored logits excluded).
+    With fp32 weights the products of the previous word's embedding with the
+    first GRU's input weights (2 E 3H per row) and the readout's word weights
+    (2 E E) are rows of per-word tables built with the model, gathered rather
+    than computed, so they are not counted there."""
     E, H, A, C, V = cfg.E, cfg.H, cfg.A, cfg.C, cfg.V
     L = src_len[sent_id].astype(np.float64)
-    per_row = (2 * (E + H) * 3 * H          # first GRU
+    xe = 0 if cfg.wtype == "f32" else E     # the embedding's share of K in the step
+    per_row = (2 * (xe + H) * 3 * H         # first GRU
                + 2 * H * A                  # attention query
                + 2 * (H + C) * 3 * H        # second GRU
-               + 2 * (H + E + C) * E        # readout
+               + 2 * (H + xe + C) * E       # readout
                + 2 * E * V)                 # vocabulary projection
     attention = float(np.sum(3 * L * A + 2 * L * C))
     vocab = 2.0 * E * V * len(sent_id)

@@ -89,6 +89,17 @@ struct nmt_model {
   Allocs mem;
   void *emb_src = nullptr, *emb_tgt = nullptr;
   Packed enc_in, enc_U[2], att_Wc, init_W, g1, att_Wq, g2, ro, out;
+  // fp32 weights: the two products of the previous word's embedding (the
+  // first GRU's input side and the readout's word term) are per-word tables
+  // [V x 3H] and [V x E], built from the embedding table and the packed
+  // weights g1x and roy when the model is created (or averaged); a step
+  // gathers their rows, and g1 and ro hold only the other weights.  bf16
+  // weights keep the products in the step: a table row in fp32 is 12x the
+  // bytes of the bf16 embedding row it replaces, and their GEMMs were
+  // bound by memory traffic, not by the products.
+  bool tables = false;
+  Packed g1x, roy;
+  float *tab_x = nullptr, *tab_y = nullptr;
   float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr;
   GruBias enc_bias, g1_bias, g2_bias;
   int* err = nullptr;  // sticky device error flag
@@ -267,6 +278,23 @@ AOperand make_a(int M, std::initializer_list<ASeg> segs) {
   return a;
 }
 
+// The model's per-word tables: tab_x = E_tgt . W_x (the first GRU's input
+// side, gates [r | z | n]) and tab_y = E_tgt . W_y (the readout's word term),
+// one row per target word, computed with the model's GEMM in its precision
+// (fp32 sums).  Allocates both tables (kept with the model's other buffers).
+hipError_t word_tables(nmt_model* m, hipStream_t st) {
+  const nmt_dims& d = m->dims;
+  const int V = d.V, E = d.E, H = d.H;
+  hipError_t e = m->mem.alloc((void**)&m->tab_x, (size_t)V * 3 * H * 4);
+  if (e == hipSuccess) e = m->mem.alloc((void**)&m->tab_y, (size_t)V * E * 4);
+  const AOperand A = make_a(V, {emb_seg(m, m->emb_tgt, nullptr, V)});
+  if (e == hipSuccess)
+    e = launch_gemm_plain(Tile::Large, A, m->g1x, PlainEpi{m->tab_x, 3 * H, nullptr, 3 * H, 0, nullptr, 1}, st);
+  if (e == hipSuccess)
+    e = launch_gemm_plain(Tile::Large, A, m->roy, PlainEpi{m->tab_y, E, nullptr, E, 0, nullptr, 1}, st);
+  return e;
+}
+
 nmt_status check_device(const nmt_model* m) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return fail(NMT_EDEVICE, "hipGetDevice failed");
@@ -329,7 +357,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   const int tiles_q = ceil_div(B, kPlainSmallTM) * ceil_div(d.A, kPlainSmallTN);
   L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->cus) : 1;
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + d.E + 2 * d.H, m->kc, Tile::Small, m->cus);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + (m->tables ? 0 : d.E) + 2 * d.H, m->kc, Tile::Small, m->cus);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
@@ -344,9 +372,10 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al(4);
   L.zreq = off;  // the requested words' logits
   off += al((size_t)B * 4);
-  // the GRUs' K splits: GRU1 reads [x | s_prev], GRU2 [s1 | c]
+  // the GRUs' K splits: GRU1 reads [x | s_prev] (s_prev alone where its
+  // input side comes from a table), GRU2 [s1 | c]
   const int kc = m->kc;
-  const int kx = m->bf16 ? (int)m->emb_ld : d.E;
+  const int kx = m->tables ? 0 : m->bf16 ? (int)m->emb_ld : d.E;
   L.ks_g1 = gru_ksplit((int)B, d.H, ceil_div(kx, kc) + ceil_div(d.H, kc), m->bf16, m->cus);
   L.ks_g2 = gru_ksplit((int)B, d.H, ceil_div(d.H, kc) + ceil_div(2 * d.H, kc), m->bf16, m->cus);
   const int ks_g = L.ks_g1 > L.ks_g2 ? L.ks_g1 : L.ks_g2;
@@ -548,14 +577,24 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   step(upload(m->mem, &m->att_b, w->att_b, A));
   if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->init_b, w->init_b, H));
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_W, E, 3 * H}, {w->g1_U, H, 3 * H}}, H, kc, bf16));
+  m->tables = !bf16;
+  if (m->tables) {
+    if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_U, H, 3 * H}}, H, kc, bf16));
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->g1x, {{w->g1_W, E, 3 * H}}, 3 * H, kPlainLargeTN, kc, bf16));
+  } else if (e == hipSuccess) {
+    step(pack_gru(m->mem, &m->g1, {{w->g1_W, E, 3 * H}, {w->g1_U, H, 3 * H}}, H, kc, bf16));
+  }
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g1_bias, w->g1_b, nullptr, H));
   if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wq, {{w->att_Wq, H, A}}, A, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->att_v, w->att_v, A));
   if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H, kc, bf16));
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g2_bias, nullptr, w->g2_b, H));
-  if (e == hipSuccess)
+  if (m->tables) {
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->roy, {{w->ro_Wy, E, E}}, E, kPlainLargeTN, kc, bf16));
+  } else if (e == hipSuccess) {
     step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
+  }
   step(upload(m->mem, &m->ro_b, w->ro_b, E));
   if (e == hipSuccess) {
     // output weights with the bias as extra rows (see vocab_bias_rows)
@@ -577,6 +616,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
     m->out.Krows = E;
     m->out.nbias = nb;
   }
+  if (e == hipSuccess && m->tables) step(word_tables(m, nullptr));
   step(m->mem.alloc((void**)&m->err, sizeof(int)));
   if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
   if (e == hipSuccess) step(noalloc_scratch(m->device, &m->noalloc_ws));
@@ -771,7 +811,6 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   };
   float* t = (float*)(ws + L.t);
   float2* part = (float2*)(ws + L.part);
-  const ASeg x_seg = emb_seg(m, m->emb_tgt, d_y_prev, V);  // E_i: embedding rows of the previous words
   ASeg h_seg = make_seg(pool, H, H, 1, m->kc);             // H_{i-1}: input states, gathered by row
   h_seg.gather = state_row;
   h_seg.gmax = pool_rows;
@@ -783,14 +822,24 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   };
   mark(0);
 
-  // first GRU: s1 = GRU(x, s_prev)
+  // first GRU: s1 = GRU(x, s_prev), x = E_i the embeddings of the previous
+  // words (ids outside the vocabulary, and -1, read zeros), or with the
+  // model's tables their products with the input-side weights, rows y_prev
+  // of the table
+  const ASeg x_seg = emb_seg(m, m->emb_tgt, d_y_prev, V);
   GruProblem g1;
-  g1.A = make_a(B, {x_seg, h_seg});
+  g1.A = m->tables ? make_a(B, {h_seg}) : make_a(B, {x_seg, h_seg});
   g1.Wp = m->g1.d;
   g1.Npad = m->g1.Npad;
   g1.ep = GruEpi{pool, H, state_row, pool_rows, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns,
                  s1, H, nullptr, 0, H};
   g1.ep.out16 = s1h;
+  if (m->tables) {
+    g1.ep.xin = m->tab_x;
+    g1.ep.ldx = 3 * H;
+    g1.ep.xrow = d_y_prev;
+    g1.ep.xrows = V;
+  }
   float* gpart = (float*)(ws + L.gpart);
   auto run_gru = [&](const GruProblem& g, int ks) {
     // (the test switch's forced streaming skips the K split, which the
@@ -832,15 +881,24 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     e = run_gru(g2, L.ks_g2);
   }
   mark(NMT_PHASE_GRU2 + 1);
-  // readout t = tanh(s_new Ws + x Wy + c Wc + b)
+  // readout t = tanh(s_new Ws + x Wy + c Wc + b), with the model's tables
+  // the word term x Wy from a table like the first GRU's input side
   if (e == hipSuccess) {
     PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
+    if (m->tables) {
+      ep.add = m->tab_y;
+      ep.ld_add = E;
+      ep.add_row = d_y_prev;
+      ep.add_rows = V;
+    }
     if (m->bf16) {  // the vocabulary and combine kernels stage t in bf16 anyway
       ep.out16 = (__bf16*)t;
       ep.ldo = bf16_row(E);
     }
     e = launch_gemm_plain(Tile::Small,
-                          make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}), m->ro,
+                          m->tables ? make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), c_seg})
+                                    : make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}),
+                          m->ro,
                           ep, st, m->cus);
   }
   mark(NMT_PHASE_READOUT + 1);
@@ -935,6 +993,8 @@ static std::vector<void**> param_fields(nmt_model* m) {
   for (Packed* P : {&m->enc_in, &m->enc_U[0], &m->enc_U[1], &m->att_Wc, &m->init_W, &m->g1, &m->att_Wq, &m->g2,
                     &m->ro, &m->out})
     f.push_back(&P->d);
+  if (m->tables)
+    for (Packed* P : {&m->g1x, &m->roy}) f.push_back(&P->d);
   for (float** b : {&m->enc_in_b, &m->att_b, &m->init_b, &m->att_v, &m->ro_b}) f.push_back((void**)b);
   for (GruBias* g : {&m->enc_bias, &m->g1_bias, &m->g2_bias}) {
     f.push_back((void**)&g->brz);
@@ -1010,7 +1070,10 @@ nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h
       delete a;
       return fail(NMT_EDEVICE, "nmt_model_average: parameter table does not match the model's buffers");
     }
-    e = a->mem.alloc((void**)&a->err, sizeof(int));
+    // the tables are products of the weights, not averaged: rebuilt from the averages
+    a->tab_x = a->tab_y = nullptr;
+    if (a->tables) e = word_tables(a, st);
+    if (e == hipSuccess) e = a->mem.alloc((void**)&a->err, sizeof(int));
   }
   if (e == hipSuccess) e = hipMemsetAsync(a->err, 0, sizeof(int), st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);

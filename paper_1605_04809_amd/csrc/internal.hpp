@@ -93,6 +93,12 @@ struct PlainEpi {
   float* part = nullptr;
   __bf16* out16 = nullptr;  // nullable: the output goes here in bf16 (nearest even) instead of to out
   int32_t defer_reduce = 0;  // ksplit > 1: leave the raw sums in part for the consumer to add (no epilogue)
+  // nullable: row m's sums also get row add_row[m] of `add` (row stride
+  // ld_add; rows outside [0, add_rows) add nothing), before bias and activation
+  const float* add = nullptr;
+  int64_t ld_add = 0;
+  const int32_t* add_row = nullptr;
+  int32_t add_rows = 0;
 };
 
 // Epilogue of the GRU gate GEMM (see device.hpp for the cell).
@@ -112,6 +118,10 @@ struct GruEpi {
   int32_t mask_pos;
   int32_t H;
   __bf16* out16 = nullptr;  // nullable: a bf16 copy of out (nearest even), row stride ldo
+  // nullable: row m's input-side pre-activations are row xrow[m] of xin
+  // (rows outside [0, xrows): zeros)
+  const int32_t* xrow = nullptr;
+  int32_t xrows = 0;
 };
 
 struct GruProblem {

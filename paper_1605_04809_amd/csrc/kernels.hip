@@ -33,6 +33,20 @@ namespace nmt {
 
 // ----------------------------------------------------------- plain GEMM
 
+// The row of a per-row table that batch row `row` reads: row itself without
+// an index, else idx[row], or -1 where that is outside [0, nrows).
+__device__ __forceinline__ int table_row(const int32_t* idx, int nrows, int row) {
+  if (!idx) return row;
+  const int r = idx[row];
+  return r >= 0 && r < nrows ? r : -1;
+}
+// PlainEpi::add's term for output (row, n).
+__device__ __forceinline__ float plain_add(const PlainEpi& ep, int row, int n) {
+  if (!ep.add) return 0.f;
+  const int r = table_row(ep.add_row, ep.add_rows, row);
+  return r >= 0 ? ep.add[(int64_t)r * ep.ld_add + n] : 0.f;
+}
+
 template <int TM, int TN, int WM, int WN, class P>
 __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOperand A, const f32x4* __restrict__ Wp,
                                                                            int64_t Npad, PlainEpi ep) {
@@ -104,7 +118,7 @@ __global__ __launch_bounds__((TM / WM) * (TN / WN) * 64) void k_gemm_plain(AOper
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm0 + 32 * i + acc_row(r, h);
         if (row >= A.M) continue;
-        float v = acc[i][j][r] + bn;
+        float v = acc[i][j][r] + plain_add(ep, row, n) + bn;
         if (ep.act == 1) v = tanhf_(v);
         if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
         if (ep.out16)
@@ -122,6 +136,7 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
   const int row = (int)(i / N), n = (int)(i % N);
   float v = 0.f;
   for (int z = 0; z < ksplit; ++z) v += part[(int64_t)z * M * N + i];
+  v += plain_add(ep, row, n);
   v += ep.bias ? ep.bias[n] : 0.f;
   if (ep.act == 1) v = tanhf_(v);
   if (ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T]) v = 0.f;
@@ -327,13 +342,19 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
       for (int q = 0; q < NG; ++q) hp[q] = hok[q] ? hp[q] : 0.f;
     }
     if (ep.xin) {
+      int xq[NG];
+#pragma unroll
+      for (int q = 0; q < NG; ++q) xq[q] = table_row(ep.xrow, ep.xrows, clamp_row(rowq[q]));
 #pragma unroll
       for (int q = 0; q < NG; ++q) {
-        const float* x = ep.xin + (int64_t)clamp_row(rowq[q]) * ep.ldx;
+        const float* x = ep.xin + (int64_t)(xq[q] >= 0 ? xq[q] : 0) * ep.ldx;
         xr[q] = x[j];
         xz[q] = x[H + j];
         xn[q] = x[2 * H + j];
       }
+#pragma unroll
+      for (int q = 0; q < NG; ++q)
+        if (xq[q] < 0) xr[q] = xz[q] = xn[q] = 0.f;
     }
     if (ep.mask_len) {
 #pragma unroll
@@ -436,8 +457,9 @@ __global__ void k_gru_cell(GruBatch batch, int H) {
     const int hr = ep.hrow ? ep.hrow[row] : row;
     if (!ep.hrow || (hr >= 0 && hr < ep.hrows)) hp = ep.h[(int64_t)hr * ep.ldh + j];
   }
-  if (ep.xin) {
-    const float* x = ep.xin + (int64_t)row * ep.ldx;
+  const int xq = ep.xin ? table_row(ep.xrow, ep.xrows, row) : -1;
+  if (xq >= 0) {
+    const float* x = ep.xin + (int64_t)xq * ep.ldx;
     xr = x[j];
     xz = x[H + j];
     xn = x[2 * H + j];
@@ -719,7 +741,7 @@ static bool try_gru_ws(const GruProblem& p, int H, bool bf16, int cus, hipStream
   if (form == 2) return false;
   // H a multiple of the block's 128 units: every wave's packed columns then
   // lie inside the matrix's rows, so no weight load leaves the matrix
-  if (!bf16 || H % kWsUB || p.A.M <= 0 || p.A.nseg != 2) return false;
+  if (!bf16 || H % kWsUB || p.A.M <= 0 || p.A.nseg != 2 || p.ep.xrow) return false;
   const ASeg &s0 = p.A.seg[0], &s1 = p.A.seg[1];
   if (s0.nchunk % 2 || s1.nchunk % 2 || s0.side == s1.side) return false;
   // the epilogue's vector accesses: 16-byte aligned rows of the state,
@@ -969,7 +991,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 static bool try_plain_ws(const AOperand& A, const Packed& W, const PlainEpi& ep, int cus, hipStream_t st) {
   const int form = g_gemm_form.load(std::memory_order_relaxed);
   if (form == 2 || !W.bf16 || cus <= 0 || A.M <= 0 || A.nseg < 1 || A.nseg > 3 || ep.N % 4) return false;
-  if (ep.defer_reduce) return false;  // the caller reads the split sums
+  if (ep.defer_reduce || ep.add) return false;  // the caller reads the split sums; no table terms here
   for (int i = 0; i < A.nseg; ++i)
     if (A.seg[i].nchunk % 2 || (i > 0 && !A.seg[i].bf16)) return false;
   // the epilogue's vector accesses: 16-byte aligned fp32 rows and bias,
