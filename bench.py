@@ -63,17 +63,22 @@ def step_flops(cfg, src_len, sent_id):
     """Flops one step computes (padding and never-stored logits excluded).
     With fp32 weights the products of the previous word's embedding with the
     first GRU's input weights (2 E 3H per row) and the readout's word weights
-    (2 E E) are rows of per-word tables built with the model, gathered rather
-    than computed, so they are not counted there."""
+    (2 E E) are rows of per-word tables built with the model, and the
+    products of the context with the second GRU's input weights (2 C 3H) and
+    the readout's context weights (2 C E) are mixed by the attention from
+    per-position projections of the annotations (2 L (3H + E) per row instead
+    of the context's 2 L C): only what the step computes is counted."""
     E, H, A, C, V = cfg.E, cfg.H, cfg.A, cfg.C, cfg.V
     L = src_len[sent_id].astype(np.float64)
-    xe = 0 if cfg.wtype == "f32" else E     # the embedding's share of K in the step
+    pre = cfg.wtype == "f32"
+    xe, xc = (0, 0) if pre else (E, C)      # the embedding's and the context's shares of K in the step
     per_row = (2 * (xe + H) * 3 * H         # first GRU
                + 2 * H * A                  # attention query
-               + 2 * (H + C) * 3 * H        # second GRU
-               + 2 * (H + xe + C) * E       # readout
+               + 2 * (H + xc) * 3 * H       # second GRU
+               + 2 * (H + xe + xc) * E      # readout
                + 2 * E * V)                 # vocabulary projection
-    attention = float(np.sum(3 * L * A + 2 * L * C))
+    mixed = 3 * H + E if pre else C         # columns the attention mixes per position
+    attention = float(np.sum(3 * L * A + 2 * L * mixed))
     vocab = 2.0 * E * V * len(sent_id)
     return per_row * len(sent_id) + attention, vocab
 

@@ -89,16 +89,20 @@ struct nmt_model {
   Allocs mem;
   void *emb_src = nullptr, *emb_tgt = nullptr;
   Packed enc_in, enc_U[2], att_Wc, init_W, g1, att_Wq, g2, ro, out;
-  // fp32 weights: the two products of the previous word's embedding (the
-  // first GRU's input side and the readout's word term) are per-word tables
-  // [V x 3H] and [V x E], built from the embedding table and the packed
-  // weights g1x and roy when the model is created (or averaged); a step
-  // gathers their rows, and g1 and ro hold only the other weights.  bf16
-  // weights keep the products in the step: a table row in fp32 is 12x the
-  // bytes of the bf16 embedding row it replaces, and their GEMMs were
-  // bound by memory traffic, not by the products.
-  bool tables = false;
-  Packed g1x, roy;
+  // precomp (fp32 weights): the products of the previous word's embedding
+  // (the first GRU's input side and the readout's word term) are per-word
+  // tables [V x 3H] and [V x E], built from the embedding table and the
+  // packed weights g1x and roy when the model is created (or averaged), and
+  // the products of the context (the second GRU's input side and the
+  // readout's context term) are mixed by the attention from per-position
+  // projections of the annotations, [S x Tpad x cpw_ld], made with cpw when
+  // a source is set up; g1, g2 and ro then hold only the state-side
+  // weights.  bf16 weights keep all these products in the step: their GEMMs
+  // are bound by memory traffic, which fp32 table rows and projections
+  // would raise.
+  bool precomp = false;
+  Packed g1x, roy, cpw;
+  int cpw_ld = 0;  // columns of a projection row: 3H + E, padded to the large tile
   float *tab_x = nullptr, *tab_y = nullptr;
   float *enc_in_b = nullptr, *att_b = nullptr, *init_b = nullptr, *att_v = nullptr, *ro_b = nullptr;
   GruBias enc_bias, g1_bias, g2_bias;
@@ -115,6 +119,10 @@ struct nmt_source {
   Allocs mem;
   float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
   float* kfac = nullptr;  // 2^{2 log2(e) pctx}: the keys' factors of the attention scores
+  // precomp models: per position, the annotation times the second GRU's
+  // input-side weights [r | z | n] and the readout's context weights, then
+  // zeros to cpw_ld columns
+  float* cproj = nullptr;
   int32_t* kbig = nullptr;  // [S] 1 where a sentence has keys too large for their factors
   float* gru_part = nullptr;  // encoder: the recurrent GRU's split-K sums [2][enc_ks][S][4H]
   int enc_ks = 1;
@@ -342,8 +350,8 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   // bf16 weights: a bf16 copy of s1 for the GEMMs that read it
   L.s1h = off;
   off += m->bf16 ? al((size_t)B * d.H * 2) : 0;
-  L.c = off;
-  off += al((size_t)B * 2 * d.H * 4);
+  L.c = off;  // the context, or (precomp) its products [B x cpw_ld]
+  off += al((size_t)B * (m->precomp ? m->cpw_ld : 2 * d.H) * 4);
   L.q = off;
   off += al((size_t)B * d.A * 4);
   L.t = off;
@@ -357,7 +365,7 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   const int tiles_q = ceil_div(B, kPlainSmallTM) * ceil_div(d.A, kPlainSmallTN);
   L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->cus) : 1;
 
-  L.ks_ro = plain_ksplit((int)B, d.E, d.H + (m->tables ? 0 : d.E) + 2 * d.H, m->kc, Tile::Small, m->cus);
+  L.ks_ro = plain_ksplit((int)B, d.E, d.H + (m->precomp ? 0 : d.E + 2 * d.H), m->kc, Tile::Small, m->cus);
   size_t kp = 0;
   if (L.ks_q > 1) kp = (size_t)L.ks_q * B * d.A;
   if (L.ks_ro > 1 && (size_t)L.ks_ro * B * d.E > kp) kp = (size_t)L.ks_ro * B * d.E;
@@ -372,12 +380,12 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al(4);
   L.zreq = off;  // the requested words' logits
   off += al((size_t)B * 4);
-  // the GRUs' K splits: GRU1 reads [x | s_prev] (s_prev alone where its
-  // input side comes from a table), GRU2 [s1 | c]
+  // the GRUs' K splits: GRU1 reads [x | s_prev], GRU2 [s1 | c] (precomp:
+  // s_prev and s1 alone, their input sides added by the cells)
   const int kc = m->kc;
-  const int kx = m->tables ? 0 : m->bf16 ? (int)m->emb_ld : d.E;
+  const int kx = m->precomp ? 0 : m->bf16 ? (int)m->emb_ld : d.E;
   L.ks_g1 = gru_ksplit((int)B, d.H, ceil_div(kx, kc) + ceil_div(d.H, kc), m->bf16, m->cus);
-  L.ks_g2 = gru_ksplit((int)B, d.H, ceil_div(d.H, kc) + ceil_div(2 * d.H, kc), m->bf16, m->cus);
+  L.ks_g2 = gru_ksplit((int)B, d.H, ceil_div(d.H, kc) + (m->precomp ? 0 : ceil_div(2 * d.H, kc)), m->bf16, m->cus);
   const int ks_g = L.ks_g1 > L.ks_g2 ? L.ks_g1 : L.ks_g2;
   L.gpart = L.q;
   if (ks_g > 1) {
@@ -416,6 +424,7 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   hipError_t e = src->mem.alloc((void**)&src->ctx, rows * 2 * d.H * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->pctx, rows * d.A * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->kfac, rows * d.A * sizeof(float));
+  if (e == hipSuccess && m->precomp) e = src->mem.alloc((void**)&src->cproj, rows * m->cpw_ld * sizeof(float));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->len, S * sizeof(int32_t));
   if (e == hipSuccess) e = src->mem.alloc((void**)&src->kbig, S * sizeof(int32_t));
   if (e == hipSuccess && with_scratch) e = src->mem.alloc((void**)&src->scratch, rows * 6 * d.H * sizeof(float));
@@ -444,6 +453,11 @@ hipError_t source_keys(nmt_model* m, nmt_source* src, hipStream_t st) {
   PlainEpi ep{src->pctx, d.A, m->att_b, d.A, 0, src->len, src->Tpad};
   hipError_t e = launch_gemm_plain(Tile::Large, A, m->att_Wc, ep, st);
   if (e == hipSuccess) e = launch_key_factors(src->S, src->Tpad, d.A, src->pctx, src->kfac, src->kbig, st);
+  if (e == hipSuccess && m->precomp) {
+    // the context's products, projected per position (zeros past the length)
+    PlainEpi pe{src->cproj, m->cpw_ld, nullptr, m->cpw_ld, 0, src->len, src->Tpad};
+    e = launch_gemm_plain(Tile::Large, A, m->cpw, pe, st);
+  }
   return e;
 }
 
@@ -577,8 +591,8 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   step(upload(m->mem, &m->att_b, w->att_b, A));
   if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->init_b, w->init_b, H));
-  m->tables = !bf16;
-  if (m->tables) {
+  m->precomp = !bf16;
+  if (m->precomp) {
     if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_U, H, 3 * H}}, H, kc, bf16));
     if (e == hipSuccess) step(pack_plain(m->mem, &m->g1x, {{w->g1_W, E, 3 * H}}, 3 * H, kPlainLargeTN, kc, bf16));
   } else if (e == hipSuccess) {
@@ -587,10 +601,22 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g1_bias, w->g1_b, nullptr, H));
   if (e == hipSuccess) step(pack_plain(m->mem, &m->att_Wq, {{w->att_Wq, H, A}}, A, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->att_v, w->att_v, A));
-  if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H, kc, bf16));
+  if (m->precomp) {
+    if (e == hipSuccess) step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}}, H, kc, bf16));
+    // [g2_Wc | ro_Wc]: C x (3H + E)
+    std::vector<float> cw((size_t)C * (3 * H + E));
+    for (int k = 0; k < C; ++k) {
+      memcpy(&cw[(size_t)k * (3 * H + E)], w->g2_Wc + (size_t)k * 3 * H, sizeof(float) * 3 * H);
+      memcpy(&cw[(size_t)k * (3 * H + E) + 3 * H], w->ro_Wc + (size_t)k * E, sizeof(float) * E);
+    }
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->cpw, {{cw.data(), C, 3 * H + E}}, 3 * H + E, kPlainLargeTN, kc, bf16));
+    m->cpw_ld = (int)m->cpw.Npad;
+  } else if (e == hipSuccess) {
+    step(pack_gru(m->mem, &m->g2, {{w->g2_U, H, 3 * H}, {w->g2_Wc, C, 3 * H}}, H, kc, bf16));
+  }
   if (e == hipSuccess) step(upload_gru_bias(m->mem, &m->g2_bias, nullptr, w->g2_b, H));
-  if (m->tables) {
-    if (e == hipSuccess) step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
+  if (m->precomp) {
+    if (e == hipSuccess) step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}}, E, kPlainSmallTN, kc, bf16));
     if (e == hipSuccess) step(pack_plain(m->mem, &m->roy, {{w->ro_Wy, E, E}}, E, kPlainLargeTN, kc, bf16));
   } else if (e == hipSuccess) {
     step(pack_plain(m->mem, &m->ro, {{w->ro_Ws, H, E}, {w->ro_Wy, E, E}, {w->ro_Wc, C, E}}, E, kPlainSmallTN, kc, bf16));
@@ -616,7 +642,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
     m->out.Krows = E;
     m->out.nbias = nb;
   }
-  if (e == hipSuccess && m->tables) step(word_tables(m, nullptr));
+  if (e == hipSuccess && m->precomp) step(word_tables(m, nullptr));
   step(m->mem.alloc((void**)&m->err, sizeof(int)));
   if (e == hipSuccess) step(hipMemset(m->err, 0, sizeof(int)));
   if (e == hipSuccess) step(noalloc_scratch(m->device, &m->noalloc_ws));
@@ -828,13 +854,13 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // of the table
   const ASeg x_seg = emb_seg(m, m->emb_tgt, d_y_prev, V);
   GruProblem g1;
-  g1.A = m->tables ? make_a(B, {h_seg}) : make_a(B, {x_seg, h_seg});
+  g1.A = m->precomp ? make_a(B, {h_seg}) : make_a(B, {x_seg, h_seg});
   g1.Wp = m->g1.d;
   g1.Npad = m->g1.Npad;
   g1.ep = GruEpi{pool, H, state_row, pool_rows, nullptr, 0, m->g1_bias.brz, m->g1_bias.bni, m->g1_bias.bns,
                  s1, H, nullptr, 0, H};
   g1.ep.out16 = s1h;
-  if (m->tables) {
+  if (m->precomp) {
     g1.ep.xin = m->tab_x;
     g1.ep.ldx = 3 * H;
     g1.ep.xrow = d_y_prev;
@@ -866,18 +892,34 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
     // (a forest's levels come with their grouping done, all in one launch)
     const AttnGroups grp =
         pre_grp ? *pre_grp : AttnGroups{(int32_t*)(ws + L.perm), (int4*)(ws + L.tiles), (int32_t*)(ws + L.ntiles)};
-    e = launch_attention(B, Aw, C, src->Tpad, qsrc, src->kfac, src->pctx, src->kbig, src->ctx, src->len, d_sent_id,
-                         src->S, m->att_v, c, d_alpha, grp, c16, m->cus, st, pre_grp != nullptr);
+    auto attend = [&](const float* X, int width, float* out, float* alpha_out, bool out16) {
+      return launch_attention(B, Aw, width, src->Tpad, qsrc, src->kfac, src->pctx, src->kbig, X, src->len, d_sent_id,
+                              src->S, m->att_v, out, alpha_out, grp, out16, m->cus, st, pre_grp != nullptr);
+    };
+    // precomp: the attention mixes the annotations' projections, giving the
+    // context's products with the second GRU's and the readout's weights;
+    // the context itself only for the debug output (the same weights over
+    // the annotations, while the query is still in place)
+    if (m->precomp) {
+      e = attend(src->cproj, m->cpw_ld, c, d_alpha, false);
+      if (e == hipSuccess && d_c) e = attend(src->ctx, C, d_c, nullptr, false);
+    } else {
+      e = attend(src->ctx, C, c, d_alpha, c16);
+    }
   }
   mark(NMT_PHASE_ATTENTION + 1);
-  // second GRU: s_new = GRU(c, s1)
+  // second GRU: s_new = GRU(c, s1) (precomp: its input side c W_c from the attention)
   if (e == hipSuccess) {
     GruProblem g2;
-    g2.A = make_a(B, {state_seg(s1, s1h, 1), c_seg});
+    g2.A = m->precomp ? make_a(B, {state_seg(s1, s1h, 1)}) : make_a(B, {state_seg(s1, s1h, 1), c_seg});
     g2.Wp = m->g2.d;
     g2.Npad = m->g2.Npad;
     g2.ep = GruEpi{s1, H, nullptr, 0, nullptr, 0, m->g2_bias.brz, m->g2_bias.bni, m->g2_bias.bns, d_s_new, H,
                    nullptr, 0, H};
+    if (m->precomp) {
+      g2.ep.xin = c;
+      g2.ep.ldx = m->cpw_ld;
+    }
     e = run_gru(g2, L.ks_g2);
   }
   mark(NMT_PHASE_GRU2 + 1);
@@ -885,19 +927,21 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // the word term x Wy from a table like the first GRU's input side
   if (e == hipSuccess) {
     PlainEpi ep{t, E, m->ro_b, E, 1, nullptr, 1, L.ks_ro, (float*)(ws + L.kpart)};
-    if (m->tables) {
+    if (m->precomp) {  // the word term from its table, the context term from the attention
       ep.add = m->tab_y;
       ep.ld_add = E;
       ep.add_row = d_y_prev;
       ep.add_rows = V;
+      ep.add2 = c + 3 * H;
+      ep.ld_add2 = m->cpw_ld;
     }
     if (m->bf16) {  // the vocabulary and combine kernels stage t in bf16 anyway
       ep.out16 = (__bf16*)t;
       ep.ldo = bf16_row(E);
     }
     e = launch_gemm_plain(Tile::Small,
-                          m->tables ? make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), c_seg})
-                                    : make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}),
+                          m->precomp ? make_a(B, {make_seg(d_s_new, H, H, 0, m->kc)})
+                                     : make_a(B, {make_seg(d_s_new, H, H, 0, m->kc), x_seg, c_seg}),
                           m->ro,
                           ep, st, m->cus);
   }
@@ -913,7 +957,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
                            m->err, zreq, st);
   mark(NMT_PHASE_COMBINE + 1);
   if (e == hipSuccess && d_s1) e = hipMemcpyAsync(d_s1, s1, (size_t)B * H * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess && d_c)
+  if (e == hipSuccess && d_c && !m->precomp)
     e = c16 ? launch_bf16_to_f32(c, B, C, C, d_c, st)
             : hipMemcpyAsync(d_c, c, (size_t)B * C * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess && d_t)
@@ -993,8 +1037,8 @@ static std::vector<void**> param_fields(nmt_model* m) {
   for (Packed* P : {&m->enc_in, &m->enc_U[0], &m->enc_U[1], &m->att_Wc, &m->init_W, &m->g1, &m->att_Wq, &m->g2,
                     &m->ro, &m->out})
     f.push_back(&P->d);
-  if (m->tables)
-    for (Packed* P : {&m->g1x, &m->roy}) f.push_back(&P->d);
+  if (m->precomp)
+    for (Packed* P : {&m->g1x, &m->roy, &m->cpw}) f.push_back(&P->d);
   for (float** b : {&m->enc_in_b, &m->att_b, &m->init_b, &m->att_v, &m->ro_b}) f.push_back((void**)b);
   for (GruBias* g : {&m->enc_bias, &m->g1_bias, &m->g2_bias}) {
     f.push_back((void**)&g->brz);
@@ -1072,7 +1116,7 @@ nmt_status nmt_model_average(int32_t K, nmt_model* const* models, const float* h
     }
     // the tables are products of the weights, not averaged: rebuilt from the averages
     a->tab_x = a->tab_y = nullptr;
-    if (a->tables) e = word_tables(a, st);
+    if (a->precomp) e = word_tables(a, st);
     if (e == hipSuccess) e = a->mem.alloc((void**)&a->err, sizeof(int));
   }
   if (e == hipSuccess) e = hipMemsetAsync(a->err, 0, sizeof(int), st);

@@ -99,6 +99,9 @@ struct PlainEpi {
   int64_t ld_add = 0;
   const int32_t* add_row = nullptr;
   int32_t add_rows = 0;
+  // nullable: row m's sums also get row m of add2 (row stride ld_add2)
+  const float* add2 = nullptr;
+  int64_t ld_add2 = 0;
 };
 
 // Epilogue of the GRU gate GEMM (see device.hpp for the cell).

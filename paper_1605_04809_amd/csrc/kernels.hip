@@ -40,11 +40,15 @@ __device__ __forceinline__ int table_row(const int32_t* idx, int nrows, int row)
   const int r = idx[row];
   return r >= 0 && r < nrows ? r : -1;
 }
-// PlainEpi::add's term for output (row, n).
+// PlainEpi's added terms for output (row, n): add's gathered row, then add2's.
 __device__ __forceinline__ float plain_add(const PlainEpi& ep, int row, int n) {
-  if (!ep.add) return 0.f;
-  const int r = table_row(ep.add_row, ep.add_rows, row);
-  return r >= 0 ? ep.add[(int64_t)r * ep.ld_add + n] : 0.f;
+  float v = 0.f;
+  if (ep.add) {
+    const int r = table_row(ep.add_row, ep.add_rows, row);
+    v = r >= 0 ? ep.add[(int64_t)r * ep.ld_add + n] : 0.f;
+  }
+  if (ep.add2) v += ep.add2[(int64_t)row * ep.ld_add2 + n];
+  return v;
 }
 
 template <int TM, int TN, int WM, int WN, class P>
@@ -991,7 +995,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void k
 static bool try_plain_ws(const AOperand& A, const Packed& W, const PlainEpi& ep, int cus, hipStream_t st) {
   const int form = g_gemm_form.load(std::memory_order_relaxed);
   if (form == 2 || !W.bf16 || cus <= 0 || A.M <= 0 || A.nseg < 1 || A.nseg > 3 || ep.N % 4) return false;
-  if (ep.defer_reduce || ep.add) return false;  // the caller reads the split sums; no table terms here
+  if (ep.defer_reduce || ep.add || ep.add2) return false;  // the caller reads the split sums; no added terms here
   for (int i = 0; i < A.nseg; ++i)
     if (A.seg[i].nchunk % 2 || (i > 0 && !A.seg[i].bf16)) return false;
   // the epilogue's vector accesses: 16-byte aligned fp32 rows and bias,
