@@ -150,6 +150,44 @@ __global__ void k_splitk_reduce(int M, int N, int ksplit, const float* __restric
     ep.out[(int64_t)row * ep.ldo + n] = v;
 }
 
+// The same for four consecutive columns per thread (N, the row strides and
+// the arrays' alignment allowing 16-byte accesses).
+__global__ void k_splitk_reduce4(int M, int N, int ksplit, const float* __restrict__ part, PlainEpi ep) {
+  const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, n4 = N / 4;
+  if (i4 >= (int64_t)M * n4) return;
+  const int row = (int)(i4 / n4), n = 4 * (int)(i4 % n4);
+  const int64_t i = (int64_t)row * N + n;
+  f32x4 v = zero4();
+  for (int z = 0; z < ksplit; ++z) v += *(const f32x4*)(part + (int64_t)z * M * N + i);
+  f32x4 t = zero4();  // the added terms, summed as plain_add sums them
+  if (ep.add) {
+    const int r = table_row(ep.add_row, ep.add_rows, row);
+    if (r >= 0) t = *(const f32x4*)(ep.add + (int64_t)r * ep.ld_add + n);
+  }
+  if (ep.add2) t += *(const f32x4*)(ep.add2 + (int64_t)row * ep.ld_add2 + n);
+  v += t;
+  if (ep.bias) v += *(const f32x4*)(ep.bias + n);
+  const bool masked = ep.mask_len && (row % ep.mask_T) >= ep.mask_len[row / ep.mask_T];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (ep.act == 1) v[e] = tanhf_(v[e]);
+    if (masked) v[e] = 0.f;
+  }
+  if (ep.out16) {
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    *(bf16x4_t*)(ep.out16 + (int64_t)row * ep.ldo + n) = bf16x4_t{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+  } else {
+    *(f32x4*)(ep.out + (int64_t)row * ep.ldo + n) = v;
+  }
+}
+
+static bool reduce4_fits(const PlainEpi& ep, const float* part) {
+  auto al = [](const void* p, int b) { return ((uintptr_t)p % b) == 0; };
+  return ep.N % 4 == 0 && ep.ldo % 4 == 0 && al(part, 16) && (ep.out16 ? al(ep.out16, 8) : al(ep.out, 16)) &&
+         (!ep.bias || al(ep.bias, 16)) && (!ep.add || (ep.ld_add % 4 == 0 && al(ep.add, 16))) &&
+         (!ep.add2 || (ep.ld_add2 % 4 == 0 && al(ep.add2, 16)));
+}
+
 template <int TM, int TN, int WM, int WN, class P>
 static void plain_tile(const AOperand& A, const f32x4* Wp, const Packed& W, const PlainEpi& ep, int ksplit,
                        hipStream_t st) {
@@ -170,7 +208,11 @@ hipError_t gemm_plain(Tile t, const AOperand& A, const Packed& W, const PlainEpi
     plain_tile<kPlainLargeTM, kPlainLargeTN, 64, 64, P>(A, Wp, W, ep, ks, st);
   if (ep.ksplit > 1 && !ep.defer_reduce) {
     const int64_t n = (int64_t)A.M * ep.N;
-    hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
+    if (reduce4_fits(ep, ep.part))
+      hipLaunchKernelGGL(k_splitk_reduce4, dim3(ceil_div(n / 4, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part,
+                         ep);
+    else
+      hipLaunchKernelGGL(k_splitk_reduce, dim3(ceil_div(n, 256)), dim3(256), 0, st, A.M, ep.N, ep.ksplit, ep.part, ep);
   }
   return hipGetLastError();
 }
@@ -240,7 +282,6 @@ __global__ __launch_bounds__((TM / WM) * (HB / 32) * 64) __attribute__((amdgpu_w
   f32x16 ar[FM], az[FM], ani[FM], ans[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) ar[i] = az[i] = ani[i] = ans[i] = f32x16{};
-
   auto chunk = [&](const f32x4* As, const f32x4* Bs, auto state_side) {
 #pragma unroll
     for (int kg = 0; kg < P::KQ / 2; ++kg) {
