@@ -588,6 +588,13 @@ def bench_workload(name, args, cpu_seconds, headline=False):
         "encode": {"ms": float(np.median(enc_ms)), "sentences": cfg.S,
                    "ms_per_sentence": float(np.median(enc_ms)) / cfg.S},
     }
+    if cfg.wtype == "f32":
+        res["precomputed"] = {
+            "per_model": "per-word tables Emb.W_x [V x 3H] and Emb.W_y [V x E], built once at model creation",
+            "per_source": "the annotations' projections ctx.[W_c(GRU2) | W_c(readout)] [S x Tpad x (3H+E)], built "
+                          "with the keys when the source is encoded (inside encode.ms)",
+            "step": "gathers the tables' rows by previous word and mixes the projections with the attention "
+                    "weights; step_tflops counts only what the step computes"}
     if graph:
         res["graph"] = graph
     if cfg.phrase_max:
