@@ -101,7 +101,11 @@ typedef struct {
 } nmt_weights;
 
 /* Copy the parameters to the current HIP device, re-laid-out for the
- * kernels.  The caller keeps ownership of the host arrays and may free them
+ * kernels.  With fp32 weights the model also holds two per-word tables, the
+ * target embeddings times the first GRU's input weights [V x 3H] and times
+ * the readout's word weights [V x E] (fp32, computed here: 1.4 GB at V =
+ * 100k, H = 1024, E = 500), which the step reads in place of those
+ * products.  The caller keeps ownership of the host arrays and may free them
  * on return.  Synchronous.  Errors: NMT_EINVAL (bad dims or null weight),
  * NMT_ENOMEM, NMT_EDEVICE. */
 nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out);
@@ -114,7 +118,11 @@ void nmt_model_destroy(nmt_model* m);
  * int32 in [0, V_src) for positions below each length (padding positions
  * are ignored); h_len [S] host int32 in [1, Tpad].  Computes the
  * annotations, the attention keys and, if d_s0_out is not NULL, the initial
- * decoder states d_s0_out [S x H].  The returned source owns its device
+ * decoder states d_s0_out [S x H]; with fp32 weights also each position's
+ * annotation times the second GRU's input weights and the readout's context
+ * weights [S x Tpad x (3H + E), padded to a multiple of 128], which the step
+ * mixes with the attention weights in place of those products of the
+ * context.  The returned source owns its device
  * buffers; it may be used by nmt_score_batch on any stream once the work
  * enqueued here has completed in stream order.  Out-of-range source ids set
  * the model's device error flag (see nmt_stream_status) and read as id 0.
@@ -124,7 +132,7 @@ nmt_status nmt_encode(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* d_sr
 
 /* A source built from given annotations d_ctx [S x Tpad x 2H] (fp32; values
  * past each length are ignored) instead of the encoder: only the attention
- * keys are computed.  For testing the decoder step in isolation. */
+ * keys (and, with fp32 weights, the annotations' projections) are computed.  For testing the decoder step in isolation. */
 nmt_status nmt_source_from_annotations(nmt_model* m, int32_t S, int32_t Tpad, const float* d_ctx,
                                        const int32_t* h_len, void* stream, nmt_source** out);
 
@@ -178,8 +186,8 @@ nmt_status nmt_score_batch_debug(nmt_model* m, const nmt_source* src, int32_t B,
 
 /* Size of the library's own scratch for nmt_score_batch_noalloc: 64 MiB per
  * device.  At the paper's dimensions (E = 500, H = A = 1024, V = 100k) that
- * holds the step of up to about 2,500 rows with fp32 weights and 2,700 with
- * bf16 weights. */
+ * holds the step of up to 2,304 rows with fp32 weights and 2,688 with bf16
+ * weights. */
 #define NMT_NOALLOC_SCRATCH_BYTES (64u << 20)
 
 /* nmt_score_batch for callers that cannot allocate device memory: code under
@@ -339,7 +347,8 @@ void nmt_rescorer_destroy(nmt_rescorer* r);
  * parameters are the element-wise average of the members'. */
 
 /* A new model whose every parameter is the weighted element-wise average
- * sum_k h_coef[k] * models[k] (h_coef NULL: 1/K each, as fp32).  The models
+ * sum_k h_coef[k] * models[k] (h_coef NULL: 1/K each, as fp32); an fp32
+ * model's per-word tables are computed anew from the averaged parameters.  The models
  * must have been created with identical nmt_dims on the current device.
  * Accumulation is fp32 in model order; results are stored in the models'
  * weight type (bf16 models keep every parameter, biases included, at a bf16
