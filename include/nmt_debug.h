@@ -5,7 +5,8 @@
  * every call that allocates reports NMT_ENOMEM and releases what it had
  * allocated when an allocation fails part-way, and choose which of the two
  * kernel forms the bf16 products of a step take, so that both are checked
- * at sizes the reference implementation finishes quickly.
+ * at sizes the reference implementation finishes quickly, and whether fp32
+ * models precompute the products of the previous word and of the context.
  */
 #ifndef NMT_DEBUG_H
 #define NMT_DEBUG_H
@@ -40,6 +41,15 @@ int32_t nmt_debug_gemm_form(int32_t form);
 /* How many launches of the process took a weight-streaming form (GRU or
  * plain product), so a test can tell which form ran. */
 int64_t nmt_debug_gemm_streamed(void);
+
+/* Whether fp32 models created from now on take the previous word's and the
+ * context's products from per-word tables and per-position projections
+ * (1, the default) or compute them in each step's GEMMs (0), so a test can
+ * compare the two on the same weights.  Models keep the form they were
+ * created with (an average takes its first member's).  Process-wide.
+ * Returns the previous setting, or -1 (and changes nothing) for a value
+ * other than 0 or 1. */
+int32_t nmt_debug_precompute(int32_t on);
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,7 @@ EXPORTS = ("nmt_model_create", "nmt_model_destroy", "nmt_encode", "nmt_source_fr
            "nmt_forest_level", "nmt_forest_pair_paths", "nmt_forest_workspace_bytes", "nmt_score_forest",
            "nmt_forest_destroy", "nmt_model_average", "nmt_ensemble_workspace_bytes", "nmt_score_ensemble",
            "nmt_rescorer_create", "nmt_rescore_stack", "nmt_rescorer_info", "nmt_rescorer_destroy",
-           "nmt_debug_alloc_hook", "nmt_debug_gemm_form", "nmt_debug_gemm_streamed")
+           "nmt_debug_alloc_hook", "nmt_debug_gemm_form", "nmt_debug_gemm_streamed", "nmt_debug_precompute")
 
 PHASES = ("gru1", "query", "attention", "gru2", "readout", "vocab", "combine")
 
@@ -121,6 +121,8 @@ def load_library(path: str = LIB_PATH):
     lib.nmt_debug_gemm_form.restype = _I32
     lib.nmt_debug_gemm_streamed.argtypes = []
     lib.nmt_debug_gemm_streamed.restype = ctypes.c_int64
+    lib.nmt_debug_precompute.argtypes = [_I32]
+    lib.nmt_debug_precompute.restype = _I32
     lib.nmt_last_error.argtypes = []
     lib.nmt_last_error.restype = ctypes.c_char_p
     for f in ("nmt_model_create", "nmt_encode", "nmt_source_from_annotations", "nmt_source_info",
@@ -151,6 +153,14 @@ def debug_gemm_form(form: int) -> int:
 def debug_gemm_streamed() -> int:
     """Test hook (nmt_debug.h): launches so far that streamed weights."""
     return int(load_library().nmt_debug_gemm_streamed())
+
+
+def debug_precompute(on: int) -> int:
+    """Test hook (nmt_debug.h): whether fp32 models created from now on
+    take the previous word's and the context's products from precomputed
+    tables and projections (1, the default) or compute them per step (0);
+    returns the previous setting."""
+    return int(load_library().nmt_debug_precompute(on))
 
 
 def last_error() -> str:

@@ -29,6 +29,7 @@ thread_local std::string g_err;
 // failures (-1: none), and the library's live device allocations.
 std::atomic<int64_t> g_alloc_budget{-1};
 std::atomic<int64_t> g_live_allocs{0};
+std::atomic<int32_t> g_precompute{1};  // nmt_debug_precompute
 
 nmt_status fail(nmt_status st, const char* fmt, ...) {
   char buf[512];
@@ -526,6 +527,11 @@ int32_t nmt_debug_gemm_form(int32_t form) {
 
 int64_t nmt_debug_gemm_streamed(void) { return nmt::g_gemm_streamed.load(); }
 
+int32_t nmt_debug_precompute(int32_t on) {
+  if (on != 0 && on != 1) return -1;
+  return g_precompute.exchange(on);
+}
+
 const char* nmt_last_error(void) { return g_err.c_str(); }
 
 nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_model** out) {
@@ -591,7 +597,7 @@ nmt_status nmt_model_create(const nmt_dims* dims, const nmt_weights* w, nmt_mode
   step(upload(m->mem, &m->att_b, w->att_b, A));
   if (e == hipSuccess) step(pack_plain(m->mem, &m->init_W, {{w->init_W, C, H}}, H, kPlainSmallTN, kc, bf16));
   step(upload(m->mem, &m->init_b, w->init_b, H));
-  m->precomp = !bf16;
+  m->precomp = !bf16 && g_precompute.load() != 0;
   if (m->precomp) {
     if (e == hipSuccess) step(pack_gru(m->mem, &m->g1, {{w->g1_U, H, 3 * H}}, H, kc, bf16));
     if (e == hipSuccess) step(pack_plain(m->mem, &m->g1x, {{w->g1_W, E, 3 * H}}, 3 * H, kPlainLargeTN, kc, bf16));

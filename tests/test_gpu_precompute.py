@@ -1,0 +1,76 @@
+"""The two forms of the fp32 decoder step (Section 5.1) on the same weights.
+
+With fp32 weights a model takes the previous word's products with the first
+GRU's input weights and the readout's word weights from per-word tables, and
+the context's products with the second GRU's input weights and the readout's
+context weights from per-position projections of the annotations mixed by
+the attention weights (the test switch nmt_debug_precompute(0) makes a model
+that computes all four in the step's GEMMs instead).  Both forms must match
+the oracle on every row, and each other to within the reassociation of fp32
+sums (products summed over C per position and then mixed, instead of mixed
+and then summed): TOL_FORMS below, well above the few 1e-6 that fp32
+rounding of sums of a few thousand O(1) terms gives, and well below the
+1e-4 that the high-signal oracle bars allow.
+"""
+import numpy as np
+import pytest
+
+from paper_1605_04809_amd.workloads import CONFIGS, high_signal, make_workload, random_annotations, unit_gain
+from tests.parity_cases import ATT, ATT_CASES, PAPER_SIGNAL
+
+pytestmark = pytest.mark.gpu
+
+TOL_LOGP = 1e-4
+TOL_INTER_HS = 1e-4
+TOL_FORMS = 2e-5
+KEYS = ("logp", "logZ", "s1", "s_new", "c", "t", "alpha")
+
+
+def _torch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+CASES = {
+    "tiny_high_signal": lambda: (make_workload(high_signal(CONFIGS["tiny"]).replace(B=70)), None),
+    "att1024_g4": lambda: (unit_gain(ATT.replace(**ATT_CASES["g4_16w"])),
+                           random_annotations(ATT.replace(**ATT_CASES["g4_16w"]), seed=91)),
+    "paper_signal": lambda: (unit_gain(PAPER_SIGNAL), random_annotations(PAPER_SIGNAL, seed=92)),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_precomputed_products_equal_the_step_gemms(case):
+    _torch()
+    from tests import gpu_cases
+    from paper_1605_04809_amd import binding as nb
+    wl, ctx = CASES[case]()
+    assert wl.cfg.wtype == "f32"
+    wl.y_prev[::9] = -1  # sentence starts: the tables' zero rows
+    g_on = gpu_cases.GpuRun(wl, ctx_f32=ctx)
+    prev = nb.debug_precompute(0)
+    try:
+        g_off = gpu_cases.GpuRun(wl, ctx_f32=ctx)
+    finally:
+        nb.debug_precompute(prev)
+    B = len(wl.y_prev)
+    # the precomputing form's workspace holds the attention's 3H + E mixed
+    # columns per row (padded) instead of the 2H-wide context
+    assert nb.nmt_score_workspace_bytes(g_on.model, B) > nb.nmt_score_workspace_bytes(g_off.model, B)
+    args = (wl.s_prev, wl.y_prev, wl.sent_id, wl.req)
+    on, off = g_on.step(*args), g_off.step(*args)
+    ref = gpu_cases.OracleRun(wl, ctx_f32=ctx).step(*args)
+    for name, res in (("precomputed", on), ("in the step", off)):
+        errs = {k: gpu_cases.max_abs(res[k], ref[k]) for k in KEYS}
+        print(f"{case} {name}: max |gpu - oracle|", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+        assert errs["logp"] <= TOL_LOGP and errs["logZ"] <= TOL_LOGP, errs
+        for k in ("s1", "s_new", "c", "t", "alpha"):
+            assert errs[k] <= TOL_INTER_HS, (k, errs)
+    d = {k: gpu_cases.max_abs(on[k], off[k]) for k in KEYS}
+    print(f"{case}: max |precomputed - in the step|", {k: f"{v:.2e}" for k, v in d.items()}, flush=True)
+    for k in KEYS:
+        assert d[k] <= TOL_FORMS, (k, d)
+    g_on.close()
+    g_off.close()
