@@ -357,7 +357,8 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * d.A * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus);
+  L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus,
+                      vocab_tm((int)B, m->bf16, m->out.Kpad, m->dims.E, m->out.nbias));
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
   // The query GEMM splits its K only where its tiles leave at least half the

@@ -155,7 +155,8 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
                                  int part_M, int tm, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
-int vocab_slices(int M, int V, bool bf16, int cus);
+int vocab_tm(int M, bool bf16, int64_t Kpad, int E, int nb);
+int vocab_slices(int M, int V, bool bf16, int cus, int tm);
 int vocab_max_kpad(bool bf16);
 bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
 // Row stride of a bf16 copy of rows E wide: whole 16-byte vectors.

@@ -1153,7 +1153,7 @@ struct VocabTune {
 // or bias row reaches it: fp32 with E + nb <= Kpad - 8), so its MFMAs, which
 // would only add zeros, are skipped; its loads stay, keeping the ring's
 // schedule.  With E = 500 that is 1 of 64 k groups.
-template <class P, int VPF, bool PAD_LAST = false>
+template <class P, int VPF, bool PAD_LAST = false, int VTM_ = VocabTune<P>::VTM>
 __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const float* __restrict__ t, int t16, int M, int E,
                                                                       int nb, int Kpad, const f32x4* __restrict__ Wp,
                                                                       int64_t Npad, int V, int nM, int nS,
@@ -1161,7 +1161,7 @@ __global__ __launch_bounds__(VocabTune<P>::VNW * 64) void k_vocab_lse(const floa
                                                                       const int32_t* __restrict__ req1,
                                                                       const int32_t* __restrict__ req_off, int nreq,
                                                                       float* __restrict__ zreq) {
-  constexpr int VTM = VocabTune<P>::VTM, VNW = VocabTune<P>::VNW, VFN = VocabTune<P>::VFN;
+  constexpr int VTM = VTM_, VNW = VocabTune<P>::VNW, VFN = VocabTune<P>::VFN;
   constexpr int FM = VTM / 32;
   __shared__ f32x4 As[VQMAX];
   __shared__ float2 red[VNW][VTM];
@@ -1453,14 +1453,30 @@ constexpr int kVocabBlockFixed = 4;
 static_assert(VocabTune<PrecF32>::VTM % 32 == 0 && VocabTune<PrecBF16>::VTM % 32 == 0 && kPlainSmallTM % 32 == 0,
               "row tiles in whole multiples of 32");
 constexpr int kVocabMaxSlices = 256;
-int vocab_slices(int M, int V, bool bf16, int cus) {
-  const int nM = ceil_div(M, bf16 ? VocabTune<PrecBF16>::VTM : VocabTune<PrecF32>::VTM);
+// Small fp32 batches (the levels of a forest, the shrinking phrase loop) take
+// row tiles of 32: a launch's blocks then split the rows finer, so the
+// SIMDs of a block end closer together (a block's groups per SIMD are whole
+// 32 x 32 tiles instead of 64 x 32 ones) and the row padding shrinks; each
+// weight fragment then feeds half the MFMAs, so 32 k groups stay in flight.
+// Taken with the deepest prefetch and a skipped padding k group (the paper's
+// E = 500), the one instantiation this form has.
+constexpr int kVocabSmallM = 768, kVocabSmallTM = 32, kVocabSmallVPF = 32;
+int vocab_tm(int M, bool bf16, int64_t Kpad, int E, int nb) {
+  if (bf16) return VocabTune<PrecBF16>::VTM;
+  const int64_t nkg = Kpad / (2 * PrecF32::KV);
+  const bool fits = nkg % kVocabSmallVPF == 0 && nkg >= 2 * kVocabSmallVPF && E + nb <= Kpad - 2 * PrecF32::KV;
+  return M <= kVocabSmallM && fits ? kVocabSmallTM : VocabTune<PrecF32>::VTM;
+}
+int vocab_slices(int M, int V, bool bf16, int cus, int tm) {
+  const int nM = ceil_div(M, tm);
   const int NB = (V + 31) / 32;
+  // a block's fixed costs, in the time of one of its column blocks
+  const double fixed = tm < 64 ? 2.0 * kVocabBlockFixed : kVocabBlockFixed;
   int best = 8;
   double best_cost = 0;
   for (int nS = 8; nS <= kVocabMaxSlices && (nS == 8 || nS <= NB); nS += 8) {
     const double rounds = (double)ceil_div((int64_t)nM * nS, cus);
-    const double cost = rounds * ((double)NB / nS + kVocabBlockFixed);
+    const double cost = rounds * ((double)NB / nS + fixed);
     if (nS == 8 || cost < best_cost) {
       best_cost = cost;
       best = nS;
@@ -1482,9 +1498,18 @@ template <class P>
 hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
                      const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
+  const f32x4* Wp = (const f32x4*)W.d;
+  if constexpr (!P::kBF16) {
+    if (vocab_tm(M, false, W.Kpad, E, W.nbias) == kVocabSmallTM) {
+      const int nM = ceil_div(M, kVocabSmallTM);
+      hipLaunchKernelGGL((k_vocab_lse<P, kVocabSmallVPF, true, kVocabSmallTM>), dim3((unsigned)(nS / 8 * 8 * nM)),
+                         dim3(VocabTune<P>::VNW * 64), 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM,
+                         nS, part, req1, req_off, nreq, zreq);
+      return hipGetLastError();
+    }
+  }
   const int nM = ceil_div(M, VocabTune<P>::VTM);
   dim3 grid((unsigned)(nS / 8 * 8 * nM)), block(VocabTune<P>::VNW * 64);
-  const f32x4* Wp = (const f32x4*)W.d;
   constexpr int PF = VocabTune<P>::VPF_MAX;
   // the deepest prefetch that divides the k groups into at least two blocks
   auto fits = [&](int vpf) { return PF >= vpf && nkg % vpf == 0 && nkg >= 2 * vpf; };

@@ -415,11 +415,14 @@ def test_paper_sized_step_every_row(gpu, name):
     g.close()
 
 
-@pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "bf16"), (1000, "bf16")])
+@pytest.mark.parametrize("B,wtype", [(2600, "f32"), (1445, "f32"), (667, "f32"), (33, "f32"), (667, "bf16"),
+                                     (1000, "bf16")])
 def test_launch_shape_boundaries_every_row(gpu, B, wtype):
     """Batches between the tile choices at the paper's dimensions: B = 2600
     takes the 64-row GRU tile with more than a round of 128-row blocks
     (fp32), B = 1445 takes 32 vocabulary slices over 23 row tiles, B = 667
+    and 33 (fp32) the vocabulary kernel's 32-row tiles of small batches (21
+    tiles and a ragged last one; two tiles, the second with one row), B = 667
     (bf16) 64-row GRU blocks split over K and 40 slices, B = 1000 (bf16)
     128-row GRU blocks split over K in two; every row."""
     _torch()
