@@ -336,7 +336,7 @@ int plain_ksplit(int M, int N, int K_total, int kc, Tile t, int cus) {
 // reuse that region, extended if they need more.
 struct WsLayout {
   size_t s1, s1h, c, q, t, part, kpart, perm, tiles, ntiles, zreq, gpart, total;
-  int nS;             // vocabulary slices
+  int nS, vtm;        // vocabulary slices and row tile
   int ks_q, ks_ro;    // K splits of the query and readout GEMMs
   int ks_g1, ks_g2;   // K splits of the two GRUs (1: fused cell, no partials)
 };
@@ -357,8 +357,8 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   off += al((size_t)B * d.A * 4);
   L.t = off;
   off += al((size_t)B * d.E * 4);
-  L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus,
-                      vocab_tm((int)B, m->bf16, m->out.Kpad, m->dims.E, m->out.nbias));
+  L.vtm = vocab_tm((int)B, m->dims.V, m->bf16, m->out.Kpad, m->dims.E, m->out.nbias, m->cus);
+  L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus, L.vtm);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
   // The query GEMM splits its K only where its tiles leave at least half the
@@ -957,7 +957,7 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   // rows with one request: the vocabulary kernel also picks out its logit
   float* zreq = rq.req ? (float*)(ws + L.zreq) : nullptr;
   if (e == hipSuccess)
-    e = launch_vocab_lse(t, m->bf16, B, E, m->out, V, part, L.nS, rq.req, rq.req_off, rq.nreq, zreq, st);
+    e = launch_vocab_lse(t, m->bf16, B, E, m->out, V, part, L.nS, L.vtm, rq.req, rq.req_off, rq.nreq, zreq, st);
   mark(NMT_PHASE_VOCAB + 1);
   if (e == hipSuccess)
     e = launch_lse_combine(B, part, L.nS, t, m->bf16, E, m->out, V, rq, d_y_prev, d_sent_id, src->S, d_logp, d_logZ,

@@ -155,7 +155,7 @@ hipError_t launch_gemm_gru_split(const GruProblem* probs, int nprob, int H, bool
                                  int part_M, int tm, hipStream_t st);
 // Number of vocabulary slices (partials per row) for M rows, and the
 // largest padded E the vocabulary kernel keeps in LDS.
-int vocab_tm(int M, bool bf16, int64_t Kpad, int E, int nb);
+int vocab_tm(int M, int V, bool bf16, int64_t Kpad, int E, int nb, int cus);
 int vocab_slices(int M, int V, bool bf16, int cus, int tm);
 int vocab_max_kpad(bool bf16);
 bool vocab_offsets_fit(int64_t Kpad, int64_t Npad, bool bf16);
@@ -166,9 +166,11 @@ inline __host__ __device__ int bf16_row(int E) { return (E + 7) / 8 * 8; }
 // req1 (nullable): the requested words, one per row (req_off NULL) or CSR
 // (req_off [M+1] over nreq words); the logit of each row that requests
 // exactly one word goes to zreq [M] (rows whose word is outside [0, V), or
-// whose span is malformed, get nothing written).
+// whose span is malformed, get nothing written).  nS and tm: the slices and
+// the row tile chosen for M rows by vocab_slices and vocab_tm.
 hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
-                            const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st);
+                            int tm, const int32_t* req1, const int32_t* req_off, int nreq, float* zreq,
+                            hipStream_t st);
 // Requests of row b: req[req_off[b] .. req_off[b+1]) with logp at the same
 // indices (req_off nullable: one request per row, req[b] -> logp[b]).  The
 // combine takes the logits of rows with one request from zreq (the

@@ -1453,20 +1453,26 @@ constexpr int kVocabBlockFixed = 4;
 static_assert(VocabTune<PrecF32>::VTM % 32 == 0 && VocabTune<PrecBF16>::VTM % 32 == 0 && kPlainSmallTM % 32 == 0,
               "row tiles in whole multiples of 32");
 constexpr int kVocabMaxSlices = 256;
-// Small fp32 batches (the levels of a forest, the shrinking phrase loop) take
-// row tiles of 32: a launch's blocks then split the rows finer, so the
-// SIMDs of a block end closer together (a block's groups per SIMD are whole
-// 32 x 32 tiles instead of 64 x 32 ones) and the row padding shrinks; each
-// weight fragment then feeds half the MFMAs, so 32 k groups stay in flight.
-// Taken with the deepest prefetch and a skipped padding k group (the paper's
-// E = 500), the one instantiation this form has.
+// Small fp32 batches (the levels of a forest, the shrinking phrase loop) may
+// take row tiles of 32: the launch's blocks then split the rows finer, so the
+// SIMDs of a block end closer together (a SIMD's share of a block is whole
+// 32 x 32 groups instead of 64 x 32 ones) and less row padding is computed;
+// each weight fragment feeds half the MFMAs, so 32 k groups stay in flight.
+// That form exists for the deepest prefetch with a skipped padding k group
+// (the paper's E = 500), its one instantiation.
 constexpr int kVocabSmallM = 768, kVocabSmallTM = 32, kVocabSmallVPF = 32;
-int vocab_tm(int M, bool bf16, int64_t Kpad, int E, int nb) {
-  if (bf16) return VocabTune<PrecBF16>::VTM;
-  const int64_t nkg = Kpad / (2 * PrecF32::KV);
-  const bool fits = nkg % kVocabSmallVPF == 0 && nkg >= 2 * kVocabSmallVPF && E + nb <= Kpad - 2 * PrecF32::KV;
-  return M <= kVocabSmallM && fits ? kVocabSmallTM : VocabTune<PrecF32>::VTM;
+
+// Launch time of nM row tiles in nS slices, in the time of one column block
+// of the tile: rounds of one block per CU, each as long as one block.  With
+// by_simd a block lasts as long as its busiest SIMD's whole groups (four
+// SIMDs share a block's groups); otherwise its share of the columns, the
+// model the 64-row tiles' slice counts were chosen and measured by.
+static double vocab_cost(int nM, int nS, int NB, int cus, double fixed, bool by_simd) {
+  const double rounds = (double)ceil_div((int64_t)nM * nS, cus);
+  const double block = by_simd ? 4.0 * ceil_div(ceil_div(NB, nS), 4) : (double)NB / nS;
+  return rounds * (block + fixed);
 }
+
 int vocab_slices(int M, int V, bool bf16, int cus, int tm) {
   const int nM = ceil_div(M, tm);
   const int NB = (V + 31) / 32;
@@ -1475,14 +1481,31 @@ int vocab_slices(int M, int V, bool bf16, int cus, int tm) {
   int best = 8;
   double best_cost = 0;
   for (int nS = 8; nS <= kVocabMaxSlices && (nS == 8 || nS <= NB); nS += 8) {
-    const double rounds = (double)ceil_div((int64_t)nM * nS, cus);
-    const double cost = rounds * ((double)NB / nS + fixed);
+    const double cost = vocab_cost(nM, nS, NB, cus, fixed, tm < 64);
     if (nS == 8 || cost < best_cost) {
       best_cost = cost;
       best = nS;
     }
   }
   return best;
+}
+
+// The row tile of a launch: 32 where that form exists and the launch's
+// time by whole groups per SIMD beats the 64-row tile's (in equal units;
+// measured on the phrase loop's levels: 500, 232 and 125 rows 2-8 % faster,
+// 364 rows slower, as this predicts).
+int vocab_tm(int M, int V, bool bf16, int64_t Kpad, int E, int nb, int cus) {
+  if (bf16) return VocabTune<PrecBF16>::VTM;
+  constexpr int TM = VocabTune<PrecF32>::VTM;
+  const int64_t nkg = Kpad / (2 * PrecF32::KV);
+  const bool fits = nkg % kVocabSmallVPF == 0 && nkg >= 2 * kVocabSmallVPF && E + nb <= Kpad - 2 * PrecF32::KV;
+  if (M > kVocabSmallM || !fits) return TM;
+  const int NB = (V + 31) / 32;
+  const double small = vocab_cost(ceil_div(M, kVocabSmallTM), vocab_slices(M, V, false, cus, kVocabSmallTM), NB,
+                                  cus, 2.0 * kVocabBlockFixed, true);
+  const double large = (double)TM / kVocabSmallTM *
+                       vocab_cost(ceil_div(M, TM), vocab_slices(M, V, false, cus, TM), NB, cus, kVocabBlockFixed, true);
+  return small < large ? kVocabSmallTM : TM;
 }
 
 // The vocabulary kernel addresses the packed weights with 32-bit byte offsets.
@@ -1495,12 +1518,12 @@ int vocab_max_kpad(bool bf16) {
 }
 
 template <class P>
-hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
+hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS, int tm,
                      const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st) {
   const int nkg = (int)(W.Kpad / (2 * P::KV));
   const f32x4* Wp = (const f32x4*)W.d;
   if constexpr (!P::kBF16) {
-    if (vocab_tm(M, false, W.Kpad, E, W.nbias) == kVocabSmallTM) {
+    if (tm == kVocabSmallTM) {
       const int nM = ceil_div(M, kVocabSmallTM);
       hipLaunchKernelGGL((k_vocab_lse<P, kVocabSmallVPF, true, kVocabSmallTM>), dim3((unsigned)(nS / 8 * 8 * nM)),
                          dim3(VocabTune<P>::VNW * 64), 0, st, t, t16, M, E, W.nbias, (int)W.Kpad, Wp, W.Npad, V, nM,
@@ -1536,15 +1559,21 @@ hipError_t vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int
 }
 
 hipError_t launch_vocab_lse(const float* t, int t16, int M, int E, const Packed& W, int V, float2* part, int nS,
-                            const int32_t* req1, const int32_t* req_off, int nreq, float* zreq, hipStream_t st) {
+                            int tm, const int32_t* req1, const int32_t* req_off, int nreq, float* zreq,
+                            hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (t16 && !W.bf16) return hipErrorInvalidValue;
+  // the small tile only where its form exists (see vocab_tm)
+  const int64_t nkg = W.Kpad / (2 * (W.bf16 ? PrecBF16::KV : PrecF32::KV));
+  if (tm == kVocabSmallTM && (W.bf16 || nkg % kVocabSmallVPF || nkg < 2 * kVocabSmallVPF ||
+                              E + W.nbias > W.Kpad - 2 * PrecF32::KV))
+    return hipErrorInvalidValue;
   if (W.Kpad > vocab_max_kpad(W.bf16) || W.Krows != E || W.nbias < 1 || W.Npad < ((int64_t)V + 31) / 32 * 32 + 32)
     return hipErrorInvalidValue;
   if (!vocab_offsets_fit(W.Kpad, W.Npad, W.bf16)) return hipErrorInvalidValue;
   if (req1 && !zreq) return hipErrorInvalidValue;
-  return W.bf16 ? vocab_lse<PrecBF16>(t, t16, M, E, W, V, part, nS, req1, req_off, nreq, zreq, st)
-                : vocab_lse<PrecF32>(t, 0, M, E, W, V, part, nS, req1, req_off, nreq, zreq, st);
+  return W.bf16 ? vocab_lse<PrecBF16>(t, t16, M, E, W, V, part, nS, tm, req1, req_off, nreq, zreq, st)
+                : vocab_lse<PrecF32>(t, 0, M, E, W, V, part, nS, tm, req1, req_off, nreq, zreq, st);
 }
 
 // ---------------------------------------------------- partials combine
