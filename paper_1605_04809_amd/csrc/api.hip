@@ -814,6 +814,11 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   const WsLayout L = ws_layout(m, B);
   if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < L.total) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
+  // a model that mixes the annotations' projections needs a source set up by
+  // a model of the same form (nmt_encode or nmt_source_from_annotations)
+  if (m->precomp != (src->cproj != nullptr))
+    return fail(NMT_EINVAL, "the source was set up for a model %s the annotations' projections",
+                src->cproj ? "with" : "without");
   nmt_status rc = check_device(m);
   if (rc != NMT_OK) return rc;
 

@@ -74,3 +74,30 @@ def test_precomputed_products_equal_the_step_gemms(case):
         assert d[k] <= TOL_FORMS, (k, d)
     g_on.close()
     g_off.close()
+
+
+def test_source_of_the_other_form_is_refused():
+    """A source holds the annotations' projections only when a precomputing
+    model set it up; the step refuses a source of the other form (nothing is
+    enqueued) instead of reading projections that are not there."""
+    torch = _torch()
+    from tests import gpu_cases
+    from paper_1605_04809_amd import binding as nb
+    wl = make_workload(CONFIGS["tiny"].replace(B=16))
+    g_on = gpu_cases.GpuRun(wl)
+    prev = nb.debug_precompute(0)
+    try:
+        g_off = gpu_cases.GpuRun(wl)
+    finally:
+        nb.debug_precompute(prev)
+    cu = gpu_cases.cuda
+    B, H = len(wl.y_prev), wl.cfg.H
+    for model, src in ((g_on.model, g_off.src), (g_off.model, g_on.src)):
+        logp, s_new = torch.empty(B, device="cuda"), torch.empty((B, H), device="cuda")
+        with pytest.raises(nb.NmtError) as ex:
+            nb.nmt_score_batch(model, src, cu(wl.s_prev), cu(wl.y_prev), cu(wl.sent_id), cu(wl.req), logp, s_new)
+        assert ex.value.status == nb.NMT_EINVAL
+    torch.cuda.synchronize()
+    assert nb.nmt_stream_status(g_on.model) == nb.NMT_OK
+    g_on.close()
+    g_off.close()
