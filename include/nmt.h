@@ -169,9 +169,10 @@ size_t nmt_score_workspace_bytes(const nmt_model* m, int32_t B);
  * ids out of range set the model's device error flag and give that row
  * logp = NaN (see nmt_stream_status).  Calls on different streams must use
  * different workspaces.  The source must come from nmt_encode or
- * nmt_source_from_annotations on this model (a source of a model that
- * differs in whether it precomputes the context's products gives
- * NMT_EINVAL).  Errors: NMT_EINVAL, NMT_EWORKSPACE, NMT_EDEVICE. */
+ * nmt_source_from_annotations on this model (a source of a model with other
+ * widths H or A, or that differs in whether it precomputes the context's
+ * products, gives NMT_EINVAL).  Errors: NMT_EINVAL, NMT_EWORKSPACE,
+ * NMT_EDEVICE. */
 nmt_status nmt_score_batch(nmt_model* m, const nmt_source* src, int32_t B, const float* d_s_prev,
                            const int32_t* d_y_prev, const int32_t* d_sent_id, const int32_t* d_req,
                            float* d_logp, float* d_s_new, float* d_logZ, void* d_workspace,

@@ -117,6 +117,7 @@ struct nmt_model {
 
 struct nmt_source {
   int32_t S = 0, Tpad = 0;
+  int32_t H = 0, A = 0, cpw_ld = 0;  // the widths of the model that set it up
   Allocs mem;
   float *ctx = nullptr, *pctx = nullptr, *scratch = nullptr;
   float* kfac = nullptr;  // 2^{2 log2(e) pctx}: the keys' factors of the attention scores
@@ -421,6 +422,9 @@ nmt_status new_source(nmt_model* m, int32_t S, int32_t Tpad, const int32_t* h_le
   nmt_source* src = new nmt_source();
   src->S = S;
   src->Tpad = Tpad;
+  src->H = d.H;
+  src->A = d.A;
+  src->cpw_ld = m->precomp ? m->cpw_ld : 0;
   src->h_len.assign(h_len, h_len + S);
   const size_t rows = (size_t)S * Tpad;
   hipError_t e = src->mem.alloc((void**)&src->ctx, rows * 2 * d.H * sizeof(float));
@@ -814,9 +818,12 @@ nmt_status score_step(nmt_model* m, const nmt_source* src, int32_t B, const floa
   const WsLayout L = ws_layout(m, B);
   if (!d_workspace || ((uintptr_t)d_workspace & 255)) return fail(NMT_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < L.total) return fail(NMT_EWORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
-  // a model that mixes the annotations' projections needs a source set up by
-  // a model of the same form (nmt_encode or nmt_source_from_annotations)
-  if (m->precomp != (src->cproj != nullptr))
+  // the source's arrays have the widths of the model that set it up, and
+  // hold the annotations' projections only for a model that mixes them
+  if (src->H != m->dims.H || src->A != m->dims.A)
+    return fail(NMT_EINVAL, "the source was set up for a model with H = %d, A = %d (this one: %d, %d)", src->H,
+                src->A, m->dims.H, m->dims.A);
+  if (m->precomp != (src->cproj != nullptr) || src->cpw_ld != (m->precomp ? m->cpw_ld : 0))
     return fail(NMT_EINVAL, "the source was set up for a model %s the annotations' projections",
                 src->cproj ? "with" : "without");
   nmt_status rc = check_device(m);
