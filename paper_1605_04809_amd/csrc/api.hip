@@ -362,11 +362,14 @@ WsLayout ws_layout(const nmt_model* m, int64_t B) {
   L.nS = vocab_slices((int)B, m->dims.V, m->bf16, m->cus, L.vtm);
   L.part = off;
   off += al((size_t)B * L.nS * sizeof(float2));
-  // The query GEMM splits its K only where its tiles leave at least half the
-  // CUs idle (the shrinking batches of a forest or phrase loop); at B = 1000
-  // (256 tiles) a split measured slower (28 -> 32 us).
+  // The query GEMM splits its K where its tiles fit in one round of the CUs
+  // (a forest's levels, the phrase loop, B = 1000 at A = 1024), the attention
+  // adding the split sums as it loads the query: ruen_b1000 query 27.1 ->
+  // 23.1 us, attention +0.4 us (with a reduction kernel of its own, the
+  // split had measured slower there, 28 -> 32 us).  At 512 tiles (B = 2000)
+  // a split of two measured even.
   const int tiles_q = ceil_div(B, kPlainSmallTM) * ceil_div(d.A, kPlainSmallTN);
-  L.ks_q = tiles_q <= m->cus / 2 ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->cus) : 1;
+  L.ks_q = tiles_q <= m->cus ? plain_ksplit((int)B, d.A, d.H, m->kc, Tile::Small, m->cus) : 1;
 
   L.ks_ro = plain_ksplit((int)B, d.E, d.H + (m->precomp ? 0 : d.E + 2 * d.H), m->kc, Tile::Small, m->cus);
   size_t kp = 0;
